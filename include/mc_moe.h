@@ -1,0 +1,165 @@
+/*
+ * mc_moe.h -- C-ABI of the Mixture Compressor (MC) MoE expert path on gfx950.
+ *
+ * The paper (Mixture Compressor for MoE LLMs, ICLR 2025) stores every expert
+ * at its own 1-, 2- or 3-bit width (Sec. 3.2, Eq. 4 chooses the widths) with
+ * asymmetric, group-wise uniform quantization (Sec. 3.1), and at inference
+ * prunes a token's low-weight experts unless the token is marked important
+ * (Sec. 3.3, Eq. 5 and the token-protection rule).  This library runs that
+ * inference path:
+ *
+ *   mc_pack            fp32 expert weights -> packed codes + fp16 scale/zero
+ *   mc_route_and_prune router logits -> top-k, Eq. 5 pruning, protection,
+ *                      per-expert token lists (CSR)
+ *   mc_moe_forward     Eq. 1 over the packed SwiGLU experts
+ *
+ * Conventions for every call
+ *   - Pointers are DEVICE pointers unless the comment says "host".
+ *   - Every call that takes `stream` (a hipStream_t; NULL = legacy default
+ *     stream) is asynchronous: it enqueues kernels and returns.
+ *   - The library never allocates device memory.  The caller owns every
+ *     buffer; sizes come from mc_pack_sizes / mc_forward_workspace.
+ *   - Arguments are validated on the host before anything is enqueued.  On any
+ *     status other than MC_OK nothing was enqueued (MC_EHIP: a launch failed;
+ *     earlier launches of the same call may have been enqueued) and
+ *     mc_last_error() describes the problem.
+ *   - Shape limits: 1 <= E <= 256 experts, 1 <= k <= min(E, 8), d and ffn
+ *     multiples of 128, group size G one of 32, 64, 128 or a multiple of 128,
+ *     dividing both d and ffn.
+ *
+ * Packed layout (normative; used by every kernel).  A matrix with R output
+ * rows and K input columns (row-major W[R][K], the reduction runs over K) at
+ * b bits is cut into tiles of 16 rows x 128 columns.  Column k of row n lives
+ * in tile (n/16, k/128) at lane l = (n%16) + 16*kq, with kk = k%128,
+ * u = kk/32, kq = (kk%32)/8, j = kk%8, pair i = 4u + j/2 and half
+ * h = j%2 (0: bits 0..15, 1: bits 16..31).  Each lane owns b consecutive
+ * 32-bit words starting at word ((tile_row*(K/128) + tile_col)*64 + l)*b:
+ *   b = 1: bit 16h + i of word 0;
+ *   b = 2: bits 16h + 2(i%8) .. +1 of word i/8;
+ *   b = 3: i < 15: bits 16h + 3(i%5) .. +2 of word i/5;
+ *          i = 15: bit p of the code sits at bit 16h + 15 of word p.
+ * Scale and zero of group g of row n form one 32-bit word (fp16 scale in
+ * bits 0..15, fp16 zero in bits 16..31) at index ((n/16)*(K/G) + g)*16 + n%16.
+ * A layer holds, expert after expert, the gate [ffn][d], up [ffn][d] and
+ * down [d][ffn] matrices in that order, each with its expert's width; the
+ * scale/zero words follow the same order.
+ */
+#ifndef MC_MOE_H
+#define MC_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MC_MAX_EXPERTS 256
+#define MC_MAX_TOPK 8
+
+typedef enum mc_status {
+  MC_OK = 0,
+  MC_EINVAL = 1,        /* bad argument (shape, null pointer, bit-width, threshold) */
+  MC_ENOSPACE = 2,      /* a caller buffer is smaller than required */
+  MC_EHIP = 3,          /* the HIP runtime reported an error */
+  MC_EUNSUPPORTED = 4   /* valid in principle, not supported by this build */
+} mc_status;
+
+/* Descriptor of one packed MoE layer; it only references caller memory. */
+typedef struct mc_layer {
+  int E;                 /* number of experts */
+  int d;                 /* hidden size (input of gate/up, output of down) */
+  int ffn;               /* expert intermediate size */
+  int group;             /* quantization group size G along the input dim */
+  const int *bits_host;  /* host [E]; expert e is stored at bits_host[e] in {1,2,3} */
+  void *words;           /* device; packed codes, words_bytes long */
+  uint32_t *sz;          /* device; scale/zero words, sz_bytes long */
+  size_t words_bytes;
+  size_t sz_bytes;
+} mc_layer;
+
+/* Bytes needed for the packed codes and the scale/zero words of a layer.
+ * codes: sum over experts of 3*d*ffn*bits/8;  scale/zero: 3*E*d*ffn/G*4.
+ * Pure host computation.  Errors: MC_EINVAL on a shape or width outside the
+ * limits above or a null pointer. */
+mc_status mc_pack_sizes(int E, int d, int ffn, const int *bits_host, int group,
+                        size_t *words_bytes, size_t *sz_bytes);
+
+/* Quantize and pack all experts of a layer (Sec. 3.1: uniform asymmetric
+ * group-wise quantizer; the widths come from the PMQ allocation of Eq. 4).
+ * For each group of G consecutive inputs of one row, with L = 2^b - 1:
+ *   s = fp16(fp32(fp32(max - min) / L)), replaced by 1 if it rounds to 0;
+ *   z = fp16(fp32(-min / s)), a -0 zero is stored as +0;
+ *   code q = the j in [0, L] whose level s*(j - z) is nearest to w, ties to
+ *   even j (decided exactly);
+ * fp16() is round-to-nearest-even, saturating to +-65504.
+ * w_gate, w_up: [E][ffn][d] fp32; w_down: [E][d][ffn] fp32; all weights must
+ * be finite.  L->words / L->sz receive the layout described above.
+ * Errors: MC_EINVAL (shape/width/null), MC_ENOSPACE (L->words_bytes or
+ * L->sz_bytes smaller than mc_pack_sizes), MC_EHIP. */
+mc_status mc_pack(const float *w_gate, const float *w_up, const float *w_down,
+                  const mc_layer *L, void *stream);
+
+/* Test surface: write the dequantized matrix `mat` (0 gate, 1 up, 2 down) of
+ * expert e as row-major fp16 [R][K]; each value is the round-to-nearest-even
+ * fp16 of the exact product s*(q - z) (one rounding).  out must hold R*K
+ * halves.  Errors: MC_EINVAL, MC_EHIP. */
+mc_status mc_dequant_export(const mc_layer *L, int e, int mat, uint16_t *out,
+                            void *stream);
+
+/* Test surface: write the integer codes of matrix `mat` of expert e as
+ * row-major uint8 [R][K].  Errors: MC_EINVAL, MC_EHIP. */
+mc_status mc_codes_export(const mc_layer *L, int e, int mat, uint8_t *out,
+                          void *stream);
+
+/* Routing result, device-resident; the host ints give its shape. */
+typedef struct mc_routing {
+  int T, E, k;           /* host: tokens, experts, experts per token */
+  int32_t *topk_idx;     /* [T][k] rank r's expert: logits in descending order,
+                            equal logits ordered by lower expert index */
+  float *topk_w;         /* [T][k] combine weight of rank r after pruning
+                            (softmax over the kept ranks), 0 when dropped */
+  uint8_t *kept;         /* [T][k] 1 when (t, r) is computed, 0 when pruned */
+  int32_t *counts;       /* [E] kept pairs per expert */
+  int32_t *offsets;      /* [E+1] exclusive scan of counts */
+  int32_t *pair_token;   /* [T*k]; entries offsets[e]..offsets[e+1]-1 list the
+                            tokens routed to e in ascending order */
+  int32_t *pair_rank;    /* [T*k] the rank r of each listed pair */
+  float *pair_w;         /* [T*k] its combine weight */
+  int32_t *pair_pos;     /* [T][k] list position of (t, r), -1 when pruned */
+  int32_t *n_pruned;     /* [1] number of pruned pairs */
+} mc_routing;
+
+/* Top-k routing with Online Dynamic Pruning (Eq. 1, Eq. 5, token protection).
+ * logits: [T][E] fp32, finite.  important: [T] uint8, nonzero = protected
+ * (may be NULL: no token protected).  threshold tau in [0, 1] acts on the
+ * top-k-normalised weight p_r = exp(l_r - l_0) / sum_{i<k} exp(l_i - l_0):
+ * for an unprotected token, rank r >= 1 is dropped when p_r < tau; rank 0 is
+ * never dropped; tau = 0 disables pruning.  For k = 2 this is Eq. 5 with
+ * mu = tau / (1 - tau) and is decided as fp32(l_0 - l_1) > delta, delta the
+ * fp32 rounding of ln((1 - tau) / tau); for k > 2 it is evaluated in fp64.
+ * Errors: MC_EINVAL (shape, null pointer, tau outside [0, 1]), MC_EHIP. */
+mc_status mc_route_and_prune(const float *logits, const uint8_t *important,
+                             float threshold, const mc_routing *r, void *stream);
+
+/* Workspace bytes mc_moe_forward needs for T tokens. Errors: MC_EINVAL. */
+mc_status mc_forward_workspace(int T, int E, int k, int d, int ffn, size_t *bytes);
+
+/* Eq. 1 over the kept pairs: y_t = sum_r w_r * E_{e_r}(x_t) with
+ * E_e(x) = W_down (silu(W_gate x) * (W_up x)) on the exact dequantized
+ * weights s*(q - z).  x: [T][d] bf16; y: [T][d] bf16 (round to nearest even
+ * of the fp32 result).  r must come from mc_route_and_prune on the same
+ * stream (or be complete).  workspace: ws_bytes >= mc_forward_workspace.
+ * Errors: MC_EINVAL (shape mismatch, null pointer), MC_ENOSPACE, MC_EHIP. */
+mc_status mc_moe_forward(const uint16_t *x_bf16, const mc_routing *r,
+                         const mc_layer *L, uint16_t *y_bf16, void *workspace,
+                         size_t ws_bytes, void *stream);
+
+/* Message for the last non-OK status returned on this thread. */
+const char *mc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MC_MOE_H */

@@ -1,0 +1,334 @@
+"""CPU oracle of the Mixture Compressor expert path -- TEST INFRASTRUCTURE.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product library never calls it and
+shares no code with it: the kernels and the C functions in ``mc_oracle.c``
+implement the same definitions independently.
+
+What it computes (Mixture Compressor for MoE LLMs, ICLR 2025):
+
+* ``quantize``      -- Sec. 3.1 uniform asymmetric group quantizer (fp16 scale
+  and zero, codes in [0, 2^b - 1], nearest level decided exactly);
+* ``layout_pack`` / ``layout_unpack`` / ``pack_sz`` / ``unpack_sz`` -- the
+  packed storage format, element by element from its index function;
+* ``dequant_f16`` / ``dequant_exact`` -- the dequantized value s*(q - z);
+* ``route``         -- Eq. 1 top-k, Eq. 5 pruning, Sec. 3.3.2 protection and
+  the per-expert token lists;
+* ``moe_forward``   -- Eq. 1 over SwiGLU experts on exact dequantized weights.
+
+Everything floating point is fp64 except operations whose precision the
+definition fixes (fp32 scale/zero arithmetic, the fp32 k = 2 logit gap).
+Parity status of each function is recorded in ``PINS`` below.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "mc_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+# Every function is pinned by tests that do not re-use its own code
+# (see tests/test_oracle_pins.py); none is "parity unpinned".
+PINS = {
+    "quantize": "Fraction brute force over all codes; level bound; range endpoints",
+    "layout_pack": "round trip, word-count closed form, hand-built words",
+    "dequant_f16": "Fraction value rounded by numpy float16 (library RNE)",
+    "route": "naive stable sort; tau=0 and protected no-op; k=2 gap == ratio rule",
+    "moe_forward": "E=1,k=1 equals numpy SwiGLU; tau=0 all-protected dense top-k; linearity",
+}
+
+
+def build(force: bool = False) -> str:
+    """Compile ``liboracle.so`` with gcc (plain C, no fast-math, no contraction)."""
+    with _lock:
+        if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            tmp = _LIB + ".tmp%d" % os.getpid()
+            subprocess.check_call([
+                "gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math",
+                "-fopenmp", "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"])
+            os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        I = ctypes.c_int
+        lib.orc_f16_to_double.restype = ctypes.c_double
+        lib.orc_f16_to_double.argtypes = [ctypes.c_uint16]
+        for name in ("orc_f16_from_double", "orc_f16_from_double_sat", "orc_bf16_from_double"):
+            getattr(lib, name).restype = ctypes.c_uint16
+            getattr(lib, name).argtypes = [ctypes.c_double]
+        lib.orc_bf16_to_double.restype = ctypes.c_double
+        lib.orc_bf16_to_double.argtypes = [ctypes.c_uint16]
+        lib.orc_quantize_group.restype = I
+        lib.orc_quantize_group.argtypes = [P, I, I, P, P, P]
+        lib.orc_quantize_matrix.restype = I
+        lib.orc_quantize_matrix.argtypes = [P, I, I, I, I, P, P, P]
+        lib.orc_dequant.restype = ctypes.c_double
+        lib.orc_dequant.argtypes = [ctypes.c_uint16, ctypes.c_uint16, I]
+        lib.orc_dequant_matrix_f16.restype = None
+        lib.orc_dequant_matrix_f16.argtypes = [P, P, P, I, I, I, P]
+        lib.orc_layout_pack.restype = I
+        lib.orc_layout_pack.argtypes = [P, I, I, I, P]
+        lib.orc_layout_unpack.restype = I
+        lib.orc_layout_unpack.argtypes = [P, I, I, I, P]
+        lib.orc_layout_pack_sz.restype = I
+        lib.orc_layout_pack_sz.argtypes = [P, P, I, I, I, P]
+        lib.orc_layout_unpack_sz.restype = I
+        lib.orc_layout_unpack_sz.argtypes = [P, I, I, I, P, P]
+        lib.orc_route.restype = I
+        lib.orc_route.argtypes = [P, P, I, I, I, ctypes.c_double, ctypes.c_float,
+                                  P, P, P, P, P, P, P, P, P, P]
+        lib.orc_expert_forward.restype = I
+        lib.orc_expert_forward.argtypes = [P, I, I, I, I, P, P, P, P, P, P, P, P, P, P, I, P, P]
+        _lib = lib
+    return _lib
+
+
+def _p(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+# ---------------------------------------------------------------- formats ---
+
+def f16_to_float(h: int) -> float:
+    return _load().orc_f16_to_double(int(h))
+
+
+def f16_round(v: float, saturate: bool = False) -> int:
+    lib = _load()
+    return int(lib.orc_f16_from_double_sat(v) if saturate else lib.orc_f16_from_double(v))
+
+
+def bf16_round(v: float) -> int:
+    return int(_load().orc_bf16_from_double(float(v)))
+
+
+def bf16_round_array(a: np.ndarray) -> np.ndarray:
+    """Round-to-nearest-even bfloat16 bits of each fp64 value (element loop in C)."""
+    lib = _load()
+    flat = np.ascontiguousarray(a, dtype=np.float64).ravel()
+    out = np.empty(flat.shape, dtype=np.uint16)
+    for i, v in enumerate(flat):
+        out[i] = lib.orc_bf16_from_double(float(v))
+    return out.reshape(np.shape(a))
+
+
+def bf16_to_float64(h: np.ndarray) -> np.ndarray:
+    """Exact widening of bfloat16 bit patterns."""
+    h = np.asarray(h, dtype=np.uint16)
+    return (h.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+# -------------------------------------------------------------- quantizer ---
+
+def quantize_group(w: np.ndarray, bits: int):
+    """Sec. 3.1 quantizer on one group: returns (s16 bits, z16 bits, codes)."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    s = np.zeros(1, np.uint16)
+    z = np.zeros(1, np.uint16)
+    q = np.zeros(w.size, np.uint8)
+    if _load().orc_quantize_group(_p(w), w.size, bits, _p(s), _p(z), _p(q)):
+        raise ValueError("bad quantize_group arguments")
+    return int(s[0]), int(z[0]), q
+
+
+def quantize(W: np.ndarray, bits: int, G: int):
+    """Row-major W[R][K] -> (codes uint8 [R][K], s16 [R][K/G], z16 [R][K/G])."""
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    R, K = W.shape
+    q = np.empty((R, K), np.uint8)
+    s = np.empty((R, K // G), np.uint16)
+    z = np.empty((R, K // G), np.uint16)
+    if _load().orc_quantize_matrix(_p(W), R, K, G, bits, _p(q), _p(s), _p(z)):
+        raise ValueError("bad quantize arguments")
+    return q, s, z
+
+
+def dequant_exact(q: np.ndarray, s: np.ndarray, z: np.ndarray, G: int) -> np.ndarray:
+    """s*(q - z) in fp64 (exact: see the quantizer comment in mc_oracle.c)."""
+    sf = s.view(np.float16).astype(np.float64)
+    zf = z.view(np.float16).astype(np.float64)
+    sf = np.repeat(sf, G, axis=1)
+    zf = np.repeat(zf, G, axis=1)
+    return sf * (q.astype(np.float64) - zf)
+
+
+def dequant_f16(q: np.ndarray, s: np.ndarray, z: np.ndarray, G: int) -> np.ndarray:
+    """fp16 bits of the single RNE rounding of s*(q - z)."""
+    R, K = q.shape
+    out = np.empty((R, K), np.uint16)
+    _load().orc_dequant_matrix_f16(_p(np.ascontiguousarray(q)), _p(np.ascontiguousarray(s)),
+                                   _p(np.ascontiguousarray(z)), R, K, G, _p(out))
+    return out
+
+
+# ----------------------------------------------------------------- layout ---
+
+def layout_pack(q: np.ndarray, bits: int) -> np.ndarray:
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    R, K = q.shape
+    words = np.empty(R * K * bits // 32, np.uint32)
+    if _load().orc_layout_pack(_p(q), R, K, bits, _p(words)):
+        raise ValueError("shape not packable")
+    return words
+
+
+def layout_unpack(words: np.ndarray, R: int, K: int, bits: int) -> np.ndarray:
+    words = np.ascontiguousarray(words, dtype=np.uint32)
+    assert words.size == R * K * bits // 32
+    q = np.empty((R, K), np.uint8)
+    if _load().orc_layout_unpack(_p(words), R, K, bits, _p(q)):
+        raise ValueError("shape not packable")
+    return q
+
+
+def pack_sz(s: np.ndarray, z: np.ndarray, G: int) -> np.ndarray:
+    s = np.ascontiguousarray(s, dtype=np.uint16)
+    z = np.ascontiguousarray(z, dtype=np.uint16)
+    R, ng = s.shape
+    out = np.empty(R * ng, np.uint32)
+    if _load().orc_layout_pack_sz(_p(s), _p(z), R, ng * G, G, _p(out)):
+        raise ValueError("shape not packable")
+    return out
+
+
+def unpack_sz(sz: np.ndarray, R: int, K: int, G: int):
+    sz = np.ascontiguousarray(sz, dtype=np.uint32)
+    s = np.empty((R, K // G), np.uint16)
+    z = np.empty((R, K // G), np.uint16)
+    if _load().orc_layout_unpack_sz(_p(sz), R, K, G, _p(s), _p(z)):
+        raise ValueError("shape not packable")
+    return s, z
+
+
+def layer_offsets(E: int, d: int, ffn: int, bits, G: int):
+    """Word and scale/zero-word offsets of (expert, matrix) inside a layer:
+    experts in order, each holding gate [ffn][d], up [ffn][d], down [d][ffn]."""
+    words, szs = {}, {}
+    wo = so = 0
+    for e in range(E):
+        for m in range(3):
+            words[(e, m)] = wo
+            szs[(e, m)] = so
+            wo += d * ffn * int(bits[e]) // 32
+            so += d * ffn // G
+    return words, szs, wo, so
+
+
+def pack_layer(mats, bits, G: int):
+    """mats[e] = (gate [ffn][d], up [ffn][d], down [d][ffn]) fp32.
+    Returns (words uint32, sz uint32, logical) with logical[e][m] = (q, s, z)."""
+    E = len(mats)
+    ffn, d = mats[0][0].shape
+    wofs, sofs, nw, ns = layer_offsets(E, d, ffn, bits, G)
+    words = np.zeros(nw, np.uint32)
+    sz = np.zeros(ns, np.uint32)
+    logical = []
+    for e in range(E):
+        per = []
+        for m in range(3):
+            q, s, z = quantize(mats[e][m], int(bits[e]), G)
+            w = layout_pack(q, int(bits[e]))
+            words[wofs[(e, m)]: wofs[(e, m)] + w.size] = w
+            p = pack_sz(s, z, G)
+            sz[sofs[(e, m)]: sofs[(e, m)] + p.size] = p
+            per.append((q, s, z))
+        logical.append(per)
+    return words, sz, logical
+
+
+# ---------------------------------------------------------------- routing ---
+
+def prune_delta(tau: float) -> float:
+    """fp32 threshold on the logit gap l_0 - l_1 equivalent to p_1 < tau at k = 2:
+    p_1 = 1 / (1 + exp(l_0 - l_1)) < tau  <=>  l_0 - l_1 > ln((1 - tau) / tau)."""
+    if tau <= 0.0:
+        return math.inf
+    if tau >= 1.0:
+        return -math.inf
+    return float(np.float32(math.log((1.0 - tau) / tau)))
+
+
+def route(logits: np.ndarray, important, k: int, tau: float):
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    T, E = logits.shape
+    imp = None if important is None else np.ascontiguousarray(important, dtype=np.uint8)
+    out = dict(
+        topk_idx=np.empty((T, k), np.int32), topk_w=np.empty((T, k), np.float64),
+        kept=np.empty((T, k), np.uint8), counts=np.empty(E, np.int32),
+        offsets=np.empty(E + 1, np.int32), pair_token=np.full(T * k, -1, np.int32),
+        pair_rank=np.full(T * k, -1, np.int32), pair_w=np.zeros(T * k, np.float64),
+        pair_pos=np.empty((T, k), np.int32), n_pruned=np.zeros(1, np.int32))
+    rc = _load().orc_route(
+        _p(logits), None if imp is None else _p(imp), T, E, k, float(tau),
+        ctypes.c_float(prune_delta(tau)),
+        _p(out["topk_idx"]), _p(out["topk_w"]), _p(out["kept"]), _p(out["counts"]),
+        _p(out["offsets"]), _p(out["pair_token"]), _p(out["pair_rank"]), _p(out["pair_w"]),
+        _p(out["pair_pos"]), _p(out["n_pruned"]))
+    if rc:
+        raise ValueError("bad route arguments")
+    out["n_pruned"] = int(out["n_pruned"][0])
+    return out
+
+
+# ---------------------------------------------------------------- forward ---
+
+def expert_forward(X: np.ndarray, logical_e, G: int, rows=None):
+    """One SwiGLU expert on token rows X [nt][d] (fp64).  Returns (H [nt][ffn],
+    Y [nt][len(rows) or d])."""
+    X = np.ascontiguousarray(X, dtype=np.float64)
+    nt, d = X.shape
+    (qg, sg, zg), (qu, su, zu), (qd, sd, zd) = logical_e
+    ffn = qg.shape[0]
+    H = np.empty((nt, ffn), np.float64)
+    if rows is None:
+        rows_a, nr = None, d
+    else:
+        rows_a = np.ascontiguousarray(rows, dtype=np.int32)
+        nr = rows_a.size
+    Y = np.empty((nt, nr), np.float64)
+    c = np.ascontiguousarray
+    rc = _load().orc_expert_forward(
+        _p(X), nt, d, ffn, G, _p(c(qg)), _p(c(sg)), _p(c(zg)), _p(c(qu)), _p(c(su)), _p(c(zu)),
+        _p(c(qd)), _p(c(sd)), _p(c(zd)), None if rows_a is None else _p(rows_a), nr, _p(H), _p(Y))
+    if rc:
+        raise ValueError("bad expert_forward arguments")
+    return H, Y
+
+
+def moe_forward(x_bf16: np.ndarray, routing, logical, G: int, rows=None, tokens=None) -> np.ndarray:
+    """Eq. 1: y_t = sum over kept ranks of w_r * E_{e_r}(x_t), fp64.
+    ``rows`` restricts the output columns, ``tokens`` the output tokens."""
+    X = bf16_to_float64(x_bf16)
+    T, d = X.shape
+    toks = np.arange(T) if tokens is None else np.asarray(tokens)
+    nr = d if rows is None else len(rows)
+    Y = np.zeros((len(toks), nr), np.float64)
+    tpos = {int(t): i for i, t in enumerate(toks)}
+    E = len(logical)
+    k = routing["topk_idx"].shape[1]
+    for e in range(E):
+        sel = [(int(t), r) for t in toks for r in range(k)
+               if routing["topk_idx"][t, r] == e and routing["kept"][t, r]]
+        if not sel:
+            continue
+        Xe = X[[t for t, _ in sel]]
+        _, Ye = expert_forward(Xe, logical[e], G, rows)
+        for i, (t, r) in enumerate(sel):
+            Y[tpos[t]] += routing["topk_w"][t, r] * Ye[i]
+    return Y

@@ -1,0 +1,380 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these tests re-types an oracle formula: each compares the oracle with
+an independent route (exact rational brute force, a library routine, a
+hand-derived fixture, a closed form or an invariant), chosen so that a dropped
+term, a wrong sign, index or tie rule, or a transposed operand fails one.
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle
+import synthetic
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _lines(name):
+    with open(os.path.join(GOLD, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                yield [p.strip() for p in line.split("|")]
+
+
+def f16val(bits):
+    return float(np.array([bits], np.uint16).view(np.float16)[0])
+
+
+# --------------------------------------------------------------- formats ---
+
+def test_f16_rounding_matches_numpy():
+    """RNE to fp16 (Sec. 3.1 stores scale and zero in 16 bits) vs numpy's float16 cast."""
+    g = np.random.default_rng(1)
+    vals = np.concatenate([
+        g.standard_normal(4000) * 10.0 ** g.integers(-9, 5, 4000),
+        np.array([65504.0, 65519.99, 65520.0, 65536.0, 2.0 ** -24, 2.0 ** -25, 3 * 2.0 ** -26,
+                  2.0 ** -14, 2.0 ** -14 - 2.0 ** -25, 1.0 + 2.0 ** -11, 1.0 + 3 * 2.0 ** -11,
+                  0.0, -0.0, -1.5, 2049.0, 2051.0]),
+    ])
+    for v in vals:
+        with np.errstate(over="ignore"):
+            want = int(np.array([v], np.float64).astype(np.float16).view(np.uint16)[0])
+        assert oracle.f16_round(float(v)) == want, v
+
+
+def test_f16_saturating():
+    assert oracle.f16_round(1e6, saturate=True) == 0x7BFF
+    assert oracle.f16_round(-1e6, saturate=True) == 0xFBFF
+    assert oracle.f16_round(65519.0, saturate=True) == 0x7BFF
+    assert oracle.f16_round(1e6) == 0x7C00
+
+
+def test_bf16_rounding_matches_torch():
+    torch = pytest.importorskip("torch")
+    g = np.random.default_rng(2)
+    v = (g.standard_normal(5000) * 10.0 ** g.integers(-30, 30, 5000)).astype(np.float32)
+    want = torch.from_numpy(v).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = oracle.bf16_round_array(v.astype(np.float64))
+    np.testing.assert_array_equal(got, want)
+
+
+# -------------------------------------------------------------- quantizer ---
+
+def _brute_codes(w, s16, z16, bits):
+    """argmin_j |w - s*(j - z)| over all 2^b codes in exact rationals, ties -> even j."""
+    s = Fraction(f16val(s16))
+    z = Fraction(f16val(z16))
+    out = []
+    for wi in w:
+        wf = Fraction(float(wi))
+        best = None
+        for j in range(2 ** bits):
+            dist = abs(wf - s * (j - z))
+            if best is None or dist < best[0] or (dist == best[0] and j % 2 == 0):
+                best = (dist, j)
+        out.append(best[1])
+    return out
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3])
+def test_quantizer_codes_are_exact_nearest_levels(bits):
+    g = np.random.default_rng(10 + bits)
+    for trial in range(40):
+        G = 32
+        w = (g.standard_normal(G) * 0.02 * (1 + trial % 5)).astype(np.float32)
+        if trial % 7 == 0:
+            w = np.round(w * 64).astype(np.float32) / np.float32(64)   # coarse grid: many ties
+        s16, z16, q = oracle.quantize_group(w, bits)
+        assert list(q) == _brute_codes(w, s16, z16, bits)
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3])
+def test_quantizer_scale_zero_properties(bits):
+    """Levels span [min, max] up to the fp16 rounding of s and z; every value
+    inside the span is within s/2 of its level; codes lie in [0, 2^b - 1]."""
+    L = 2 ** bits - 1
+    g = np.random.default_rng(20 + bits)
+    for _ in range(200):
+        w = (g.standard_normal(64) * g.uniform(0.001, 3.0) + g.uniform(-1, 1)).astype(np.float32)
+        s16, z16, q = oracle.quantize_group(w, bits)
+        s, z = f16val(s16), f16val(z16)
+        mn, mx = float(w.min()), float(w.max())
+        assert s > 0
+        assert abs(s - (mx - mn) / L) <= 2.0 ** -10 * (mx - mn) / L + 1e-12
+        assert q.max() <= L
+        lo, hi = s * (0 - z), s * (L - z)
+        tol = 2.0 ** -9 * (abs(mx) + abs(mn)) + 2.0 ** -11 * abs(z) * s * 4 + 1e-9
+        assert abs(lo - mn) <= tol and abs(hi - mx) <= tol * (L + 1)
+        for wi, qi in zip(w, q):
+            if lo <= wi <= hi:
+                assert abs(float(wi) - s * (int(qi) - z)) <= s / 2 * (1 + 1e-12)
+
+
+def test_quantizer_golden_cases():
+    for bits, vals, fill, s, z, codes in _lines("quant_ties.txt"):
+        bits = int(bits)
+        vals = [float(v) for v in vals.split()]
+        w = np.full(32, float(fill), np.float32)
+        w[: len(vals)] = vals
+        s16, z16, q = oracle.quantize_group(w, bits)
+        assert f16val(s16) == float(s)
+        assert f16val(z16) == float(z) and not (z16 & 0x8000 and f16val(z16) == 0.0)
+        assert list(q[: len(vals)]) == [int(c) for c in codes.split()]
+
+
+def test_quantize_matrix_groups_along_rows():
+    """Each row's groups are quantized independently (a transposed group axis fails)."""
+    g = np.random.default_rng(3)
+    W = (g.standard_normal((16, 128)) * 0.02).astype(np.float32)
+    W[3, 64:96] *= 50.0                       # one loud group
+    q, s, z = oracle.quantize(W, 2, 32)
+    for r in range(16):
+        for gi in range(4):
+            s16, z16, qq = oracle.quantize_group(W[r, 32 * gi: 32 * gi + 32], 2)
+            assert (s[r, gi], z[r, gi]) == (s16, z16)
+            np.testing.assert_array_equal(q[r, 32 * gi: 32 * gi + 32], qq)
+    assert f16val(s[3, 2]) > 20 * f16val(s[3, 1])
+
+
+# ------------------------------------------------------------- dequant ---
+
+def test_dequant_exact_and_single_rounding():
+    """fp16 export = one RNE rounding of the exact rational s*(q - z) (numpy's
+    float16 cast of the exact value); a naive fp32 product rounded again would
+    differ on some of these triples."""
+    g = np.random.default_rng(4)
+    n = 200000
+    s = (np.abs(g.standard_normal(n)) * 0.01 + 1e-4).astype(np.float16)
+    z = (g.uniform(-1, 8, n)).astype(np.float16)
+    q = g.integers(0, 8, n).astype(np.uint8)
+    s16 = s.view(np.uint16).reshape(n, 1)
+    z16 = z.view(np.uint16).reshape(n, 1)
+    got = oracle.dequant_f16(q.reshape(n, 1), s16, z16, 1).ravel()
+    exact = [Fraction(float(si)) * (int(qi) - Fraction(float(zi))) for si, zi, qi in zip(s, z, q)]
+    want = np.array([float(v) for v in exact], np.float64).astype(np.float16).view(np.uint16)
+    np.testing.assert_array_equal(got, want)
+
+
+def test_dequant_double_rounding_cases():
+    """Triples where an fp32 product rounded again to fp16 is one ulp off: the
+    oracle must give the single rounding of the exact rational value."""
+    for trip, good, bad in _lines("dequant_double_rounding.txt"):
+        s16, z16, q = (int(v) for v in trip.split())
+        exact = Fraction(f16val(s16)) * (q - Fraction(f16val(z16)))
+        want = int(np.array([float(exact)]).astype(np.float16).view(np.uint16)[0])
+        assert want == int(good) != int(bad)
+        got = oracle.dequant_f16(np.array([[q]], np.uint8), np.array([[s16]], np.uint16),
+                                 np.array([[z16]], np.uint16), 1)
+        assert int(got[0, 0]) == want
+
+
+# ---------------------------------------------------------------- layout ---
+
+@pytest.mark.parametrize("bits", [1, 2, 3])
+def test_layout_round_trip_and_size(bits):
+    g = np.random.default_rng(5 + bits)
+    R, K = 48, 384
+    q = g.integers(0, 2 ** bits, (R, K)).astype(np.uint8)
+    w = oracle.layout_pack(q, bits)
+    assert w.size == R * K * bits // 32                 # dense: no padding words
+    np.testing.assert_array_equal(oracle.layout_unpack(w, R, K, bits), q)
+    # every bit of every word is used: all-ones codes give all-ones words
+    full = oracle.layout_pack(np.full((R, K), 2 ** bits - 1, np.uint8), bits)
+    assert (full == 0xFFFFFFFF).all()
+
+
+def test_layout_golden_positions():
+    for shape, code, words in _lines("layout_bits.txt"):
+        R, K, bits = (int(v) for v in shape.split())
+        n, k, c = (int(v) for v in code.split())
+        q = np.zeros((R, K), np.uint8)
+        q[n, k] = c
+        w = oracle.layout_pack(q, bits)
+        toks = words.split()
+        want = {int(toks[i]): int(toks[i + 1], 16) for i in range(0, len(toks), 2)}
+        nz = {int(i): int(w[i]) for i in np.nonzero(w)[0]}
+        assert nz == want, (shape, code)
+
+
+def test_scale_zero_layout():
+    g = np.random.default_rng(6)
+    R, K, G = 32, 256, 64
+    s = g.integers(0, 65536, (R, K // G)).astype(np.uint16)
+    z = g.integers(0, 65536, (R, K // G)).astype(np.uint16)
+    sz = oracle.pack_sz(s, z, G)
+    # closed form of the index: ((n/16)*(K/G) + g)*16 + n%16
+    for n in (0, 5, 16, 31):
+        for gi in range(K // G):
+            idx = ((n // 16) * (K // G) + gi) * 16 + n % 16
+            assert sz[idx] == int(s[n, gi]) | (int(z[n, gi]) << 16)
+    s2, z2 = oracle.unpack_sz(sz, R, K, G)
+    np.testing.assert_array_equal(s2, s)
+    np.testing.assert_array_equal(z2, z)
+
+
+# --------------------------------------------------------------- routing ---
+
+def test_route_golden():
+    rows = list(_lines("route_small.txt"))
+    logits = np.array([[float(v) for v in r[0].split()] for r in rows], np.float32)
+    imp = np.array([int(r[1]) for r in rows], np.uint8)
+    out = oracle.route(logits, imp, 2, 0.3)
+    for t, r in enumerate(rows):
+        assert list(out["topk_idx"][t]) == [int(v) for v in r[2].split()]
+        assert list(out["kept"][t]) == [int(v) for v in r[3].split()]
+        np.testing.assert_allclose(out["topk_w"][t], [float(v) for v in r[4].split()], atol=1e-6)
+
+
+def _naive_topk(l, k):
+    return sorted(range(len(l)), key=lambda i: (-float(l[i]), i))[:k]
+
+
+@pytest.mark.parametrize("cid,T", [(1, 64), (4, 300), (2, 32)])
+def test_route_matches_naive_sort_and_softmax(cid, T):
+    c = synthetic.config(cid)
+    E, k, tau = c["E"], c["k"], c["tau"][0]
+    lg = synthetic.logits(cid, T)
+    lg[::7, 1] = lg[::7, 0]                  # exact ties
+    imp = synthetic.important_mask(cid, T)
+    out = oracle.route(lg, imp, k, tau)
+    for t in range(T):
+        sel = _naive_topk(lg[t], k)
+        assert list(out["topk_idx"][t]) == sel
+        p = scipy.special.softmax(lg[t, sel].astype(np.float64))
+        for r in range(1, k):
+            if imp[t]:
+                assert out["kept"][t, r] == 1
+            elif abs(p[r] - tau) > 1e-9:
+                assert out["kept"][t, r] == (0 if p[r] < tau else 1), (t, r, p[r])
+        assert out["kept"][t, 0] == 1
+        keep = out["kept"][t].astype(bool)
+        want_w = np.where(keep, p, 0.0) / p[keep].sum()
+        np.testing.assert_allclose(out["topk_w"][t], want_w, rtol=1e-12, atol=1e-15)
+
+
+def test_route_k2_gap_rule_equals_eq5_ratio():
+    """Eq. 5 prunes the secondary expert when w1/w0 < mu; with mu = tau/(1-tau)
+    that is the logit-gap rule, checked in exact rationals away from the boundary."""
+    g = np.random.default_rng(7)
+    T, E = 4000, 8
+    lg = (g.standard_normal((T, E)) * 1.5).astype(np.float32)
+    for tau in (0.1, 0.3, 0.45):
+        out = oracle.route(lg, None, 2, tau)
+        mu = tau / (1 - tau)
+        for t in range(T):
+            i0, i1 = out["topk_idx"][t]
+            ratio = math.exp(float(lg[t, i1]) - float(lg[t, i0]))       # w1/w0
+            if abs(ratio - mu) > 1e-6:
+                assert out["kept"][t, 1] == (0 if ratio < mu else 1)
+
+
+def test_route_tau_zero_and_all_protected_prune_nothing():
+    lg = synthetic.logits(4, 256)
+    for tau, imp in ((0.0, None), (0.9, np.ones(256, np.uint8))):
+        out = oracle.route(lg, imp, 8, tau)
+        assert out["n_pruned"] == 0 and out["kept"].all()
+
+
+def test_route_csr_invariants():
+    for cid, T in ((4, 2048), (1, 64), (2, 32)):
+        c = synthetic.config(cid)
+        lg = synthetic.logits(cid, T)
+        out = oracle.route(lg, synthetic.important_mask(cid, T), c["k"], c["tau"][0])
+        k, E = c["k"], c["E"]
+        assert out["counts"].sum() == T * k - out["n_pruned"]
+        assert out["offsets"][0] == 0 and (np.diff(out["offsets"]) == out["counts"]).all()
+        seen = set()
+        for e in range(E):
+            toks = out["pair_token"][out["offsets"][e]: out["offsets"][e + 1]]
+            assert (np.diff(toks) > 0).all()
+            for p in range(out["offsets"][e], out["offsets"][e + 1]):
+                t, r = out["pair_token"][p], out["pair_rank"][p]
+                assert out["topk_idx"][t, r] == e and out["kept"][t, r]
+                assert out["pair_pos"][t, r] == p and out["pair_w"][p] == out["topk_w"][t, r]
+                seen.add((t, r))
+        assert len(seen) == out["counts"].sum()
+        assert ((out["pair_pos"] >= 0) == out["kept"].astype(bool)).all()
+
+
+# --------------------------------------------------------------- forward ---
+
+def _swiglu_numpy(X, logical_e, G):
+    (qg, sg, zg), (qu, su, zu), (qd, sd, zd) = logical_e
+    Wg = oracle.dequant_exact(qg, sg, zg, G)
+    Wu = oracle.dequant_exact(qu, su, zu, G)
+    Wd = oracle.dequant_exact(qd, sd, zd, G)
+    a = X @ Wg.T
+    return (a * scipy.special.expit(a) * (X @ Wu.T)) @ Wd.T
+
+
+def _tiny_layer(E, bits, G=32, d=256, ffn=512, seed_cfg=1):
+    mats = synthetic.layer_weights(seed_cfg, E=E, d=d, ffn=ffn)
+    _, _, logical = oracle.pack_layer(mats, bits, G)
+    return logical
+
+
+def test_forward_single_expert_is_plain_swiglu():
+    """E = 1, k = 1: Eq. 1 reduces to one SwiGLU FFN (numpy matmuls on the
+    dequantized weights)."""
+    logical = _tiny_layer(1, [2])
+    x = synthetic.activations(1, 16)
+    lg = np.zeros((16, 1), np.float32)
+    rt = oracle.route(lg, None, 1, 0.3)
+    y = oracle.moe_forward(x, rt, logical, 32)
+    want = _swiglu_numpy(oracle.bf16_to_float64(x), logical[0], 32)
+    np.testing.assert_allclose(y, want, rtol=1e-10, atol=1e-12)
+
+
+def test_forward_dense_topk_when_nothing_pruned():
+    """tau = 0 with every token protected = dense top-k MoE with softmax weights."""
+    c = synthetic.config(1)
+    logical = _tiny_layer(4, c["bits"])
+    T = 24
+    x = synthetic.activations(1, T)
+    lg = synthetic.logits(1, T)
+    rt = oracle.route(lg, np.ones(T, np.uint8), 2, 0.0)
+    y = oracle.moe_forward(x, rt, logical, 32)
+    X = oracle.bf16_to_float64(x)
+    want = np.zeros_like(y)
+    for t in range(T):
+        sel = _naive_topk(lg[t], 2)
+        p = scipy.special.softmax(lg[t, sel].astype(np.float64))
+        for r, e in enumerate(sel):
+            want[t] += p[r] * _swiglu_numpy(X[t: t + 1], logical[e], 32)[0]
+    np.testing.assert_allclose(y, want, rtol=1e-10, atol=1e-12)
+
+
+def test_forward_pruned_token_uses_primary_only():
+    """A pruned k = 2 token's output is exactly its primary expert's output (Eq. 5)."""
+    c = synthetic.config(1)
+    logical = _tiny_layer(4, c["bits"])
+    T = 64
+    x = synthetic.activations(1, T)
+    lg = synthetic.logits(1, T)
+    rt = oracle.route(lg, None, 2, 0.3)
+    y = oracle.moe_forward(x, rt, logical, 32)
+    X = oracle.bf16_to_float64(x)
+    pruned = np.nonzero(rt["kept"][:, 1] == 0)[0]
+    assert len(pruned) > 3
+    for t in pruned[:4]:
+        e0 = rt["topk_idx"][t, 0]
+        np.testing.assert_allclose(y[t], _swiglu_numpy(X[t: t + 1], logical[e0], 32)[0],
+                                   rtol=1e-10, atol=1e-12)
+
+
+def test_forward_rows_and_tokens_subset():
+    c = synthetic.config(1)
+    logical = _tiny_layer(4, c["bits"])
+    x = synthetic.activations(1, 64)
+    rt = oracle.route(synthetic.logits(1, 64), synthetic.important_mask(1, 64), 2, 0.3)
+    full = oracle.moe_forward(x, rt, logical, 32)
+    rows = [0, 7, 100, 255]
+    toks = [3, 10, 63]
+    part = oracle.moe_forward(x, rt, logical, 32, rows=rows, tokens=toks)
+    np.testing.assert_array_equal(part, full[np.ix_(toks, rows)])
