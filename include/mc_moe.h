@@ -24,8 +24,8 @@
  *     earlier launches of the same call may have been enqueued) and
  *     mc_last_error() describes the problem.
  *   - Shape limits: 1 <= E <= 256 experts, 1 <= k <= min(E, 8), d and ffn
- *     multiples of 128, group size G one of 32, 64, 128 or a multiple of 128,
- *     dividing both d and ffn.
+ *     multiples of 128 with d*ffn <= 2^31, group size G one of 32, 64, 128
+ *     (other multiples of 32 give MC_EUNSUPPORTED).
  *
  * Packed layout (normative; used by every kernel).  A matrix with R output
  * rows and K input columns (row-major W[R][K], the reduction runs over K) at

@@ -1,0 +1,21 @@
+"""MI355X (gfx950) hot path of the Mixture Compressor MoE method.
+
+Thin Python binding of ``libmcmoe.so`` (C-ABI in ``include/mc_moe.h``): every
+step runs in the HIP kernels; this module only marshals torch device tensors
+into the C descriptors and passes the current stream.  It raises if the
+library is not built -- there is no fallback.
+"""
+from ._binding import (  # noqa: F401
+    MCError,
+    PackedLayer,
+    Routing,
+    codes_export,
+    dequant_export,
+    forward_workspace,
+    lib_path,
+    load,
+    moe_forward,
+    pack,
+    pack_sizes,
+    route_and_prune,
+)

@@ -1,0 +1,179 @@
+"""ctypes binding of the C-ABI (argument marshalling only).
+
+Functions carry the C names without the ``mc_`` prefix.  Device buffers are
+torch tensors on the current CUDA (HIP) device; the library never allocates,
+so ``PackedLayer`` and ``Routing`` allocate their buffers with torch and build
+the descriptors over them.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libmcmoe.so")
+_lib = None
+
+MC_OK, MC_EINVAL, MC_ENOSPACE, MC_EHIP, MC_EUNSUPPORTED = range(5)
+MAX_EXPERTS = 256
+MAX_TOPK = 8
+
+
+class MCError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("mc status %d: %s" % (status, msg))
+        self.status = status
+
+
+class _Layer(ctypes.Structure):
+    _fields_ = [("E", ctypes.c_int), ("d", ctypes.c_int), ("ffn", ctypes.c_int),
+                ("group", ctypes.c_int), ("bits_host", ctypes.POINTER(ctypes.c_int)),
+                ("words", ctypes.c_void_p), ("sz", ctypes.c_void_p),
+                ("words_bytes", ctypes.c_size_t), ("sz_bytes", ctypes.c_size_t)]
+
+
+class _Routing(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int), ("E", ctypes.c_int), ("k", ctypes.c_int),
+                ("topk_idx", ctypes.c_void_p), ("topk_w", ctypes.c_void_p),
+                ("kept", ctypes.c_void_p), ("counts", ctypes.c_void_p),
+                ("offsets", ctypes.c_void_p), ("pair_token", ctypes.c_void_p),
+                ("pair_rank", ctypes.c_void_p), ("pair_w", ctypes.c_void_p),
+                ("pair_pos", ctypes.c_void_p), ("n_pruned", ctypes.c_void_p)]
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def load():
+    """Load libmcmoe.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError("libmcmoe.so is not built (run __graft_entry__.build())")
+        lib = ctypes.CDLL(_LIB_PATH)
+        P, I, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+        st = ctypes.c_int
+        lib.mc_last_error.restype = ctypes.c_char_p
+        lib.mc_last_error.argtypes = []
+        lib.mc_pack_sizes.restype = st
+        lib.mc_pack_sizes.argtypes = [I, I, I, P, I, ctypes.POINTER(S), ctypes.POINTER(S)]
+        lib.mc_pack.restype = st
+        lib.mc_pack.argtypes = [P, P, P, ctypes.POINTER(_Layer), P]
+        lib.mc_dequant_export.restype = st
+        lib.mc_dequant_export.argtypes = [ctypes.POINTER(_Layer), I, I, P, P]
+        lib.mc_codes_export.restype = st
+        lib.mc_codes_export.argtypes = [ctypes.POINTER(_Layer), I, I, P, P]
+        lib.mc_route_and_prune.restype = st
+        lib.mc_route_and_prune.argtypes = [P, P, ctypes.c_float, ctypes.POINTER(_Routing), P]
+        lib.mc_forward_workspace.restype = st
+        lib.mc_forward_workspace.argtypes = [I, I, I, I, I, ctypes.POINTER(S)]
+        lib.mc_moe_forward.restype = st
+        lib.mc_moe_forward.argtypes = [P, ctypes.POINTER(_Routing), ctypes.POINTER(_Layer), P, P,
+                                       S, P]
+        _lib = lib
+    return _lib
+
+
+def _check(status: int):
+    if status != MC_OK:
+        raise MCError(status, load().mc_last_error().decode())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def pack_sizes(E: int, d: int, ffn: int, bits, group: int):
+    arr = (ctypes.c_int * len(bits))(*[int(b) for b in bits])
+    wb, szb = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(load().mc_pack_sizes(E, d, ffn, arr, group, ctypes.byref(wb), ctypes.byref(szb)))
+    return wb.value, szb.value
+
+
+class PackedLayer:
+    """Device buffers + descriptor of one packed layer (torch-allocated)."""
+
+    def __init__(self, E: int, d: int, ffn: int, bits, group: int, device=None):
+        self.E, self.d, self.ffn, self.group = E, d, ffn, group
+        self.bits = [int(b) for b in bits]
+        wb, szb = pack_sizes(E, d, ffn, self.bits, group)
+        device = device or torch.device("cuda")
+        self.words = torch.empty(wb // 4, dtype=torch.int32, device=device)
+        self.sz = torch.empty(szb // 4, dtype=torch.int32, device=device)
+        self._bits_c = (ctypes.c_int * E)(*self.bits)
+        self.desc = _Layer(E, d, ffn, group, self._bits_c, self.words.data_ptr(),
+                           self.sz.data_ptr(), wb, szb)
+
+    @property
+    def nbytes(self) -> int:
+        return self.words.numel() * 4 + self.sz.numel() * 4
+
+
+class Routing:
+    """Device buffers + descriptor of a routing result for T tokens."""
+
+    def __init__(self, T: int, E: int, k: int, device=None):
+        device = device or torch.device("cuda")
+        self.T, self.E, self.k = T, E, k
+        i32 = dict(dtype=torch.int32, device=device)
+        self.topk_idx = torch.empty((T, k), **i32)
+        self.topk_w = torch.empty((T, k), dtype=torch.float32, device=device)
+        self.kept = torch.empty((T, k), dtype=torch.uint8, device=device)
+        self.counts = torch.empty(E, **i32)
+        self.offsets = torch.empty(E + 1, **i32)
+        self.pair_token = torch.full((T * k,), -1, **i32)
+        self.pair_rank = torch.full((T * k,), -1, **i32)
+        self.pair_w = torch.zeros(T * k, dtype=torch.float32, device=device)
+        self.pair_pos = torch.empty((T, k), **i32)
+        self.n_pruned = torch.empty(1, **i32)
+        self.desc = _Routing(T, E, k, *[t.data_ptr() for t in (
+            self.topk_idx, self.topk_w, self.kept, self.counts, self.offsets, self.pair_token,
+            self.pair_rank, self.pair_w, self.pair_pos, self.n_pruned)])
+
+
+def pack(w_gate, w_up, w_down, layer: PackedLayer, stream=None):
+    for t in (w_gate, w_up, w_down):
+        assert t.dtype == torch.float32 and t.is_contiguous() and t.is_cuda
+    _check(load().mc_pack(_ptr(w_gate), _ptr(w_up), _ptr(w_down), ctypes.byref(layer.desc),
+                          _stream(stream)))
+
+
+def dequant_export(layer: PackedLayer, e: int, mat: int, out, stream=None):
+    assert out.dtype in (torch.float16, torch.int16) and out.is_contiguous()
+    _check(load().mc_dequant_export(ctypes.byref(layer.desc), e, mat, _ptr(out), _stream(stream)))
+
+
+def codes_export(layer: PackedLayer, e: int, mat: int, out, stream=None):
+    assert out.dtype == torch.uint8 and out.is_contiguous()
+    _check(load().mc_codes_export(ctypes.byref(layer.desc), e, mat, _ptr(out), _stream(stream)))
+
+
+def route_and_prune(logits, important, threshold: float, routing: Routing, stream=None):
+    assert logits.dtype == torch.float32 and logits.is_contiguous()
+    if important is not None:
+        assert important.dtype == torch.uint8 and important.is_contiguous()
+    _check(load().mc_route_and_prune(_ptr(logits), _ptr(important), float(threshold),
+                                     ctypes.byref(routing.desc), _stream(stream)))
+
+
+def forward_workspace(T: int, E: int, k: int, d: int, ffn: int) -> int:
+    b = ctypes.c_size_t()
+    _check(load().mc_forward_workspace(T, E, k, d, ffn, ctypes.byref(b)))
+    return b.value
+
+
+def moe_forward(x, routing: Routing, layer: PackedLayer, y, workspace, stream=None):
+    """x, y: bf16 (or int16 bit patterns) [T][d] device tensors."""
+    assert x.is_contiguous() and y.is_contiguous() and x.element_size() == 2
+    _check(load().mc_moe_forward(_ptr(x), ctypes.byref(routing.desc), ctypes.byref(layer.desc),
+                                 _ptr(y), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                 _stream(stream)))

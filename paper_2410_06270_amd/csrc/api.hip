@@ -1,0 +1,190 @@
+// api.hip -- the extern "C" boundary: argument validation, descriptors,
+// launches on the caller's stream.  No allocation anywhere.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "mc_internal.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+mc_status fail(mc_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+mc_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return MC_OK;
+  return fail(MC_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+mc_status check_shape(int E, int d, int ffn, const int* bits, int G) {
+  if (E < 1 || E > MC_MAX_EXPERTS) return fail(MC_EINVAL, "E=%d outside [1, %d]", E, MC_MAX_EXPERTS);
+  if (d <= 0 || ffn <= 0 || d % 128 || ffn % 128)
+    return fail(MC_EINVAL, "d=%d and ffn=%d must be positive multiples of 128", d, ffn);
+  if ((long long)d * ffn > (1LL << 31))
+    return fail(MC_EUNSUPPORTED, "d*ffn=%lld exceeds 2^31", (long long)d * ffn);
+  if (G != 32 && G != 64 && G != 128)
+    return fail(G > 0 && G % 32 == 0 ? MC_EUNSUPPORTED : MC_EINVAL,
+                "group size %d: this build supports 32, 64 and 128", G);
+  if (!bits) return fail(MC_EINVAL, "bits_host is NULL");
+  for (int e = 0; e < E; ++e)
+    if (bits[e] < 1 || bits[e] > 3) return fail(MC_EINVAL, "bits[%d]=%d not in {1,2,3}", e, bits[e]);
+  return MC_OK;
+}
+
+void sizes(int E, int d, int ffn, const int* bits, int G, size_t* wb, size_t* szb) {
+  size_t w = 0;
+  for (int e = 0; e < E; ++e) w += 3 * (size_t)d * ffn * bits[e] / 8;
+  *wb = w;
+  *szb = 3 * (size_t)E * d * ffn / G * 4;
+}
+
+mc_status check_layer(const mc_layer* L, bool need_buffers) {
+  if (!L) return fail(MC_EINVAL, "layer descriptor is NULL");
+  mc_status s = check_shape(L->E, L->d, L->ffn, L->bits_host, L->group);
+  if (s != MC_OK) return s;
+  if (!need_buffers) return MC_OK;
+  if (!L->words || !L->sz) return fail(MC_EINVAL, "layer words/sz pointer is NULL");
+  size_t wb, szb;
+  sizes(L->E, L->d, L->ffn, L->bits_host, L->group, &wb, &szb);
+  if (L->words_bytes < wb || L->sz_bytes < szb)
+    return fail(MC_ENOSPACE, "layer buffers hold %zu/%zu bytes, need %zu/%zu", L->words_bytes,
+                L->sz_bytes, wb, szb);
+  return MC_OK;
+}
+
+mc::LayerArgs layer_args(const mc_layer* L) {
+  mc::LayerArgs a;
+  a.words = static_cast<const uint32_t*>(L->words);
+  a.sz = L->sz;
+  a.E = L->E;
+  a.d = L->d;
+  a.ffn = L->ffn;
+  a.G = L->group;
+  a.cum_bits[0] = 0;
+  for (int e = 0; e < L->E; ++e) a.cum_bits[e + 1] = (uint16_t)(a.cum_bits[e] + L->bits_host[e]);
+  for (int e = L->E; e < MC_MAX_EXPERTS; ++e) a.cum_bits[e + 1] = a.cum_bits[e];
+  return a;
+}
+
+mc_status check_routing(const mc_routing* r) {
+  if (!r) return fail(MC_EINVAL, "routing descriptor is NULL");
+  if (r->T < 1) return fail(MC_EINVAL, "T=%d must be >= 1", r->T);
+  if (r->E < 1 || r->E > MC_MAX_EXPERTS) return fail(MC_EINVAL, "E=%d outside [1, %d]", r->E, MC_MAX_EXPERTS);
+  if (r->k < 1 || r->k > r->E || r->k > MC_MAX_TOPK)
+    return fail(MC_EINVAL, "k=%d outside [1, min(E=%d, %d)]", r->k, r->E, MC_MAX_TOPK);
+  if ((long long)r->T * r->k >= (1LL << 31) || (long long)r->T * r->E >= (1LL << 31))
+    return fail(MC_EUNSUPPORTED, "T=%d too large", r->T);
+  if (!r->topk_idx || !r->topk_w || !r->kept || !r->counts || !r->offsets || !r->pair_token ||
+      !r->pair_rank || !r->pair_w || !r->pair_pos || !r->n_pruned)
+    return fail(MC_EINVAL, "a routing output pointer is NULL");
+  return MC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mc_last_error(void) { return g_err; }
+
+mc_status mc_pack_sizes(int E, int d, int ffn, const int* bits_host, int group, size_t* words_bytes,
+                        size_t* sz_bytes) {
+  mc_status s = check_shape(E, d, ffn, bits_host, group);
+  if (s != MC_OK) return s;
+  if (!words_bytes || !sz_bytes) return fail(MC_EINVAL, "output size pointer is NULL");
+  sizes(E, d, ffn, bits_host, group, words_bytes, sz_bytes);
+  return MC_OK;
+}
+
+mc_status mc_pack(const float* w_gate, const float* w_up, const float* w_down, const mc_layer* L,
+                  void* stream) {
+  mc_status s = check_layer(L, true);
+  if (s != MC_OK) return s;
+  if (!w_gate || !w_up || !w_down) return fail(MC_EINVAL, "weight pointer is NULL");
+  (void)hipGetLastError();
+  const mc::LayerArgs a = layer_args(L);
+  return hip_status(mc::launch_pack(w_gate, w_up, w_down, a, static_cast<uint32_t*>(L->words),
+                                    L->sz, static_cast<hipStream_t>(stream)),
+                    "mc_pack launch");
+}
+
+static mc_status export_common(const mc_layer* L, int e, int mat, void* out, bool dequant,
+                               void* stream) {
+  mc_status s = check_layer(L, true);
+  if (s != MC_OK) return s;
+  if (e < 0 || e >= L->E) return fail(MC_EINVAL, "expert %d outside [0, %d)", e, L->E);
+  if (mat < 0 || mat > 2) return fail(MC_EINVAL, "matrix %d not in {0,1,2}", mat);
+  if (!out) return fail(MC_EINVAL, "output pointer is NULL");
+  const mc::LayerArgs a = layer_args(L);
+  const int b = L->bits_host[e];
+  const size_t per_bit = (size_t)L->d * L->ffn / 32;
+  const size_t wofs = (3 * (size_t)a.cum_bits[e] + (size_t)mat * b) * per_bit;
+  const size_t sofs = (3 * (size_t)e + mat) * ((size_t)L->d * L->ffn / L->group);
+  const int R = mat < 2 ? L->ffn : L->d, K = mat < 2 ? L->d : L->ffn;
+  (void)hipGetLastError();
+  return hip_status(mc::launch_export(static_cast<const uint32_t*>(L->words) + wofs, L->sz + sofs,
+                                      b, R, K, L->group, dequant, out,
+                                      static_cast<hipStream_t>(stream)),
+                    "export launch");
+}
+
+mc_status mc_dequant_export(const mc_layer* L, int e, int mat, uint16_t* out, void* stream) {
+  return export_common(L, e, mat, out, true, stream);
+}
+
+mc_status mc_codes_export(const mc_layer* L, int e, int mat, uint8_t* out, void* stream) {
+  return export_common(L, e, mat, out, false, stream);
+}
+
+mc_status mc_route_and_prune(const float* logits, const uint8_t* important, float threshold,
+                             const mc_routing* r, void* stream) {
+  mc_status s = check_routing(r);
+  if (s != MC_OK) return s;
+  if (!logits) return fail(MC_EINVAL, "logits pointer is NULL");
+  if (!(threshold >= 0.0f && threshold <= 1.0f))
+    return fail(MC_EINVAL, "threshold %g outside [0, 1]", (double)threshold);
+  const double tau = (double)threshold;
+  float delta32;
+  if (tau == 0.0) delta32 = INFINITY;
+  else if (tau == 1.0) delta32 = -INFINITY;
+  else delta32 = (float)std::log((1.0 - tau) / tau);
+  (void)hipGetLastError();
+  return hip_status(mc::launch_route(logits, important, delta32, tau, *r,
+                                     static_cast<hipStream_t>(stream)),
+                    "mc_route_and_prune launch");
+}
+
+mc_status mc_forward_workspace(int T, int E, int k, int d, int ffn, size_t* bytes) {
+  if (T < 1 || E < 1 || E > MC_MAX_EXPERTS || k < 1 || k > E || k > MC_MAX_TOPK || d <= 0 ||
+      ffn <= 0 || d % 128 || ffn % 128)
+    return fail(MC_EINVAL, "bad shape T=%d E=%d k=%d d=%d ffn=%d", T, E, k, d, ffn);
+  if (!bytes) return fail(MC_EINVAL, "bytes pointer is NULL");
+  *bytes = mc::forward_workspace_bytes(T, E, k, d, ffn);
+  return MC_OK;
+}
+
+mc_status mc_moe_forward(const uint16_t* x_bf16, const mc_routing* r, const mc_layer* L,
+                         uint16_t* y_bf16, void* workspace, size_t ws_bytes, void* stream) {
+  mc_status s = check_routing(r);
+  if (s != MC_OK) return s;
+  s = check_layer(L, true);
+  if (s != MC_OK) return s;
+  if (r->E != L->E) return fail(MC_EINVAL, "routing has E=%d, layer has E=%d", r->E, L->E);
+  if (!x_bf16 || !y_bf16 || !workspace) return fail(MC_EINVAL, "x, y or workspace is NULL");
+  const size_t need = mc::forward_workspace_bytes(r->T, r->E, r->k, L->d, L->ffn);
+  if (ws_bytes < need) return fail(MC_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+  (void)hipGetLastError();
+  const mc::LayerArgs a = layer_args(L);
+  return hip_status(mc::launch_forward(x_bf16, a, *r, y_bf16, workspace,
+                                       static_cast<hipStream_t>(stream)),
+                    "mc_moe_forward launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,127 @@
+// mc_device.hpp -- device-side helpers shared by the gfx950 kernels of the
+// MC expert path: number formats, the packed-code layout and launch-argument
+// structs.  Internal to the library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/mc_moe.h"
+
+namespace mc {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+
+constexpr int kTileRows = 16;    // rows of one packed tile (MFMA N)
+constexpr int kTileCols = 128;   // reduction columns of one packed tile (4 MFMA K-steps)
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- formats --
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
+  _Float16 v;
+  uint16_t b = (uint16_t)h;
+  __builtin_memcpy(&v, &b, 2);
+  return (float)v;
+}
+
+// Round to nearest even fp16; saturate to +-65504 instead of infinity.
+__device__ __forceinline__ uint16_t float_to_half_sat(float f) {
+  _Float16 v = (_Float16)f;
+  uint16_t b;
+  __builtin_memcpy(&b, &v, 2);
+  if ((b & 0x7fffu) == 0x7c00u) b = (uint16_t)((b & 0x8000u) | 0x7bffu);
+  return b;
+}
+
+__device__ __forceinline__ float bf16_bits_to_float(uint32_t h) {
+  return __uint_as_float(h << 16);
+}
+
+// Round to nearest even bfloat16 (finite inputs).
+__device__ __forceinline__ uint16_t float_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// fp16 bits of the single round-to-nearest-even rounding of a double.
+// Rounds to fp32 with round-to-odd first (24 >= 11 + 2 bits, so the second
+// rounding cannot create a double-rounding error: Boldo & Melquiond,
+// "Emulation of FMA and correctly rounded sums: proved algorithms using
+// rounding to odd", IEEE TC 2008), then to fp16 with round-to-nearest-even.
+__device__ __forceinline__ uint16_t double_to_half_rne(double v) {
+  float f = (float)v;
+  if ((double)f != v) {
+    uint32_t b = __float_as_uint(f);
+    if (fabs((double)f) > fabs(v)) b -= 1u;   // step the magnitude toward zero
+    b |= 1u;                                  // sticky odd bit
+    f = __uint_as_float(b);
+  }
+  _Float16 h = (_Float16)f;
+  uint16_t r;
+  __builtin_memcpy(&r, &h, 2);
+  return r;
+}
+
+// ------------------------------------------------------------------ layout --
+// Lane l of a 16x128 tile holds, for MFMA step u (32 columns) and register v
+// (0..3), the codes of columns 32u + 8*(l/16) + 2v (low half) and +1 (high
+// half) of row l%16: "pair" i = 4u + v.  extract_pair returns that pair as
+// two 16-bit lanes holding the code in bits 0..2 with `magic` OR-ed in
+// (0x4300 = bf16 128.0: the lane then holds the bf16 value 128 + code).
+
+template <int BITS>
+__device__ __forceinline__ uint32_t extract_pair(const uint32_t* w, int i, uint32_t magic2) {
+  if constexpr (BITS == 1) {
+    return ((w[0] >> i) & 0x00010001u) | magic2;
+  } else if constexpr (BITS == 2) {
+    return ((w[i >> 3] >> (2 * (i & 7))) & 0x00030003u) | magic2;
+  } else {
+    if (i < 15) {
+      const int wi = i / 5, f = i - 5 * wi;
+      return ((w[wi] >> (3 * f)) & 0x00070007u) | magic2;
+    }
+    return ((w[0] >> 15) & 0x00010001u) | ((w[1] >> 14) & 0x00020002u) |
+           ((w[2] >> 13) & 0x00040004u) | magic2;
+  }
+}
+
+// Code of pair i, half h (for the export kernels).
+template <int BITS>
+__device__ __forceinline__ int extract_code(const uint32_t* w, int i, int h) {
+  return (int)((extract_pair<BITS>(w, i, 0u) >> (16 * h)) & 7u);
+}
+
+// --------------------------------------------------------------- arguments --
+
+struct LayerArgs {
+  const uint32_t* words;
+  const uint32_t* sz;
+  int E, d, ffn, G;
+  uint16_t cum_bits[MC_MAX_EXPERTS + 1];   // prefix sums of the expert widths
+};
+
+// Word offset of matrix m (0 gate, 1 up, 2 down) of expert e.
+__device__ __forceinline__ size_t layer_word_offset(const LayerArgs& L, int e, int m) {
+  const size_t per_bit = (size_t)L.d * (size_t)L.ffn / 32;
+  const int b = L.cum_bits[e + 1] - L.cum_bits[e];
+  return (3 * (size_t)L.cum_bits[e] + (size_t)m * b) * per_bit;
+}
+
+__device__ __forceinline__ size_t layer_sz_offset(const LayerArgs& L, int e, int m) {
+  return (3 * (size_t)e + m) * ((size_t)L.d * (size_t)L.ffn / L.G);
+}
+
+struct RouteArgs {
+  const int32_t* counts;
+  const int32_t* offsets;
+  const int32_t* pair_token;
+  const int32_t* pair_pos;
+  const float* topk_w;
+  int T, E, k;
+};
+
+}  // namespace mc

@@ -1,0 +1,22 @@
+// mc_internal.hpp -- launchers shared between the kernel files and the C-ABI.
+#pragma once
+
+#include "mc_device.hpp"
+
+namespace mc {
+
+constexpr int kRouteFusedMaxT = 256;   // up to this many tokens routing runs in one launch
+constexpr int kDecodeMaxT = 64;        // up to this many tokens one workgroup holds all of an expert's tokens
+
+hipError_t launch_pack(const float* wg, const float* wu, const float* wd, const LayerArgs& L,
+                       uint32_t* words, uint32_t* sz, hipStream_t stream);
+hipError_t launch_export(const uint32_t* words, const uint32_t* sz, int bits, int R, int K, int G,
+                         bool dequant, void* out, hipStream_t stream);
+hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,
+                        const mc_routing& r, hipStream_t stream);
+int forward_nsplit(int T, int E, int k, int d, int ffn);
+size_t forward_workspace_bytes(int T, int E, int k, int d, int ffn);
+hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
+                          void* ws, hipStream_t stream);
+
+}  // namespace mc

@@ -1,0 +1,207 @@
+// pack.hip -- quantize + pack kernels and the dequant/code export kernels.
+//
+// Quantizer (paper Sec. 3.1: uniform asymmetric, group-wise, values mapped onto
+// the integer grid 0..2^b-1; widths 1/2/3 from the PMQ allocation of Eq. 4).
+// Per group of G inputs of one row, L = 2^b - 1:
+//   s = fp16(fp32(max - min) / L) (1.0 if it rounds to zero), z = fp16(-min / s),
+//   code = nearest level s*(j - z), ties to the even j, decided exactly in fp64.
+#include "mc_internal.hpp"
+
+namespace mc {
+
+// ------------------------------------------------------------ scale / zero --
+// One group per `lpg` consecutive lanes (lpg = min(64, G/4)); every lane
+// reduces float4 pieces, then the group's lanes combine with butterflies.
+__global__ void __launch_bounds__(256) pack_sz_kernel(const float* __restrict__ wg,
+                                                      const float* __restrict__ wu,
+                                                      const float* __restrict__ wd,
+                                                      LayerArgs L, uint32_t* __restrict__ sz_out,
+                                                      long long total_groups) {
+  const int G = L.G;
+  const int lpg = G / 4 < 64 ? G / 4 : 64;          // lanes per group (power of two)
+  const int per_lane = G / 4 / lpg;                  // float4 pieces per lane
+  const int lane = threadIdx.x & 63;
+  const long long wave = ((long long)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const long long grp = wave * (64 / lpg) + lane / lpg;
+  const int sub = lane % lpg;
+  const bool valid = grp < total_groups;
+  const long long gpm = (long long)L.d * L.ffn / G;  // groups per matrix
+  const long long gg = valid ? grp : 0;
+  const int em = (int)(gg / gpm);
+  const int e = em / 3, m = em % 3;
+  const long long gi = gg % gpm;
+  const int K = (m < 2) ? L.d : L.ffn;
+  const int ng = K / G;
+  const int row = (int)(gi / ng), g = (int)(gi % ng);
+  const float* W = (m == 0) ? wg : (m == 1) ? wu : wd;
+  const float* src = W + (size_t)e * L.d * L.ffn + (size_t)row * K + (size_t)g * G;
+
+  float mn = __builtin_inff(), mx = -__builtin_inff();
+  if (valid) {
+    for (int p = 0; p < per_lane; ++p) {
+      const float4 v = reinterpret_cast<const float4*>(src)[sub + p * lpg];
+      mn = fminf(mn, fminf(fminf(v.x, v.y), fminf(v.z, v.w)));
+      mx = fmaxf(mx, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+    }
+  }
+  for (int off = 1; off < lpg; off <<= 1) {
+    mn = fminf(mn, __shfl_xor(mn, off));
+    mx = fmaxf(mx, __shfl_xor(mx, off));
+  }
+  if (!valid || sub != 0) return;
+  const int b = L.cum_bits[e + 1] - L.cum_bits[e];
+  const float Lf = (float)((1 << b) - 1);
+  const float s32 = (mx - mn) / Lf;                 // IEEE fp32 division
+  uint16_t s16 = float_to_half_sat(s32);
+  if ((s16 & 0x7fffu) == 0) s16 = 0x3c00;           // scale 0 -> 1.0
+  const float z32 = -mn / half_bits_to_float(s16);
+  uint16_t z16 = float_to_half_sat(z32);
+  if (z16 == 0x8000u) z16 = 0;                      // -0 -> +0
+  const size_t idx = layer_sz_offset(L, e, m) + ((size_t)(row / 16) * ng + g) * 16 + (row % 16);
+  sz_out[idx] = (uint32_t)s16 | ((uint32_t)z16 << 16);
+}
+
+// ------------------------------------------------------------------- codes --
+// One thread per (matrix, tile, lane): 32 codes -> b words.
+// Code of w: the number of level midpoints s*(j + 1/2 - z) below w, moved to
+// the even neighbour when w sits exactly on a midpoint.  Each midpoint is
+// exact in fp64 (j + 1/2 - z needs <= 41 bits, times the 11-bit s <= 52).
+__device__ __forceinline__ int nearest_code(float w, double s, double z, int L) {
+  const double wd = (double)w;
+  int below = 0;
+  for (int j = 0; j < L; ++j) below += (s * (((double)j + 0.5) - z) < wd) ? 1 : 0;
+  if (below < L && (below & 1) && s * (((double)below + 0.5) - z) == wd) ++below;
+  return below;
+}
+
+__global__ void __launch_bounds__(256) pack_codes_kernel(const float* __restrict__ wg,
+                                                         const float* __restrict__ wu,
+                                                         const float* __restrict__ wd,
+                                                         LayerArgs L,
+                                                         const uint32_t* __restrict__ sz,
+                                                         uint32_t* __restrict__ words_out,
+                                                         long long total_lanes) {
+  const long long tid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid >= total_lanes) return;
+  const long long lpm = (long long)L.d * L.ffn / 32;   // lanes per matrix
+  const int em = (int)(tid / lpm);
+  const int e = em / 3, m = em % 3;
+  const long long rest = tid % lpm;
+  const int lane = (int)(rest & 63);
+  const long long tile = rest >> 6;
+  const int K = (m < 2) ? L.d : L.ffn;
+  const int tiles_per_row = K / kTileCols;
+  const int trow = (int)(tile / tiles_per_row), tcol = (int)(tile % tiles_per_row);
+  const int n = trow * kTileRows + (lane & 15);
+  const int kq = lane >> 4;
+  const int G = L.G, ng = K / G;
+  const int b = L.cum_bits[e + 1] - L.cum_bits[e];
+  const int Lc = (1 << b) - 1;
+  const float* W = (m == 0) ? wg : (m == 1) ? wu : wd;
+  const float* row = W + (size_t)e * L.d * L.ffn + (size_t)n * K;
+  const uint32_t* szm = sz + layer_sz_offset(L, e, m);
+
+  uint32_t w[3] = {0u, 0u, 0u};
+  for (int u = 0; u < 4; ++u) {
+    const int k0 = tcol * kTileCols + 32 * u + 8 * kq;
+    const int g = k0 / G;
+    const uint32_t szw = szm[((size_t)(n / 16) * ng + g) * 16 + (n % 16)];
+    const double s = (double)half_bits_to_float(szw & 0xffffu);
+    const double z = (double)half_bits_to_float(szw >> 16);
+    const float4 a = reinterpret_cast<const float4*>(row + k0)[0];
+    const float4 c = reinterpret_cast<const float4*>(row + k0)[1];
+    const float v[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t code = (uint32_t)nearest_code(v[j], s, z, Lc);
+      const int i = 4 * u + (j >> 1), h = j & 1;
+      if (b == 1) {
+        w[0] |= code << (16 * h + i);
+      } else if (b == 2) {
+        w[i >> 3] |= code << (16 * h + 2 * (i & 7));
+      } else if (i < 15) {
+        w[i / 5] |= code << (16 * h + 3 * (i % 5));
+      } else {
+        for (int p = 0; p < 3; ++p) w[p] |= ((code >> p) & 1u) << (16 * h + 15);
+      }
+    }
+  }
+  uint32_t* dst = words_out + layer_word_offset(L, e, m) + ((size_t)tile * 64 + lane) * b;
+  for (int p = 0; p < b; ++p) dst[p] = w[p];
+}
+
+// ------------------------------------------------------------------ export --
+// One thread per tile lane of one matrix: writes its 32 values.
+template <int BITS, bool DEQUANT>
+__global__ void __launch_bounds__(256) export_kernel(const uint32_t* __restrict__ words,
+                                                    const uint32_t* __restrict__ sz, int R, int K,
+                                                    int G, void* __restrict__ out) {
+  const long long tid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long lanes = (long long)R * K / 32;
+  if (tid >= lanes) return;
+  const int lane = (int)(tid & 63);
+  const long long tile = tid >> 6;
+  const int tiles_per_row = K / kTileCols;
+  const int trow = (int)(tile / tiles_per_row), tcol = (int)(tile % tiles_per_row);
+  const int n = trow * kTileRows + (lane & 15);
+  const int kq = lane >> 4;
+  const int ng = K / G;
+  uint32_t w[3] = {0u, 0u, 0u};
+  const uint32_t* src = words + ((size_t)tile * 64 + lane) * BITS;
+  for (int p = 0; p < BITS; ++p) w[p] = src[p];
+  for (int u = 0; u < 4; ++u) {
+    const int k0 = tcol * kTileCols + 32 * u + 8 * kq;
+    const uint32_t szw = sz[((size_t)(n / 16) * ng + k0 / G) * 16 + (n % 16)];
+    const double s = (double)half_bits_to_float(szw & 0xffffu);
+    const double z = (double)half_bits_to_float(szw >> 16);
+    for (int j = 0; j < 8; ++j) {
+      const int code = extract_code<BITS>(w, 4 * u + (j >> 1), j & 1);
+      const size_t o = (size_t)n * K + k0 + j;
+      if constexpr (DEQUANT) {
+        // s*(q - z): q - z needs <= 41 bits, the product <= 52: exact in fp64.
+        static_cast<uint16_t*>(out)[o] = double_to_half_rne(s * ((double)code - z));
+      } else {
+        static_cast<uint8_t*>(out)[o] = (uint8_t)code;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- launchers --
+
+hipError_t launch_pack(const float* wg, const float* wu, const float* wd, const LayerArgs& L,
+                       uint32_t* words, uint32_t* sz, hipStream_t stream) {
+  const long long groups = 3LL * L.E * L.d * L.ffn / L.G;
+  const int lpg = L.G / 4 < 64 ? L.G / 4 : 64;
+  const long long waves = (groups + (64 / lpg) - 1) / (64 / lpg);
+  const long long blocks_sz = (waves * 64 + 255) / 256;
+  hipLaunchKernelGGL(pack_sz_kernel, dim3((unsigned)blocks_sz), dim3(256), 0, stream, wg, wu, wd,
+                     L, sz, groups);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const long long lanes = 3LL * L.E * L.d * L.ffn / 32;
+  hipLaunchKernelGGL(pack_codes_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, stream,
+                     wg, wu, wd, L, sz, words, lanes);
+  return hipGetLastError();
+}
+
+hipError_t launch_export(const uint32_t* words, const uint32_t* sz, int bits, int R, int K, int G,
+                         bool dequant, void* out, hipStream_t stream) {
+  const long long lanes = (long long)R * K / 32;
+  const dim3 grid((unsigned)((lanes + 255) / 256)), block(256);
+#define MC_EXPORT_CASE(B)                                                                     \
+  if (bits == B) {                                                                            \
+    if (dequant)                                                                              \
+      hipLaunchKernelGGL((export_kernel<B, true>), grid, block, 0, stream, words, sz, R, K, G, \
+                         out);                                                                \
+    else                                                                                      \
+      hipLaunchKernelGGL((export_kernel<B, false>), grid, block, 0, stream, words, sz, R, K,  \
+                         G, out);                                                             \
+  }
+  MC_EXPORT_CASE(1)
+  MC_EXPORT_CASE(2)
+  MC_EXPORT_CASE(3)
+#undef MC_EXPORT_CASE
+  return hipGetLastError();
+}
+
+}  // namespace mc

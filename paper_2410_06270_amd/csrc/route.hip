@@ -1,0 +1,223 @@
+// route.hip -- top-k routing with Online Dynamic Pruning and token protection.
+//
+// Eq. 1: each token is sent to its top-k experts (largest logits; equal logits
+// ordered by lower expert index), weighted by the softmax over the selected k.
+// Eq. 5 (k = 2): the secondary expert is dropped when w1/w0 < mu, decided here
+// as fp32(l0 - l1) > delta with delta = fp32(ln((1 - tau)/tau)), tau = mu/(1+mu);
+// for k > 2 rank r >= 1 is dropped when its normalised weight is below tau
+// (fp64).  Sec. 3.3.2: a protected token keeps every selected expert.  The
+// kept weights are renormalised over the kept ranks.
+//
+// Phase 1 (one wavefront per token): lanes hold the logits, k rounds of a
+// 64-bit max-reduction pick the experts.  Phase 2 (one workgroup): per-expert
+// token lists in ascending token order, built with ballots and popcount
+// prefixes (no atomics, so the lists are deterministic).
+#include "mc_internal.hpp"
+
+namespace mc {
+
+constexpr int kCsrThreads = 1024;
+constexpr int kCsrChunk = 2048;     // tokens staged in LDS per pass (k <= 8 -> 32 KB)
+
+__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v) {
+  for (int off = 32; off >= 1; off >>= 1) {
+    const unsigned lo = __shfl_xor((unsigned)(v & 0xffffffffu), off);
+    const unsigned hi = __shfl_xor((unsigned)(v >> 32), off);
+    const unsigned long long o = ((unsigned long long)hi << 32) | lo;
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
+// Order-preserving integer image of a float, with -0 mapped onto +0.
+__device__ __forceinline__ uint32_t ordered_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) == 0) u = 0;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ void select_token(const float* __restrict__ logits, const uint8_t* __restrict__ important,
+                             int t, int E, int k, float delta32, double tau,
+                             int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
+                             uint8_t* __restrict__ kept, int32_t* __restrict__ pair_pos) {
+  const int lane = threadIdx.x & 63;
+  const float* l = logits + (size_t)t * E;
+  unsigned long long key[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + 64 * j;
+    key[j] = (e < E) ? (((unsigned long long)ordered_bits(l[e]) << 32) | (unsigned)(0xffff - e)) : 0ull;
+  }
+  int sel[MC_MAX_TOPK];
+#pragma unroll
+  for (int r = 0; r < MC_MAX_TOPK; ++r) {
+    if (r < k) {
+      unsigned long long best = key[0];
+#pragma unroll
+      for (int j = 1; j < 4; ++j) best = key[j] > best ? key[j] : best;
+      best = wave_max_u64(best);
+      const int e = 0xffff - (int)(best & 0xffffu);
+      sel[r] = e;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (lane + 64 * j == e) key[j] = 0ull;
+    } else {
+      sel[r] = 0;
+    }
+  }
+  // weights and pruning: every lane evaluates the same k terms
+  const float l0 = l[sel[0]];
+  double ex[MC_MAX_TOPK];
+  double sum_all = 0.0;
+#pragma unroll
+  for (int r = 0; r < MC_MAX_TOPK; ++r) {
+    ex[r] = (r < k) ? exp((double)l[sel[r]] - (double)l0) : 0.0;
+    sum_all += ex[r];
+  }
+  const bool prot = important != nullptr && important[t] != 0;
+  bool keep[MC_MAX_TOPK];
+  double sum_kept = 0.0;
+#pragma unroll
+  for (int r = 0; r < MC_MAX_TOPK; ++r) {
+    bool kp = r < k;
+    if (kp && r > 0 && !prot) {
+      if (k == 2) {
+        const float gap = l0 - l[sel[1]];
+        kp = !(gap > delta32);
+      } else {
+        kp = !(ex[r] < tau * sum_all);
+      }
+    }
+    keep[r] = kp;
+    if (kp) sum_kept += ex[r];
+  }
+#pragma unroll
+  for (int r = 0; r < MC_MAX_TOPK; ++r) {
+    if (r < k && lane == r) {
+      const size_t o = (size_t)t * k + r;
+      topk_idx[o] = sel[r];
+      kept[o] = keep[r] ? 1 : 0;
+      topk_w[o] = keep[r] ? (float)(ex[r] / sum_kept) : 0.0f;
+      pair_pos[o] = -1;
+    }
+  }
+}
+
+// Per-expert lists.  Runs in one workgroup of kCsrThreads threads.
+__device__ void build_lists(int T, int E, int k, const int32_t* __restrict__ topk_idx,
+                            const uint8_t* __restrict__ kept, const float* __restrict__ topk_w,
+                            int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+                            int32_t* __restrict__ pair_token, int32_t* __restrict__ pair_rank,
+                            float* __restrict__ pair_w, int32_t* __restrict__ pair_pos,
+                            int32_t* __restrict__ n_pruned) {
+  __shared__ uint16_t ent[kCsrChunk * MC_MAX_TOPK];   // expert of (t, r), 0xffff if pruned
+  __shared__ int cnt[MC_MAX_EXPERTS];
+  __shared__ int base[MC_MAX_EXPERTS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nwaves = blockDim.x >> 6;
+  for (int e = tid; e < E; e += blockDim.x) cnt[e] = 0;
+  for (int pass = 0; pass < 2; ++pass) {
+    if (pass == 1) {
+      __syncthreads();
+      if (tid == 0) {
+        int acc = 0;
+        for (int e = 0; e < E; ++e) {
+          offsets[e] = acc;
+          counts[e] = cnt[e];
+          base[e] = acc;
+          acc += cnt[e];
+        }
+        offsets[E] = acc;
+        *n_pruned = T * k - acc;
+      }
+    }
+    for (int c0 = 0; c0 < T; c0 += kCsrChunk) {
+      const int nc = (T - c0) < kCsrChunk ? (T - c0) : kCsrChunk;
+      __syncthreads();
+      for (int i = tid; i < nc * k; i += blockDim.x) {
+        const size_t o = (size_t)c0 * k + i;
+        ent[i] = kept[o] ? (uint16_t)topk_idx[o] : (uint16_t)0xffff;
+      }
+      __syncthreads();
+      for (int e = wave; e < E; e += nwaves) {
+        int run = (pass == 0) ? 0 : base[e];
+        for (int t0 = 0; t0 < nc; t0 += 64) {
+          const int tl = t0 + lane;
+          int rr = -1;
+          if (tl < nc)
+            for (int r = 0; r < k; ++r)
+              if (ent[tl * k + r] == e) rr = r;
+          const unsigned long long m = __ballot(rr >= 0);
+          if (pass == 1 && rr >= 0) {
+            const int pos = run + __popcll(m & ((1ull << lane) - 1ull));
+            const int t = c0 + tl;
+            pair_token[pos] = t;
+            pair_rank[pos] = rr;
+            pair_w[pos] = topk_w[(size_t)t * k + rr];
+            pair_pos[(size_t)t * k + rr] = pos;
+          }
+          run += __popcll(m);
+        }
+        if (lane == 0) {
+          if (pass == 0) cnt[e] += run;
+          else base[e] = run;
+        }
+      }
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256) route_select_kernel(const float* __restrict__ logits,
+                                                           const uint8_t* __restrict__ important,
+                                                           int T, int E, int k, float delta32,
+                                                           double tau, int32_t* topk_idx,
+                                                           float* topk_w, uint8_t* kept,
+                                                           int32_t* pair_pos) {
+  const int t = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (t >= T) return;
+  select_token(logits, important, t, E, k, delta32, tau, topk_idx, topk_w, kept, pair_pos);
+}
+
+__global__ void __launch_bounds__(kCsrThreads) route_lists_kernel(
+    int T, int E, int k, const int32_t* topk_idx, const uint8_t* kept, const float* topk_w,
+    int32_t* counts, int32_t* offsets, int32_t* pair_token, int32_t* pair_rank, float* pair_w,
+    int32_t* pair_pos, int32_t* n_pruned) {
+  build_lists(T, E, k, topk_idx, kept, topk_w, counts, offsets, pair_token, pair_rank, pair_w,
+              pair_pos, n_pruned);
+}
+
+// Small batches: both phases in one workgroup (one launch).
+__global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
+    const float* __restrict__ logits, const uint8_t* __restrict__ important, int T, int E, int k,
+    float delta32, double tau, int32_t* topk_idx, float* topk_w, uint8_t* kept, int32_t* counts,
+    int32_t* offsets, int32_t* pair_token, int32_t* pair_rank, float* pair_w, int32_t* pair_pos,
+    int32_t* n_pruned) {
+  const int nwaves = blockDim.x >> 6;
+  for (int t = threadIdx.x >> 6; t < T; t += nwaves)
+    select_token(logits, important, t, E, k, delta32, tau, topk_idx, topk_w, kept, pair_pos);
+  __threadfence_block();
+  __syncthreads();
+  build_lists(T, E, k, topk_idx, kept, topk_w, counts, offsets, pair_token, pair_rank, pair_w,
+              pair_pos, n_pruned);
+}
+
+hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,
+                        const mc_routing& r, hipStream_t stream) {
+  if (r.T <= kRouteFusedMaxT) {
+    hipLaunchKernelGGL(route_fused_kernel, dim3(1), dim3(kCsrThreads), 0, stream, logits,
+                       important, r.T, r.E, r.k, delta32, tau, r.topk_idx, r.topk_w, r.kept,
+                       r.counts, r.offsets, r.pair_token, r.pair_rank, r.pair_w, r.pair_pos,
+                       r.n_pruned);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(route_select_kernel, dim3((r.T + 3) / 4), dim3(256), 0, stream, logits,
+                     important, r.T, r.E, r.k, delta32, tau, r.topk_idx, r.topk_w, r.kept,
+                     r.pair_pos);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(route_lists_kernel, dim3(1), dim3(kCsrThreads), 0, stream, r.T, r.E, r.k,
+                     r.topk_idx, r.kept, r.topk_w, r.counts, r.offsets, r.pair_token,
+                     r.pair_rank, r.pair_w, r.pair_pos, r.n_pruned);
+  return hipGetLastError();
+}
+
+}  // namespace mc

@@ -1,0 +1,265 @@
+"""GPU parity: the HIP path through the C-ABI against the CPU oracle.
+
+Bit-exact: packed words, scale/zero words, exported codes and fp16
+dequantized values, expert selections, kept flags, per-expert lists.
+Tolerance (bf16 outputs, fp64 oracle): MAE of |y - bf16(y_ref)| <= 1e-3 and
+max |y - y_ref| / max(|y_ref|, rms(y_ref)) <= 2e-2.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synthetic
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def mc():
+    import paper_2410_06270_amd as m
+    m.load()
+    return m
+
+
+def to_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def u32(t):
+    return t.cpu().numpy().view(np.uint32)
+
+
+def pack_gpu(mc, mats, bits, G):
+    E = len(mats)
+    ffn, d = mats[0][0].shape
+    wg = to_dev(np.stack([m[0] for m in mats]))
+    wu = to_dev(np.stack([m[1] for m in mats]))
+    wd = to_dev(np.stack([m[2] for m in mats]))
+    L = mc.PackedLayer(E, d, ffn, bits, G)
+    mc.pack(wg, wu, wd, L)
+    torch.cuda.synchronize()
+    return L
+
+
+def special_matrices(E, d, ffn, seed=0):
+    """Weights with adversarial groups: exact midpoints, constant groups, signed
+    zeros, tiny and huge ranges."""
+    g = np.random.default_rng(seed)
+    mats = []
+    for e in range(E):
+        per = []
+        for shape in ((ffn, d), (ffn, d), (d, ffn)):
+            W = (g.standard_normal(shape) * 0.02).astype(np.float32)
+            W[0, :32] = 0.25                                   # constant group
+            W[1, :32] = np.where(np.arange(32) % 2, 0.0, -0.0)  # signed zeros
+            W[2, :32] = np.arange(32) / 31.0 * 0.75            # coarse grid
+            W[2, 5] = 0.125
+            W[3, :32] = g.standard_normal(32) * 1e-6           # tiny range (s rounds to 0?)
+            W[4, :32] = g.standard_normal(32) * 3e4            # huge range (saturating s/z)
+            W[5, :32] = np.float32(7.0)
+            W[5, 0] = 0.0                                      # min 0, max 7 (ties at x.5)
+            W[5, 1:8] = np.array([0.5, 1.5, 2.5, 3.5, 4.5, 5.5, 6.5], np.float32)
+            per.append(W)
+        mats.append(tuple(per))
+    return mats
+
+
+@pytest.mark.parametrize("case", ["tiny", "special", "olmoe8"])
+def test_pack_bit_exact(mc, case):
+    if case == "tiny":
+        c = synthetic.config(1)
+        mats = synthetic.layer_weights(1)
+        bits, G = c["bits"], c["G"]
+    elif case == "special":
+        mats = special_matrices(3, 256, 128)
+        bits, G = [1, 2, 3], 32
+    else:
+        c = synthetic.config(4)
+        mats = synthetic.layer_weights(4, E=8)
+        bits, G = c["bits"][:8], c["G"]
+    words, sz, logical = oracle.pack_layer(mats, bits, G)
+    L = pack_gpu(mc, mats, bits, G)
+    np.testing.assert_array_equal(u32(L.sz), sz)
+    np.testing.assert_array_equal(u32(L.words), words)
+    for e in range(len(mats)):
+        for m in range(3):
+            q, s, z = logical[e][m]
+            codes = torch.empty(q.shape, dtype=torch.uint8, device="cuda")
+            mc.codes_export(L, e, m, codes)
+            deq = torch.empty(q.shape, dtype=torch.float16, device="cuda")
+            mc.dequant_export(L, e, m, deq)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(codes.cpu().numpy(), q)
+            np.testing.assert_array_equal(deq.cpu().numpy().view(np.uint16),
+                                          oracle.dequant_f16(q, s, z, G))
+
+
+def route_gpu(mc, logits, imp, k, tau):
+    T, E = logits.shape
+    r = mc.Routing(T, E, k)
+    mc.route_and_prune(to_dev(logits), None if imp is None else to_dev(imp), tau, r)
+    torch.cuda.synchronize()
+    return r
+
+
+def assert_routing_equal(r, ref, T, k):
+    np.testing.assert_array_equal(r.topk_idx.cpu().numpy(), ref["topk_idx"])
+    np.testing.assert_array_equal(r.kept.cpu().numpy(), ref["kept"])
+    np.testing.assert_array_equal(r.counts.cpu().numpy(), ref["counts"])
+    np.testing.assert_array_equal(r.offsets.cpu().numpy(), ref["offsets"])
+    n = int(ref["offsets"][-1])
+    np.testing.assert_array_equal(r.pair_token.cpu().numpy()[:n], ref["pair_token"][:n])
+    np.testing.assert_array_equal(r.pair_rank.cpu().numpy()[:n], ref["pair_rank"][:n])
+    np.testing.assert_array_equal(r.pair_pos.cpu().numpy(), ref["pair_pos"])
+    assert int(r.n_pruned.cpu()[0]) == ref["n_pruned"]
+    np.testing.assert_allclose(r.topk_w.cpu().numpy(), ref["topk_w"], rtol=2e-7, atol=1e-30)
+    np.testing.assert_allclose(r.pair_w.cpu().numpy()[:n], ref["pair_w"][:n], rtol=2e-7, atol=1e-30)
+
+
+def assert_margin(logits, imp, k, tau):
+    """For k > 2 the pruning test runs in fp64 on both sides with different exp
+    implementations: no normalised weight may sit within 1e-9 of tau."""
+    if k <= 2 or tau == 0:
+        return
+    for t in range(logits.shape[0]):
+        l = np.sort(logits[t].astype(np.float64))[::-1][:k]
+        p = np.exp(l - l[0])
+        p /= p.sum()
+        assert np.all(np.abs(p[1:] - tau) > 1e-9 * tau), t
+
+
+@pytest.mark.parametrize("cid,T,tau", [
+    (1, 64, 0.3), (2, 1, 0.3), (2, 8, 0.3), (2, 32, 0.3), (3, 4096, 0.0), (3, 4096, 0.2),
+    (3, 4096, 0.4), (4, 2048, 0.05), (4, 16, 0.05), (4, 300, 0.05), (1, 5000, 0.3),
+])
+def test_route_bit_exact(mc, cid, T, tau):
+    c = synthetic.config(cid)
+    logits = synthetic.logits(cid, T)
+    logits[::5, 1] = logits[::5, 0]                 # exact ties
+    imp = synthetic.important_mask(cid, T)
+    assert_margin(logits, imp, c["k"], tau)
+    ref = oracle.route(logits, imp, c["k"], tau)
+    r = route_gpu(mc, logits, imp, c["k"], tau)
+    assert_routing_equal(r, ref, T, c["k"])
+
+
+def test_route_edge_cases(mc):
+    g = np.random.default_rng(9)
+    # k = 1 (nothing to prune), k = E, E = 256, signed zeros, no mask, tau = 1
+    for T, E, k, tau, imp in ((7, 4, 1, 0.3, None), (9, 8, 8, 0.1, None), (33, 256, 8, 0.02, None),
+                              (12, 8, 2, 1.0, None), (12, 8, 2, 0.0, None), (3, 1, 1, 0.5, None)):
+        lg = g.standard_normal((T, E)).astype(np.float32)
+        lg[0, :] = 0.0
+        lg[1, ::2] = -0.0
+        assert_margin(lg, imp, k, tau)
+        ref = oracle.route(lg, imp, k, tau)
+        r = route_gpu(mc, lg, imp, k, tau)
+        assert_routing_equal(r, ref, T, k)
+
+
+def layer_case(cid=1, E=None, bits=None, d=None, ffn=None):
+    c = synthetic.config(cid)
+    E = E or c["E"]
+    d = d or c["d"]
+    ffn = ffn or c["ffn"]
+    bits = bits or c["bits"][:E]
+    mats = synthetic.layer_weights(cid, E=E, d=d, ffn=ffn)
+    _, _, logical = oracle.pack_layer(mats, bits, c["G"])
+    return mats, bits, c["G"], logical
+
+
+def forward_gpu(mc, L, x_bits, logits, imp, k, tau):
+    T, E = logits.shape
+    r = route_gpu(mc, logits, imp, k, tau)
+    y = torch.empty((T, L.d), dtype=torch.int16, device="cuda")
+    ws = torch.empty(mc.forward_workspace(T, E, k, L.d, L.ffn), dtype=torch.uint8, device="cuda")
+    mc.moe_forward(to_dev(x_bits.view(np.int16)), r, L, y, ws)
+    torch.cuda.synchronize()
+    return y.cpu().numpy().view(np.uint16), r
+
+
+def check_tol(y_bits, y_ref):
+    g = oracle.bf16_to_float64(y_bits)
+    rb = oracle.bf16_to_float64(oracle.bf16_round_array(y_ref))
+    mae = np.abs(g - rb).mean()
+    rms = np.sqrt((y_ref ** 2).mean())
+    maxrel = (np.abs(g - y_ref) / np.maximum(np.abs(y_ref), rms)).max()
+    assert mae <= 1e-3, (mae, maxrel)
+    assert maxrel <= 2e-2, (mae, maxrel)
+    return mae, maxrel
+
+
+@pytest.fixture(scope="module")
+def tiny(mc):
+    mats, bits, G, logical = layer_case(1)
+    L = pack_gpu(mc, mats, bits, G)
+    return L, logical, G
+
+
+@pytest.mark.parametrize("T", [1, 2, 16, 17, 33, 64, 65, 200])
+def test_forward_tiny_tolerance(mc, tiny, T):
+    L, logical, G = tiny
+    x = synthetic.activations(1, T)
+    lg = synthetic.logits(1, T)
+    imp = synthetic.important_mask(1, T)
+    y, _ = forward_gpu(mc, L, x, lg, imp, 2, 0.3)
+    ref = oracle.route(lg, imp, 2, 0.3)
+    y_ref = oracle.moe_forward(x, ref, logical, G)
+    mae, maxrel = check_tol(y, y_ref)
+    # the decode and prefill paths dequantize exactly: the error is far below the bar
+    assert mae < 2e-4, mae
+
+
+def test_forward_skewed_and_dense(mc, tiny):
+    """All tokens on one expert (full token chunks), then tau = 0 with every
+    token protected (dense top-k)."""
+    L, logical, G = tiny
+    T = 64
+    x = synthetic.activations(1, T)
+    lg = synthetic.logits(1, T)
+    lg[:, 2] += 20.0
+    for imp, tau in ((None, 0.3), (np.ones(T, np.uint8), 0.0)):
+        y, _ = forward_gpu(mc, L, x, lg, imp, 2, tau)
+        y_ref = oracle.moe_forward(x, oracle.route(lg, imp, 2, tau), logical, G)
+        check_tol(y, y_ref)
+
+
+def test_forward_single_expert_k1(mc):
+    mats, bits, G, logical = layer_case(1, E=1, bits=[3])
+    L = pack_gpu(mc, mats, bits, G)
+    T = 24
+    x = synthetic.activations(1, T)
+    lg = np.zeros((T, 1), np.float32)
+    y, _ = forward_gpu(mc, L, x, lg, None, 1, 0.3)
+    y_ref = oracle.moe_forward(x, oracle.route(lg, None, 1, 0.3), logical, G)
+    check_tol(y, y_ref)
+
+
+def test_forward_olmoe_shaped_small(mc):
+    """64 experts, top-8, G = 64, d = 2048 / ffn = 1024 at a reduced expert count
+    of the real shape (16 experts) and 16 decode tokens."""
+    c = synthetic.config(4)
+    E = 16
+    mats, bits, G, logical = layer_case(4, E=E)
+    L = pack_gpu(mc, mats, bits, G)
+    T = 16
+    x = synthetic.activations(4, T)
+    lg = synthetic.logits(4, T)[:, :E].copy()
+    imp = synthetic.important_mask(4, T)
+    assert_margin(lg, imp, 8, 0.05)
+    y, _ = forward_gpu(mc, L, x, lg, imp, 8, 0.05)
+    y_ref = oracle.moe_forward(x, oracle.route(lg, imp, 8, 0.05), logical, G)
+    check_tol(y, y_ref)
+
+
+def test_forward_deterministic(mc, tiny):
+    L, logical, G = tiny
+    T = 64
+    x = synthetic.activations(1, T)
+    lg = synthetic.logits(1, T)
+    imp = synthetic.important_mask(1, T)
+    y1, _ = forward_gpu(mc, L, x, lg, imp, 2, 0.3)
+    y2, _ = forward_gpu(mc, L, x, lg, imp, 2, 0.3)
+    np.testing.assert_array_equal(y1, y2)
