@@ -1,0 +1,272 @@
+#!/usr/bin/env python3
+"""Benchmark of the MC expert path on one MI355X.
+
+Workload (the paper's Mixtral 8x7b MoE layer shape, synthetic data): d=4096,
+ffn=14336, 8 experts, top-2, expert widths [3,3,3,2,2,2,2,3] (2.5 code bits,
+the paper's 2.54-bit setting), G=128, decode batch of T tokens (default 32),
+bf16 activations N(0,1), logits N(0,1) + per-expert bias N(0,0.5^2),
+prune threshold 0.3, round(0.1*T) protected tokens.
+
+One step = route_and_prune + moe_forward over the batch for one layer.  The
+step rotates over --copies packed copies of the layer (>= 4 x 484 MB) so the
+weights come from HBM, not from the 256 MB Infinity Cache.  Prints ONE JSON
+line.  Per-kernel durations come from the library's HIP-event instrumentation
+on the launch stream, recorded over a second pass of the same timed steps.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+METRIC = "MoE-layer tokens/s + achieved HBM GB/s (decode) / MFMA % (prefill), 1 GPU"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--tokens", type=int, default=32)
+    p.add_argument("--copies", type=int, default=4)
+    p.add_argument("--sweep", default="1,8", help="extra decode batch sizes to report")
+    p.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    return p.parse_args()
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2410_06270_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def expert_bytes(d, ffn, G, b, mats=(0, 1, 2)):
+    """Packed codes + scale/zero words of the listed matrices of one expert."""
+    return len(mats) * (d * ffn * b // 8 + d * ffn // G * 4)
+
+
+class Workload:
+    def __init__(self, mc, torch, synthetic, T, copies):
+        c = synthetic.config(2)
+        self.c, self.T = c, T
+        E, d, ffn, k, G, bits = c["E"], c["d"], c["ffn"], c["k"], c["G"], c["bits"]
+        self.layers = []
+        for cp in range(copies):
+            gen = torch.Generator(device="cuda")
+            gen.manual_seed(synthetic.BASE_SEED + 2 + 1000 * cp)
+            w = [torch.randn((E, ffn, d) if m < 2 else (E, d, ffn), generator=gen, device="cuda",
+                             dtype=torch.float32).mul_(0.02) for m in range(3)]
+            L = mc.PackedLayer(E, d, ffn, bits, G)
+            mc.pack(w[0], w[1], w[2], L)
+            del w
+            self.layers.append(L)
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        self.set_tokens(mc, torch, synthetic, T)
+
+    def set_tokens(self, mc, torch, synthetic, T):
+        c = self.c
+        self.T = T
+        dev = lambda a: torch.from_numpy(a).cuda()
+        self.x = dev(synthetic.activations(2, T).view("int16"))
+        self.logits = dev(synthetic.logits(2, T))
+        self.imp = dev(synthetic.important_mask(2, T))
+        self.r = mc.Routing(T, c["E"], c["k"])
+        self.y = torch.empty((T, c["d"]), dtype=torch.int16, device="cuda")
+        self.ws = torch.empty(mc.forward_workspace(T, c["E"], c["k"], c["d"], c["ffn"]),
+                              dtype=torch.uint8, device="cuda")
+
+    def step(self, mc, i):
+        mc.route_and_prune(self.logits, self.imp, self.c["tau"][0], self.r)
+        mc.moe_forward(self.x, self.r, self.layers[i % len(self.layers)], self.y, self.ws)
+
+    def touched(self):
+        counts = self.r.counts.cpu().tolist()
+        return [e for e, n in enumerate(counts) if n > 0], int(self.r.n_pruned.cpu()[0])
+
+    def alg_bytes(self):
+        c = self.c
+        d, ffn, G, E = c["d"], c["ffn"], c["G"], c["E"]
+        touched, _ = self.touched()
+        gateup = sum(expert_bytes(d, ffn, G, c["bits"][e], (0, 1)) for e in touched)
+        down = sum(expert_bytes(d, ffn, G, c["bits"][e], (2,)) for e in touched)
+        act = self.T * d * 2            # x in (gate/up) and y out (combine)
+        logits = self.T * E * 4
+        return dict(gateup=gateup + act, down=down, combine=act, step=gateup + down + 2 * act + logits)
+
+
+def time_steps(mc, torch, wl, steps, warmup):
+    for i in range(warmup):
+        wl.step(mc, i)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record()
+    for i in range(steps):
+        wl.step(mc, i)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return ev0.elapsed_time(ev1) / steps, wall
+
+
+def kernel_times(mc, torch, wl, steps):
+    mc.timing_enable(True)
+    for i in range(steps):
+        wl.step(mc, i)
+    torch.cuda.synchronize()
+    out = {}
+    for name in ("route_fused", "route_select", "route_lists", "gateup", "down", "combine"):
+        ms, n = mc.timing_read(name)
+        if n:
+            out[name] = dict(avg_us=1e3 * ms / n, launches=n)
+    mc.timing_enable(False)
+    return out
+
+
+def traffic_from_profiles(kernel, workload, hash_now):
+    """HBM bytes per launch measured with rocprofv3 counters (stored summary),
+    or None when no summary matches the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            rec = json.load(f).get("%s/%s" % (kernel, workload))
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_hash") != hash_now:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(synthetic, T):
+    """The oracle on the same decode batch and layer shape: routing of all T
+    tokens and the SwiGLU forward over every kept pair, on random codes and
+    fp16 scale/zero of the real shapes (the timing does not depend on values)."""
+    import numpy as np
+    import oracle
+    c = synthetic.config(2)
+    E, d, ffn, k, G, bits, tau = c["E"], c["d"], c["ffn"], c["k"], c["G"], c["bits"], c["tau"][0]
+    lg = synthetic.logits(2, T)
+    imp = synthetic.important_mask(2, T)
+    x = synthetic.activations(2, T)
+    g = np.random.default_rng(7)
+    t_route = time.perf_counter()
+    rt = oracle.route(lg, imp, k, tau)
+    t_route = time.perf_counter() - t_route
+    logical = []
+    for e in range(E):
+        if rt["counts"][e] == 0:
+            logical.append(None)
+            continue
+        per = []
+        for m in range(3):
+            R, K = (ffn, d) if m < 2 else (d, ffn)
+            q = g.integers(0, 2 ** bits[e], (R, K), dtype=np.uint8)
+            s = (np.abs(g.standard_normal((R, K // G))) * 0.01 + 1e-3).astype(np.float16).view(np.uint16)
+            z = g.uniform(0, 2 ** bits[e] - 1, (R, K // G)).astype(np.float16).view(np.uint16)
+            per.append((q, s, z))
+        logical.append(per)
+    t0 = time.perf_counter()
+    oracle.moe_forward(x, rt, logical, G)
+    el = time.perf_counter() - t0 + t_route
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return dict(value=T / el, unit="tokens/s", cores=threads, kind="oracle",
+                seconds=round(el, 3),
+                sample="the full T=%d decode batch: routing + SwiGLU forward over its %d kept "
+                       "pairs on the d=4096/ffn=14336/E=8 layer (random codes, same shapes)"
+                       % (T, int(rt["counts"].sum())))
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus > 1 or world > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the sharding design is described in DESIGN.md); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2410_06270_amd as mc
+    import synthetic
+
+    mc.load()
+    torch.cuda.set_device(0)
+    wl = Workload(mc, torch, synthetic, args.tokens, args.copies)
+    c = wl.c
+    hash_now = source_hash()
+
+    def measure(T):
+        wl.set_tokens(mc, torch, synthetic, T)
+        ms, wall = time_steps(mc, torch, wl, args.steps, args.warmup)
+        kt = kernel_times(mc, torch, wl, args.steps)
+        ab = wl.alg_bytes()
+        touched, pruned = wl.touched()
+        return dict(T=T, ms=ms, wall=wall, kernels=kt, alg=ab, touched=touched, pruned=pruned)
+
+    sweep = []
+    for t in [int(v) for v in args.sweep.split(",") if v]:
+        if t != args.tokens:
+            m = measure(t)
+            sweep.append(dict(tokens=t, tokens_per_s=round(t / (m["ms"] / 1e3), 1),
+                              ms_per_step=round(m["ms"], 5),
+                              step_hbm_gbs=round(m["alg"]["step"] / (m["ms"] * 1e6), 1),
+                              gateup_hbm_frac=round(m["alg"]["gateup"] / (m["kernels"]["gateup"]["avg_us"] * 1e3) / HBM_PEAK_GBS, 4),
+                              experts_touched=len(m["touched"])))
+    main_m = measure(args.tokens)
+    ms = main_m["ms"]
+    T = args.tokens
+    kt = main_m["kernels"]
+    ab = main_m["alg"]
+    gu_us = kt["gateup"]["avg_us"]
+    achieved = ab["gateup"] / (gu_us * 1e3)        # GB/s
+    traffic = traffic_from_profiles("gateup", "mixtral_decode_T%d" % T, hash_now)
+    roofline = dict(bound="hbm", kernel="gateup", achieved=round(achieved, 1), peak=HBM_PEAK_GBS,
+                    unit="GB/s", frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
+                    alg_bytes_per_launch=ab["gateup"], avg_launch_us=round(gu_us, 3))
+    out = {
+        "metric": METRIC,
+        "value": round(T / (ms / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "mixtral_8x7b_moe_layer_decode", "d": c["d"], "ffn": c["ffn"],
+                   "experts": c["E"], "top_k": c["k"], "bits": c["bits"], "group": c["G"],
+                   "tokens": T, "tau": c["tau"][0], "protected": int(synthetic.important_mask(2, T).sum()),
+                   "layer_copies": args.copies},
+        "step_hbm_gbs": round(ab["step"] / (ms * 1e6), 1),
+        "step_hbm_frac": round(ab["step"] / (ms * 1e6) / HBM_PEAK_GBS, 4),
+        "experts_touched": len(main_m["touched"]),
+        "pairs_pruned": main_m["pruned"],
+        "roofline": roofline,
+        "kernels_us": {k2: round(v["avg_us"], 3) for k2, v in kt.items()},
+        "sweep": sweep,
+        "source_hash": hash_now,
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(synthetic, T)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -155,6 +155,16 @@ mc_status mc_moe_forward(const uint16_t *x_bf16, const mc_routing *r,
                          const mc_layer *L, uint16_t *y_bf16, void *workspace,
                          size_t ws_bytes, void *stream);
 
+/* Instrumentation.  mc_timing_enable(1) clears the record and brackets every
+ * kernel launch made afterwards by two HIP events on the launch stream;
+ * mc_timing_enable(0) stops recording.  mc_timing_read waits for the recorded
+ * events of one kernel and returns the summed duration in ms and the number
+ * of launches.  Kernel names: pack_scale_zero, pack_codes, export,
+ * route_fused, route_select, route_lists, gateup, down, combine.
+ * Errors: MC_EINVAL (unknown name, NULL pointer), MC_EHIP. */
+mc_status mc_timing_enable(int on);
+mc_status mc_timing_read(const char *kernel, double *total_ms, int *launches);
+
 /* Message for the last non-OK status returned on this thread. */
 const char *mc_last_error(void);
 

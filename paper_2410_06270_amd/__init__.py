@@ -18,4 +18,6 @@ from ._binding import (  # noqa: F401
     pack,
     pack_sizes,
     route_and_prune,
+    timing_enable,
+    timing_read,
 )

@@ -73,6 +73,11 @@ def load():
         lib.mc_moe_forward.restype = st
         lib.mc_moe_forward.argtypes = [P, ctypes.POINTER(_Routing), ctypes.POINTER(_Layer), P, P,
                                        S, P]
+        lib.mc_timing_enable.restype = st
+        lib.mc_timing_enable.argtypes = [I]
+        lib.mc_timing_read.restype = st
+        lib.mc_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(I)]
         _lib = lib
     return _lib
 
@@ -177,3 +182,14 @@ def moe_forward(x, routing: Routing, layer: PackedLayer, y, workspace, stream=No
     _check(load().mc_moe_forward(_ptr(x), ctypes.byref(routing.desc), ctypes.byref(layer.desc),
                                  _ptr(y), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                  _stream(stream)))
+
+
+def timing_enable(on: bool = True):
+    _check(load().mc_timing_enable(1 if on else 0))
+
+
+def timing_read(kernel: str):
+    """(summed ms, launches) of the events recorded for one kernel."""
+    ms, n = ctypes.c_double(), ctypes.c_int()
+    _check(load().mc_timing_read(kernel.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value

@@ -187,4 +187,16 @@ mc_status mc_moe_forward(const uint16_t* x_bf16, const mc_routing* r, const mc_l
                     "mc_moe_forward launch");
 }
 
+mc_status mc_timing_enable(int on) {
+  mc::timing_enable(on);
+  return MC_OK;
+}
+
+mc_status mc_timing_read(const char* kernel, double* total_ms, int* launches) {
+  if (!kernel || !total_ms || !launches) return fail(MC_EINVAL, "NULL argument");
+  const int site = mc::timing_site(kernel);
+  if (site < 0) return fail(MC_EINVAL, "unknown kernel name '%s'", kernel);
+  return hip_status(mc::timing_read(site, total_ms, launches), "mc_timing_read");
+}
+
 }  // extern "C"

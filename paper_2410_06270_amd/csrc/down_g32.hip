@@ -1,0 +1,7 @@
+// down_g32.hip -- down-projection kernels for quantization groups of 32 columns.
+#include "fwd_kernels.hpp"
+
+namespace mc {
+template hipError_t launch_down<4>(const uint16_t*, size_t, const LayerArgs&, const mc_routing&,
+                                    int, float*, size_t, int, int, hipStream_t);
+}  // namespace mc

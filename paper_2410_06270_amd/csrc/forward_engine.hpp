@@ -1,0 +1,319 @@
+// forward_engine.hpp -- Eq. 1 over packed SwiGLU experts (dequantization in registers).
+//
+// y_t = sum over kept ranks r of w_r * E_{e_r}(x_t),
+// E_e(x) = W_down (silu(W_gate x) * (W_up x)), weights s*(q - z) per group.
+//
+// The codes go straight into bf16 MFMA operands as 128 + q (exact), so the
+// dequantized weight is never rounded: for each group g of G inputs
+//   sum_k s (q_k - z) x_k = s * (acc_g - (128 + z) * sum_k x_k),
+// acc_g = sum_k (128 + q_k) x_k from the MFMA; the group sums of x are formed
+// once per workgroup in LDS.  The hidden vector h is kept as two bf16 planes
+// (h = hi + lo, ~16 significant bits) for the down projection.
+//
+// Kernels (all on the caller's stream, no host synchronisation; experts with
+// no kept token exit at once because the counts are read on the device):
+//   gateup_kernel  grid (ffn/64, E, chunks): 4 waves x 16 rows of gate and up,
+//                  up to 16*NTMAX tokens of one expert per chunk -> h planes;
+//   down_kernel    grid (d/128, E, chunks*S): 4 waves x 32 rows, split-K over
+//                  ffn -> fp32 partials;
+//   combine_kernel grid (d/256, T): y = bf16(sum_r w_r sum_s partial), fixed
+//                  order, so the result is deterministic.
+#pragma once
+
+#include "mc_internal.hpp"
+
+namespace mc {
+
+constexpr uint32_t kMagic2 = 0x43004300u;     // bf16 128.0 in both halves
+constexpr int kRowPad = 8;                    // bf16 elements of padding per slab row
+constexpr int kSxBytes = 8 * 1024;            // group sums of the staged slab (LDS)
+
+// LDS for the staged activation slab: up to 16 tokens (batches of <= 16) or 64.
+// 34 KB holds 16 tokens x 2 planes x 512 columns; 68 KB holds 64 x 2 x 256.
+constexpr int kXsBytesSmall = 34 * 1024;
+constexpr int kXsBytesLarge = 68 * 1024;
+// Chunks (16 rows x 128 columns of codes) kept in flight per stream, by the
+// number of 16-token blocks and of groups per chunk (the slab is a multiple
+// of this many chunks); deeper rings cost registers the wider variants lack.
+__host__ __device__ constexpr int prefetch_depth(int ntb, int gpc = 1) {
+  return (ntb >= 3 || gpc >= 4) ? 2 : 4;
+}
+// Smallest slab (one ring of chunks) of the worst case of each token-block
+// count must fit the LDS budget: planes x tokens x (columns + pad) x 2 bytes.
+constexpr int slab_floor_bytes(int ntb, int planes) {
+  return planes * 16 * ntb * (prefetch_depth(ntb) * kTileCols + kRowPad) * 2;
+}
+static_assert(slab_floor_bytes(1, 2) <= kXsBytesSmall, "LDS budget (<= 16 tokens)");
+static_assert(slab_floor_bytes(2, 2) <= kXsBytesLarge, "LDS budget (<= 32 tokens)");
+static_assert(slab_floor_bytes(3, 2) <= kXsBytesLarge, "LDS budget (<= 48 tokens)");
+static_assert(slab_floor_bytes(4, 2) <= kXsBytesLarge, "LDS budget (<= 64 tokens)");
+// Group sums: 16*ntb rows x (slab / G) groups x 4 bytes; the slab is capped by
+// kSxBytes, which must allow at least one ring of chunks at G = 32.
+static_assert((kSxBytes / (4 * 64)) * 32 >= 2 * kTileCols, "group-sum budget");
+
+__device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
+
+__device__ __forceinline__ bf16x8 load_a(const uint16_t* p, bool valid) {
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (valid) v = *reinterpret_cast<const u32x4*>(p);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+template <int BITS>
+__device__ __forceinline__ bf16x8 b_operand(const uint32_t* w, int u) {
+  u32x4 v;
+  v[0] = extract_pair<BITS>(w, 4 * u + 0, kMagic2);
+  v[1] = extract_pair<BITS>(w, 4 * u + 1, kMagic2);
+  v[2] = extract_pair<BITS>(w, 4 * u + 2, kMagic2);
+  v[3] = extract_pair<BITS>(w, 4 * u + 3, kMagic2);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ float sum8_bf16(u32x4 v) {
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    s += __uint_as_float(v[i] << 16);
+    s += __uint_as_float(v[i] & 0xffff0000u);
+  }
+  return s;
+}
+
+// Group epilogue: tot += s * (acc - (128 + z) * sum_x); acc = 0.
+__device__ __forceinline__ void group_end(f32x4& acc, f32x4& tot, uint32_t szw, const float* sx4p) {
+  const float s = half_bits_to_float(szw & 0xffffu);
+  const float c = 128.0f + half_bits_to_float(szw >> 16);
+  const f32x4 sx = *reinterpret_cast<const f32x4*>(sx4p);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float t = fmaf(-c, sx[i], acc[i]);
+    tot[i] = fmaf(s, t, tot[i]);
+    acc[i] = 0.0f;
+  }
+}
+
+// Two weight streams per wave (gate and up rows of one block, or two row
+// blocks of down) share every activation fragment.  Each stream reads through
+// a buffer resource that covers exactly its chunks [c_begin, c_end): the chunk
+// offset is wave-uniform and the lane offset is one VGPR.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcWord3 = 0x00020000;   // raw 32-bit buffer (gfx9 family)
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRsrcWord3);
+}
+
+struct Streams {
+  rsrc_t w[2];        // packed words of chunks [c_begin, c_end) of the stream's row block
+  rsrc_t s[2];        // scale/zero words of the same groups
+  uint32_t lane_w;    // byte offset of this lane's words inside a chunk
+  uint32_t lane_s;    // byte offset of this lane's scale/zero word inside a group
+};
+
+template <int BITS>
+__device__ __forceinline__ void load_words(uint32_t (&w)[BITS], rsrc_t r, uint32_t off) {
+  if constexpr (BITS == 1) {
+    w[0] = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+  } else if constexpr (BITS == 2) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+    w[0] = v[0];
+    w[1] = v[1];
+  } else {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b96(r, off, 0, 0);
+    w[0] = v[0];
+    w[1] = v[1];
+    w[2] = v[2];
+  }
+}
+
+// Loads chunk min(cc, last) (relative to c_begin) so that the ring refill is
+// unconditional (no control flow around the in-flight registers); refills
+// past the end re-read the last chunk and are never consumed.
+template <int BITS, int GPC>
+__device__ __forceinline__ void load_chunk(uint32_t (&w)[2][BITS], uint32_t (&s)[2][GPC],
+                                           const Streams& st, int cc, int last) {
+  const uint32_t c = (uint32_t)(cc < last ? cc : last);
+  const uint32_t ow = st.lane_w + c * (64u * BITS * 4u);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) load_words<BITS>(w[j], st.w[j], ow);
+#pragma unroll
+  for (int q = 0; q < GPC; ++q) {
+    const uint32_t os = st.lane_s + (c * GPC + q) * 64u;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) s[j][q] = __builtin_amdgcn_raw_buffer_load_b32(st.s[j], os, 0, 0);
+  }
+}
+
+// Copy rows [nt][ks, ks+kw) of every plane into LDS and form the sums of each
+// group of G columns (lanes of a wave hold consecutive 8-column pieces of one
+// row, so a group is G/8 neighbouring lanes: butterfly in a fixed order).
+template <int PLANES, typename RowFn>
+__device__ __forceinline__ void stage_slab(uint16_t* xs, float* sxs, RowFn rowsrc,
+                                           size_t plane_stride, int nt, int rows, int ks, int kw,
+                                           int RS, int G) {
+  const int lane = threadIdx.x & 63;
+  const int pieces = kw >> 3;
+  const int total = nt * pieces;
+  const int gp = G >> 3;
+  for (int base = threadIdx.x & ~63; base < total; base += blockDim.x) {
+    const int idx = base + lane;
+    const bool valid = idx < total;
+    int m = 0, p = 0;
+    float sum = 0.0f;
+    if (valid) {
+      m = idx / pieces;
+      p = idx - m * pieces;
+#pragma unroll
+      for (int pl = 0; pl < PLANES; ++pl) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(rowsrc(m) + pl * plane_stride + ks + 8 * p);
+        *reinterpret_cast<u32x4*>(xs + (size_t)(pl * nt + m) * RS + 8 * p) = v;
+        sum += sum8_bf16(v);
+      }
+    }
+    for (int off = 1; off < gp; off <<= 1) sum += __shfl_xor(sum, off);
+    if (valid && (p % gp) == 0) sxs[(p / gp) * rows + m] = sum;
+  }
+  __syncthreads();
+}
+
+template <int BITS, int NT, int PLANES, int GPC>
+__device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
+                                              const uint32_t (&s)[2][GPC], f32x4 (&acc)[2][NT],
+                                              f32x4 (&tot)[2][NT], const uint16_t* xs,
+                                              const float* sxs, int lc, int nt, int RS, int lane) {
+  constexpr int SPG = 4 / GPC;   // MFMA steps per quantization group
+  constexpr int rows = 16 * NT;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const bf16x8 b0 = b_operand<BITS>(w[0], u);
+    const bf16x8 b1 = b_operand<BITS>(w[1], u);
+    const int kk = lc * kTileCols + 32 * u + 8 * (lane >> 4);
+#pragma unroll
+    for (int tb = 0; tb < NT; ++tb) {
+      const int m = tb * 16 + (lane & 15);
+#pragma unroll
+      for (int pl = 0; pl < PLANES; ++pl) {
+        const bf16x8 a = load_a(xs + (size_t)(pl * nt + m) * RS + kk, m < nt);
+        acc[0][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b0, acc[0][tb], 0, 0, 0);
+        acc[1][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b1, acc[1][tb], 0, 0, 0);
+      }
+    }
+    if ((u + 1) % SPG == 0) {
+      const int q = (u + 1) / SPG - 1;
+      const int gl = lc * GPC + q;
+#pragma unroll
+      for (int tb = 0; tb < NT; ++tb) {
+        const float* sxp = sxs + gl * rows + tb * 16 + 4 * (lane >> 4);
+        group_end(acc[0][tb], tot[0][tb], s[0][q], sxp);
+        group_end(acc[1][tb], tot[1][tb], s[1][q], sxp);
+      }
+    }
+  }
+}
+
+// Stream chunks [c_begin, c_end) of two weight streams against the staged
+// activations of nt (<= 16*NT) tokens; a ring of D chunks of packed words and
+// scale/zero words stays in flight in registers across chunk and slab
+// boundaries.
+template <int BITS, int NT, int PLANES, int GPC, typename RowFn>
+__device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int c_end,
+                                            RowFn rowsrc, size_t plane_stride, int nt, int G,
+                                            uint16_t* xs, float* sxs, int xs_elems,
+                                            f32x4 (&tot)[2][NT]) {
+  constexpr int D = prefetch_depth(NT, GPC);
+  constexpr int rows = 16 * NT;
+  const int lane = threadIdx.x & 63;
+  int ks = xs_elems / (PLANES * nt) - kRowPad;
+  const int ks_sx = (kSxBytes / (4 * rows)) * G;
+  ks = ks < ks_sx ? ks : ks_sx;
+  const int unit = D * kTileCols;
+  ks = (ks / unit) * unit;
+  if (ks < unit) ks = unit;               // the host's LDS budget makes this fit
+  const int slab_chunks = ks / kTileCols;
+  const int RS = ks + kRowPad;
+  const int last = c_end - c_begin - 1;     // ring chunk indices are relative to c_begin
+
+  f32x4 acc[2][NT];
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int tb = 0; tb < NT; ++tb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[st][tb][i] = 0.0f;
+
+  uint32_t wr[D][2][BITS];
+  uint32_t sr[D][2][GPC];
+#pragma unroll
+  for (int j = 0; j < D; ++j) load_chunk<BITS, GPC>(wr[j], sr[j], sp, j, last);
+
+  for (int c0 = c_begin; c0 < c_end; c0 += slab_chunks) {
+    const int c1 = (c0 + slab_chunks) < c_end ? (c0 + slab_chunks) : c_end;
+    __syncthreads();
+    stage_slab<PLANES>(xs, sxs, rowsrc, plane_stride, nt, rows, c0 * kTileCols,
+                       (c1 - c0) * kTileCols, RS, G);
+    int c = c0;
+    for (; c + D <= c1; c += D) {
+#pragma unroll
+      for (int j = 0; j < D; ++j) {
+        compute_chunk<BITS, NT, PLANES, GPC>(wr[j], sr[j], acc, tot, xs, sxs, c + j - c0, nt, RS,
+                                             lane);
+        load_chunk<BITS, GPC>(wr[j], sr[j], sp, c + j + D - c_begin, last);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < D; ++j) {        // remainder of the last slab
+      if (c + j < c1) {
+        compute_chunk<BITS, NT, PLANES, GPC>(wr[j], sr[j], acc, tot, xs, sxs, c + j - c0, nt, RS,
+                                             lane);
+      }
+    }
+  }
+}
+
+// Runs the streams for one expert width with the number of 16-token blocks
+// fixed at compile time (no token-block branches inside the loop).  NTMAX is
+// the largest block count a launch can see; tot[st][tb] for blocks beyond the
+// workgroup's count are left as they were.
+template <int BITS, int GPC, int PLANES, int NTMAX, typename RowFn>
+__device__ __forceinline__ void run_width(const Streams& sp, int c_begin, int c_end, RowFn rowsrc,
+                                          size_t plane_stride, int nt, int G, uint16_t* xs,
+                                          float* sxs, int xs_elems, f32x4 (&tot)[2][NTMAX]) {
+  const int ntb = (nt + 15) >> 4;
+  if (NTMAX == 1 || ntb == 1) {
+    f32x4 t[2][1];
+    t[0][0] = tot[0][0];
+    t[1][0] = tot[1][0];
+    stream_pair<BITS, 1, PLANES, GPC>(sp, c_begin, c_end, rowsrc, plane_stride, nt, G, xs, sxs,
+                                      xs_elems, t);
+    tot[0][0] = t[0][0];
+    tot[1][0] = t[1][0];
+  } else if (NTMAX == 2 || ntb == 2) {
+    constexpr int N = NTMAX < 2 ? NTMAX : 2;
+    f32x4 t[2][N];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int b = 0; b < N; ++b) t[j][b] = tot[j][b];
+    stream_pair<BITS, N, PLANES, GPC>(sp, c_begin, c_end, rowsrc, plane_stride, nt, G, xs, sxs,
+                                      xs_elems, t);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int b = 0; b < N; ++b) tot[j][b] = t[j][b];
+  } else {
+    stream_pair<BITS, NTMAX, PLANES, GPC>(sp, c_begin, c_end, rowsrc, plane_stride, nt, G, xs, sxs,
+                                          xs_elems, tot);
+  }
+}
+
+// Launchers (one translation unit per kernel and group size).
+template <int GPC>
+hipError_t launch_gateup(const uint16_t* x, const LayerArgs& L, const mc_routing& r,
+                         uint16_t* h_hi, uint16_t* h_lo, int ntmax, int xs_bytes,
+                         hipStream_t stream);
+template <int GPC>
+hipError_t launch_down(const uint16_t* h_hi, size_t plane_stride, const LayerArgs& L,
+                       const mc_routing& r, int nsplit, float* partial, size_t part_stride,
+                       int ntmax, int xs_bytes, hipStream_t stream);
+
+}  // namespace mc

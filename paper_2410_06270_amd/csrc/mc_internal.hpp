@@ -8,6 +8,16 @@ namespace mc {
 constexpr int kRouteFusedMaxT = 256;   // up to this many tokens routing runs in one launch
 constexpr int kDecodeMaxT = 64;        // up to this many tokens one workgroup holds all of an expert's tokens
 
+enum TimingSite {
+  kSitePackSz, kSitePackCodes, kSiteExport, kSiteRouteFused, kSiteRouteSelect, kSiteRouteLists,
+  kSiteGateUp, kSiteDown, kSiteCombine, kNumSites
+};
+void timing_begin(hipStream_t stream, int site);
+void timing_end(hipStream_t stream, int site);
+int timing_site(const char* name);
+hipError_t timing_read(int site, double* total_ms, int* launches);
+void timing_enable(int on);
+
 hipError_t launch_pack(const float* wg, const float* wu, const float* wd, const LayerArgs& L,
                        uint32_t* words, uint32_t* sz, hipStream_t stream);
 hipError_t launch_export(const uint32_t* words, const uint32_t* sz, int bits, int R, int K, int G,

@@ -174,13 +174,17 @@ hipError_t launch_pack(const float* wg, const float* wu, const float* wd, const 
   const int lpg = L.G / 4 < 64 ? L.G / 4 : 64;
   const long long waves = (groups + (64 / lpg) - 1) / (64 / lpg);
   const long long blocks_sz = (waves * 64 + 255) / 256;
+  timing_begin(stream, kSitePackSz);
   hipLaunchKernelGGL(pack_sz_kernel, dim3((unsigned)blocks_sz), dim3(256), 0, stream, wg, wu, wd,
                      L, sz, groups);
+  timing_end(stream, kSitePackSz);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const long long lanes = 3LL * L.E * L.d * L.ffn / 32;
+  timing_begin(stream, kSitePackCodes);
   hipLaunchKernelGGL(pack_codes_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, stream,
                      wg, wu, wd, L, sz, words, lanes);
+  timing_end(stream, kSitePackCodes);
   return hipGetLastError();
 }
 
@@ -197,9 +201,11 @@ hipError_t launch_export(const uint32_t* words, const uint32_t* sz, int bits, in
       hipLaunchKernelGGL((export_kernel<B, false>), grid, block, 0, stream, words, sz, R, K,  \
                          G, out);                                                             \
   }
+  timing_begin(stream, kSiteExport);
   MC_EXPORT_CASE(1)
   MC_EXPORT_CASE(2)
   MC_EXPORT_CASE(3)
+  timing_end(stream, kSiteExport);
 #undef MC_EXPORT_CASE
   return hipGetLastError();
 }

@@ -203,20 +203,26 @@ __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
 hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,
                         const mc_routing& r, hipStream_t stream) {
   if (r.T <= kRouteFusedMaxT) {
+    timing_begin(stream, kSiteRouteFused);
     hipLaunchKernelGGL(route_fused_kernel, dim3(1), dim3(kCsrThreads), 0, stream, logits,
                        important, r.T, r.E, r.k, delta32, tau, r.topk_idx, r.topk_w, r.kept,
                        r.counts, r.offsets, r.pair_token, r.pair_rank, r.pair_w, r.pair_pos,
                        r.n_pruned);
+    timing_end(stream, kSiteRouteFused);
     return hipGetLastError();
   }
+  timing_begin(stream, kSiteRouteSelect);
   hipLaunchKernelGGL(route_select_kernel, dim3((r.T + 3) / 4), dim3(256), 0, stream, logits,
                      important, r.T, r.E, r.k, delta32, tau, r.topk_idx, r.topk_w, r.kept,
                      r.pair_pos);
+  timing_end(stream, kSiteRouteSelect);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
+  timing_begin(stream, kSiteRouteLists);
   hipLaunchKernelGGL(route_lists_kernel, dim3(1), dim3(kCsrThreads), 0, stream, r.T, r.E, r.k,
                      r.topk_idx, r.kept, r.topk_w, r.counts, r.offsets, r.pair_token,
                      r.pair_rank, r.pair_w, r.pair_pos, r.n_pruned);
+  timing_end(stream, kSiteRouteLists);
   return hipGetLastError();
 }
 

@@ -1,0 +1,110 @@
+"""Parity at the benchmark's full sizes (Mixtral-8x7B-shaped layer: d=4096,
+ffn=14336, E=8, widths [3,3,3,2,2,2,2,3], G=128) in the launch configuration
+the benchmark times.  Packed words are compared in full for one expert; the
+layer output is compared on sampled tokens x rows, which the oracle computes
+one by one from its own quantization of the same fp32 weights."""
+import numpy as np
+import pytest
+
+import oracle
+import synthetic
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def mc():
+    import paper_2410_06270_amd as m
+    m.load()
+    return m
+
+
+_LOGICAL = {}     # oracle quantization per expert, shared by the tests of this module
+
+
+def to_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+@pytest.fixture(scope="module")
+def mixtral(mc):
+    c = synthetic.config(2)
+    E, d, ffn, G, bits = c["E"], c["d"], c["ffn"], c["G"], c["bits"]
+    mats = synthetic.layer_weights(2)
+    L = mc.PackedLayer(E, d, ffn, bits, G)
+    wg = torch.empty((E, ffn, d), dtype=torch.float32, device="cuda")
+    wu = torch.empty((E, ffn, d), dtype=torch.float32, device="cuda")
+    wd = torch.empty((E, d, ffn), dtype=torch.float32, device="cuda")
+    for e in range(E):
+        wg[e].copy_(torch.from_numpy(mats[e][0]))
+        wu[e].copy_(torch.from_numpy(mats[e][1]))
+        wd[e].copy_(torch.from_numpy(mats[e][2]))
+    mc.pack(wg, wu, wd, L)
+    torch.cuda.synchronize()
+    del wg, wu, wd
+    torch.cuda.empty_cache()
+    return c, mats, L
+
+
+def test_mixtral_expert_words_bit_exact(mc, mixtral):
+    c, mats, L = mixtral
+    E, d, ffn, G, bits = c["E"], c["d"], c["ffn"], c["G"], c["bits"]
+    wofs, sofs, _, _ = oracle.layer_offsets(E, d, ffn, bits, G)
+    words = L.words.cpu().numpy().view(np.uint32)
+    sz = L.sz.cpu().numpy().view(np.uint32)
+    for e in (0, 3):                      # one 3-bit and one 2-bit expert, all three matrices
+        _LOGICAL[e] = [oracle.quantize(mats[e][m], bits[e], G) for m in range(3)]
+        for m in range(3):
+            q, s, z = _LOGICAL[e][m]
+            w = oracle.layout_pack(q, bits[e])
+            np.testing.assert_array_equal(words[wofs[(e, m)]: wofs[(e, m)] + w.size], w)
+            p = oracle.pack_sz(s, z, G)
+            np.testing.assert_array_equal(sz[sofs[(e, m)]: sofs[(e, m)] + p.size], p)
+
+
+@pytest.mark.parametrize("T", [1, 8, 32, 64])
+def test_mixtral_decode_sampled(mc, mixtral, T):
+    c, mats, L = mixtral
+    E, d, ffn, k, G, bits, tau = c["E"], c["d"], c["ffn"], c["k"], c["G"], c["bits"], c["tau"][0]
+    x = synthetic.activations(2, T)
+    lg = synthetic.logits(2, T)
+    imp = synthetic.important_mask(2, T)
+    r = mc.Routing(T, E, k)
+    mc.route_and_prune(to_dev(lg), to_dev(imp), tau, r)
+    y = torch.empty((T, d), dtype=torch.int16, device="cuda")
+    ws = torch.empty(mc.forward_workspace(T, E, k, d, ffn), dtype=torch.uint8, device="cuda")
+    mc.moe_forward(to_dev(x.view(np.int16)), r, L, y, ws)
+    torch.cuda.synchronize()
+    ref = oracle.route(lg, imp, k, tau)
+    np.testing.assert_array_equal(r.topk_idx.cpu().numpy(), ref["topk_idx"])
+    np.testing.assert_array_equal(r.kept.cpu().numpy(), ref["kept"])
+    # sample: a pruned token, a protected token and the first/last tokens
+    toks = {0, T - 1}
+    pr = np.nonzero(ref["kept"][:, 1] == 0)[0]
+    if len(pr):
+        toks.add(int(pr[0]))
+    pt = np.nonzero(imp)[0]
+    if len(pt):
+        toks.add(int(pt[0]))
+    toks = sorted(toks)
+    rows = sorted(set(np.random.default_rng(T).choice(d, 48, replace=False).tolist()) | {0, d - 1})
+    need = sorted({int(ref["topk_idx"][t, rr]) for t in toks for rr in range(k) if ref["kept"][t, rr]})
+    logical = [None] * E
+    for e in need:
+        if e not in _LOGICAL:
+            _LOGICAL[e] = [oracle.quantize(mats[e][m], bits[e], G) for m in range(3)]
+        logical[e] = _LOGICAL[e]
+    y_ref = oracle.moe_forward(x, ref, logical, G, rows=rows, tokens=toks)
+    g = oracle.bf16_to_float64(y.cpu().numpy().view(np.uint16)[np.ix_(toks, rows)])
+    rb = oracle.bf16_to_float64(oracle.bf16_round_array(y_ref))
+    mae = np.abs(g - rb).mean()
+    rms = np.sqrt((y_ref ** 2).mean())
+    maxrel = (np.abs(g - y_ref) / np.maximum(np.abs(y_ref), rms)).max()
+    print("T=%d tokens %s MAE %.3e MaxRel %.3e rms %.3f" % (T, toks, mae, maxrel, rms))
+    assert mae <= 1e-3 and maxrel <= 2e-2, (mae, maxrel)
+    # the whole output is finite and has the reference's scale
+    yall = oracle.bf16_to_float64(y.cpu().numpy().view(np.uint16))
+    assert np.isfinite(yall).all()
+    assert 0.5 * rms < np.sqrt((yall ** 2).mean()) < 2.0 * rms
