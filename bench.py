@@ -38,6 +38,9 @@ def parse():
     p.add_argument("--copies", type=int, default=4)
     p.add_argument("--sweep", default="1,8", help="extra decode batch sizes to report")
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="only run a plain device-to-device copy of MIB MiB 5 times (reference "
+                        "for the FETCH_SIZE / WRITE_SIZE counters) and exit")
     return p.parse_args()
 
 
@@ -199,6 +202,16 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     import torch
+
+    if args.copy_calibration:
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n * 4, "copies": 5}))
+        return
 
     import paper_2410_06270_amd as mc
     import synthetic

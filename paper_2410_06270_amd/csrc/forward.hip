@@ -5,24 +5,35 @@
 namespace mc {
 
 // ---------------------------------------------------------------- combine --
-
+// y[t][i..i+3] = bf16(sum over kept ranks r, in rank order, of
+// w_r * sum over splits s, in order, of partial[s][pos(t, r)][i..i+3]).
+template <int NSPLIT>
 __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ partial,
-                                                      size_t part_stride, int nsplit,
+                                                      size_t part_stride,
                                                       const int32_t* __restrict__ pair_pos,
                                                       const float* __restrict__ topk_w, int k, int d,
                                                       uint16_t* __restrict__ y) {
   const int t = blockIdx.y;
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int i = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
   if (i >= d) return;
-  float acc = 0.0f;
+  f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
   for (int r = 0; r < k; ++r) {
     const int pos = pair_pos[(size_t)t * k + r];
     if (pos < 0) continue;
-    float v = 0.0f;
-    for (int s = 0; s < nsplit; ++s) v += partial[(size_t)s * part_stride + (size_t)pos * d + i];
-    acc = fmaf(topk_w[(size_t)t * k + r], v, acc);
+    const float w = topk_w[(size_t)t * k + r];
+    f32x4 v[NSPLIT];
+#pragma unroll
+    for (int s = 0; s < NSPLIT; ++s)
+      v[s] = *reinterpret_cast<const f32x4*>(partial + s * part_stride + (size_t)pos * d + i);
+    f32x4 sum = v[0];
+#pragma unroll
+    for (int s = 1; s < NSPLIT; ++s) sum += v[s];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[c] = fmaf(w, sum[c], acc[c]);
   }
-  y[(size_t)t * d + i] = float_to_bf16(acc);
+  uint32_t lo = (uint32_t)float_to_bf16(acc[0]) | ((uint32_t)float_to_bf16(acc[1]) << 16);
+  uint32_t hi = (uint32_t)float_to_bf16(acc[2]) | ((uint32_t)float_to_bf16(acc[3]) << 16);
+  *reinterpret_cast<uint2*>(y + (size_t)t * d + i) = make_uint2(lo, hi);
 }
 
 // --------------------------------------------------------------- launchers --
@@ -33,7 +44,7 @@ int forward_nsplit(int T, int E, int k, int d, int ffn) {
   const int tiles = d / 128;
   const int active = (T * k) < E ? (T * k) : E;
   int s = (2048 + tiles * active - 1) / (tiles * active);
-  const int maxs = (ffn / kTileCols) / prefetch_depth(4);
+  const int maxs = (ffn / kTileCols) / 4;
   if (T > kDecodeMaxT) s = 1;
   if (s > maxs) s = maxs;
   if (s > 8) s = 8;
@@ -60,7 +71,7 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
   const int nsplit = forward_nsplit(T, r.E, k, L.d, L.ffn);
   // An expert sees at most min(T, 16*ntmax) tokens per workgroup.
   const int ntmax = T <= 16 ? 1 : (T <= 32 ? 2 : 4);
-  const int xs_bytes = ntmax == 1 ? kXsBytesSmall : kXsBytesLarge;
+  const int xs_bytes = ntmax <= 2 ? kXsBytesSmall : kXsBytesLarge;
   hipError_t err;
   timing_begin(stream, kSiteGateUp);
   if (L.G == 128) err = launch_gateup<1>(x, L, r, h_hi, h_hi + plane, ntmax, xs_bytes, stream);
@@ -75,8 +86,21 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
   timing_end(stream, kSiteDown);
   if (err != hipSuccess) return err;
   timing_begin(stream, kSiteCombine);
-  hipLaunchKernelGGL(combine_kernel, dim3((L.d + 255) / 256, T), dim3(256), 0, stream, partial,
-                     part_stride, nsplit, r.pair_pos, r.topk_w, k, L.d, y);
+  const dim3 cgrid((L.d / 4 + 255) / 256, T);
+#define MC_COMBINE(S)                                                                              \
+  hipLaunchKernelGGL(combine_kernel<S>, cgrid, dim3(256), 0, stream, partial, part_stride,         \
+                     r.pair_pos, r.topk_w, k, L.d, y)
+  switch (nsplit) {
+    case 1: MC_COMBINE(1); break;
+    case 2: MC_COMBINE(2); break;
+    case 3: MC_COMBINE(3); break;
+    case 4: MC_COMBINE(4); break;
+    case 5: MC_COMBINE(5); break;
+    case 6: MC_COMBINE(6); break;
+    case 7: MC_COMBINE(7); break;
+    default: MC_COMBINE(8); break;
+  }
+#undef MC_COMBINE
   timing_end(stream, kSiteCombine);
   return hipGetLastError();
 }

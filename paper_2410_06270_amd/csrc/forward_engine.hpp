@@ -26,46 +26,56 @@ namespace mc {
 
 constexpr uint32_t kMagic2 = 0x43004300u;     // bf16 128.0 in both halves
 constexpr int kRowPad = 8;                    // bf16 elements of padding per slab row
-constexpr int kSxBytes = 8 * 1024;            // group sums of the staged slab (LDS)
+constexpr int kSxBytes = 4 * 1024;            // group sums of the staged slab (LDS)
 
-// LDS for the staged activation slab: up to 16 tokens (batches of <= 16) or 64.
-// 34 KB holds 16 tokens x 2 planes x 512 columns; 68 KB holds 64 x 2 x 256.
-constexpr int kXsBytesSmall = 34 * 1024;
+// LDS for the staged activation slab.  Batches whose experts see at most 32
+// tokens per workgroup use 36 KB (+4 KB group sums: four workgroups per CU);
+// up to 64 tokens use 68 KB.
+constexpr int kXsBytesSmall = 36 * 1024;
 constexpr int kXsBytesLarge = 68 * 1024;
-// Chunks (16 rows x 128 columns of codes) kept in flight per stream, by the
-// number of 16-token blocks and of groups per chunk (the slab is a multiple
-// of this many chunks); deeper rings cost registers the wider variants lack.
-__host__ __device__ constexpr int prefetch_depth(int ntb, int gpc = 1) {
-  return (ntb >= 3 || gpc >= 4) ? 2 : 4;
+// Chunks (16 rows x 128 columns of codes) kept in flight per stream.  The slab
+// is a multiple of this many chunks, so it is smaller where the slab rows are
+// many (token blocks x planes) or the registers few (groups per chunk).
+__host__ __device__ constexpr int prefetch_depth(int ntb, int gpc, int planes) {
+  return (ntb >= 3 || gpc >= 4 || ntb * planes >= 4) ? 2 : 4;
 }
 // Smallest slab (one ring of chunks) of the worst case of each token-block
-// count must fit the LDS budget: planes x tokens x (columns + pad) x 2 bytes.
+// count must fit its LDS budget: (planes x tokens + zero row) x (columns + pad) x 2 bytes.
 constexpr int slab_floor_bytes(int ntb, int planes) {
-  return planes * 16 * ntb * (prefetch_depth(ntb) * kTileCols + kRowPad) * 2;
+  return (planes * 16 * ntb + 1) * (prefetch_depth(ntb, 1, planes) * kTileCols + kRowPad) * 2;
 }
 static_assert(slab_floor_bytes(1, 2) <= kXsBytesSmall, "LDS budget (<= 16 tokens)");
-static_assert(slab_floor_bytes(2, 2) <= kXsBytesLarge, "LDS budget (<= 32 tokens)");
+static_assert(slab_floor_bytes(2, 1) <= kXsBytesSmall, "LDS budget (<= 32 tokens, 1 plane)");
+static_assert(slab_floor_bytes(2, 2) <= kXsBytesSmall, "LDS budget (<= 32 tokens, 2 planes)");
 static_assert(slab_floor_bytes(3, 2) <= kXsBytesLarge, "LDS budget (<= 48 tokens)");
 static_assert(slab_floor_bytes(4, 2) <= kXsBytesLarge, "LDS budget (<= 64 tokens)");
 // Group sums: 16*ntb rows x (slab / G) groups x 4 bytes; the slab is capped by
 // kSxBytes, which must allow at least one ring of chunks at G = 32.
-static_assert((kSxBytes / (4 * 64)) * 32 >= 2 * kTileCols, "group-sum budget");
+static_assert((kSxBytes / (4 * 64)) * 32 >= 2 * kTileCols, "group-sum budget (64 tokens)");
+static_assert((kSxBytes / (4 * 32)) * 32 >= 4 * kTileCols, "group-sum budget (32 tokens)");
 
 __device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
 
-__device__ __forceinline__ bf16x8 load_a(const uint16_t* p, bool valid) {
-  u32x4 v = {0u, 0u, 0u, 0u};
-  if (valid) v = *reinterpret_cast<const u32x4*>(p);
-  return __builtin_bit_cast(bf16x8, v);
+__device__ __forceinline__ bf16x8 load_a(const uint16_t* p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
+}
+
+// A constant the compiler keeps in a VGPR: with the mask in an SGPR it lets
+// (w >> f) & mask | magic issue as one v_and_or_b32 (gfx9 VOP3 encodings take
+// no literal constants).
+__device__ __forceinline__ uint32_t vgpr_constant(uint32_t c) {
+  uint32_t v;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(v) : "i"(c));
+  return v;
 }
 
 template <int BITS>
-__device__ __forceinline__ bf16x8 b_operand(const uint32_t* w, int u) {
+__device__ __forceinline__ bf16x8 b_operand(const uint32_t* w, int u, uint32_t magic) {
   u32x4 v;
-  v[0] = extract_pair<BITS>(w, 4 * u + 0, kMagic2);
-  v[1] = extract_pair<BITS>(w, 4 * u + 1, kMagic2);
-  v[2] = extract_pair<BITS>(w, 4 * u + 2, kMagic2);
-  v[3] = extract_pair<BITS>(w, 4 * u + 3, kMagic2);
+  v[0] = extract_pair<BITS>(w, 4 * u + 0, magic);
+  v[1] = extract_pair<BITS>(w, 4 * u + 1, magic);
+  v[2] = extract_pair<BITS>(w, 4 * u + 2, magic);
+  v[3] = extract_pair<BITS>(w, 4 * u + 3, magic);
   return __builtin_bit_cast(bf16x8, v);
 }
 
@@ -155,7 +165,7 @@ __device__ __forceinline__ void stage_slab(uint16_t* xs, float* sxs, RowFn rowsr
   const int pieces = kw >> 3;
   const int total = nt * pieces;
   const int gp = G >> 3;
-  for (int base = threadIdx.x & ~63; base < total; base += blockDim.x) {
+  for (int base = wave_id() * 64; base < total; base += blockDim.x) {
     const int idx = base + lane;
     const bool valid = idx < total;
     int m = 0, p = 0;
@@ -176,24 +186,26 @@ __device__ __forceinline__ void stage_slab(uint16_t* xs, float* sxs, RowFn rowsr
   __syncthreads();
 }
 
+// One chunk (4 MFMA steps of 32 columns) of both streams.  arow[tb][pl] is
+// this lane's activation row in the slab (a zero row for padding tokens).
 template <int BITS, int NT, int PLANES, int GPC>
 __device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
                                               const uint32_t (&s)[2][GPC], f32x4 (&acc)[2][NT],
-                                              f32x4 (&tot)[2][NT], const uint16_t* xs,
-                                              const float* sxs, int lc, int nt, int RS, int lane) {
+                                              f32x4 (&tot)[2][NT],
+                                              const uint16_t* const (&arow)[NT][PLANES],
+                                              const float* sxs, int lc, int lane, uint32_t magic) {
   constexpr int SPG = 4 / GPC;   // MFMA steps per quantization group
   constexpr int rows = 16 * NT;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const bf16x8 b0 = b_operand<BITS>(w[0], u);
-    const bf16x8 b1 = b_operand<BITS>(w[1], u);
-    const int kk = lc * kTileCols + 32 * u + 8 * (lane >> 4);
+    const bf16x8 b0 = b_operand<BITS>(w[0], u, magic);
+    const bf16x8 b1 = b_operand<BITS>(w[1], u, magic);
+    const int kk = lc * kTileCols + 32 * u;
 #pragma unroll
     for (int tb = 0; tb < NT; ++tb) {
-      const int m = tb * 16 + (lane & 15);
 #pragma unroll
       for (int pl = 0; pl < PLANES; ++pl) {
-        const bf16x8 a = load_a(xs + (size_t)(pl * nt + m) * RS + kk, m < nt);
+        const bf16x8 a = load_a(arow[tb][pl] + kk);
         acc[0][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b0, acc[0][tb], 0, 0, 0);
         acc[1][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b1, acc[1][tb], 0, 0, 0);
       }
@@ -220,10 +232,10 @@ __device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int 
                                             RowFn rowsrc, size_t plane_stride, int nt, int G,
                                             uint16_t* xs, float* sxs, int xs_elems,
                                             f32x4 (&tot)[2][NT]) {
-  constexpr int D = prefetch_depth(NT, GPC);
+  constexpr int D = prefetch_depth(NT, GPC, PLANES);
   constexpr int rows = 16 * NT;
   const int lane = threadIdx.x & 63;
-  int ks = xs_elems / (PLANES * nt) - kRowPad;
+  int ks = xs_elems / (PLANES * nt + 1) - kRowPad;   // + one zero row for padding tokens
   const int ks_sx = (kSxBytes / (4 * rows)) * G;
   ks = ks < ks_sx ? ks : ks_sx;
   const int unit = D * kTileCols;
@@ -246,6 +258,20 @@ __device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int 
 #pragma unroll
   for (int j = 0; j < D; ++j) load_chunk<BITS, GPC>(wr[j], sr[j], sp, j, last);
 
+  // zero row after the staged rows; lanes of tokens >= nt read it
+  uint16_t* zrow = xs + (size_t)PLANES * nt * RS;
+  for (int i = threadIdx.x; i < RS / 8; i += blockDim.x)
+    *reinterpret_cast<u32x4*>(zrow + 8 * i) = u32x4{0u, 0u, 0u, 0u};
+  const uint16_t* arow[NT][PLANES];
+#pragma unroll
+  for (int tb = 0; tb < NT; ++tb) {
+    const int m = tb * 16 + (lane & 15);
+#pragma unroll
+    for (int pl = 0; pl < PLANES; ++pl)
+      arow[tb][pl] = (m < nt ? xs + (size_t)(pl * nt + m) * RS : zrow) + 8 * (lane >> 4);
+  }
+  const uint32_t magic = vgpr_constant(kMagic2);
+
   for (int c0 = c_begin; c0 < c_end; c0 += slab_chunks) {
     const int c1 = (c0 + slab_chunks) < c_end ? (c0 + slab_chunks) : c_end;
     __syncthreads();
@@ -255,16 +281,16 @@ __device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int 
     for (; c + D <= c1; c += D) {
 #pragma unroll
       for (int j = 0; j < D; ++j) {
-        compute_chunk<BITS, NT, PLANES, GPC>(wr[j], sr[j], acc, tot, xs, sxs, c + j - c0, nt, RS,
-                                             lane);
+        compute_chunk<BITS, NT, PLANES, GPC>(wr[j], sr[j], acc, tot, arow, sxs, c + j - c0, lane,
+                                             magic);
         load_chunk<BITS, GPC>(wr[j], sr[j], sp, c + j + D - c_begin, last);
       }
     }
 #pragma unroll
     for (int j = 0; j < D; ++j) {        // remainder of the last slab
       if (c + j < c1) {
-        compute_chunk<BITS, NT, PLANES, GPC>(wr[j], sr[j], acc, tot, xs, sxs, c + j - c0, nt, RS,
-                                             lane);
+        compute_chunk<BITS, NT, PLANES, GPC>(wr[j], sr[j], acc, tot, arow, sxs, c + j - c0, lane,
+                                             magic);
       }
     }
   }

@@ -39,8 +39,11 @@ __device__ __forceinline__ void stream_rsrc(const LayerArgs& L, int e, int m, in
 // Workgroup: expert e, 64 rows (4 waves x 16) of gate and up, up to
 // 16*NTMAX of the expert's tokens.  Writes h = silu(gate x) * (up x)
 // as bf16 hi/lo planes.
+// Up to 32 tokens per workgroup the kernels are held to 128 registers so that
+// four workgroups (16 waves) share a CU.
 template <int GPC, int NTMAX>
-__global__ void __launch_bounds__(256) gateup_kernel(const uint16_t* __restrict__ x, LayerArgs L,
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2)))
+gateup_kernel(const uint16_t* __restrict__ x, LayerArgs L,
                                                      const int32_t* __restrict__ counts,
                                                      const int32_t* __restrict__ offsets,
                                                      const int32_t* __restrict__ pair_token,
@@ -57,7 +60,7 @@ __global__ void __launch_bounds__(256) gateup_kernel(const uint16_t* __restrict_
   const int nt = (ce - t0) < 16 * NTMAX ? (ce - t0) : 16 * NTMAX;
   const int pbase = offsets[e] + t0;
   for (int i = threadIdx.x; i < nt; i += blockDim.x) toks[i] = pair_token[pbase + i];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int K = L.d, G = L.G, ntiles = K / kTileCols;
   const int b = L.cum_bits[e + 1] - L.cum_bits[e];
   const int rb = blockIdx.x * 4 + wave;
@@ -96,7 +99,8 @@ __global__ void __launch_bounds__(256) gateup_kernel(const uint16_t* __restrict_
 // Workgroup: expert e, 128 output rows (4 waves x 2 row blocks), one split of
 // the ffn reduction, up to 16*NTMAX of the expert's pairs -> fp32 partials.
 template <int GPC, int NTMAX>
-__global__ void __launch_bounds__(256) down_kernel(const uint16_t* __restrict__ h_hi,
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2)))
+down_kernel(const uint16_t* __restrict__ h_hi,
                                                    size_t plane_stride, LayerArgs L,
                                                    const int32_t* __restrict__ counts,
                                                    const int32_t* __restrict__ offsets, int nsplit,
@@ -112,7 +116,7 @@ __global__ void __launch_bounds__(256) down_kernel(const uint16_t* __restrict__ 
   if (t0 >= ce) return;
   const int nt = (ce - t0) < 16 * NTMAX ? (ce - t0) : 16 * NTMAX;
   const int pbase = offsets[e] + t0;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int K = L.ffn, G = L.G, ntiles = K / kTileCols;
   const int b = L.cum_bits[e + 1] - L.cum_bits[e];
   const int per = (ntiles + nsplit - 1) / nsplit;

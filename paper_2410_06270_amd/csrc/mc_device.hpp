@@ -18,6 +18,9 @@ constexpr int kTileRows = 16;    // rows of one packed tile (MFMA N)
 constexpr int kTileCols = 128;   // reduction columns of one packed tile (4 MFMA K-steps)
 constexpr int kWave = 64;
 
+// Index of the calling wavefront in its workgroup, as a wave-uniform (scalar) value.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
 // ---------------------------------------------------------------- formats --
 
 __device__ __forceinline__ float half_bits_to_float(uint32_t h) {

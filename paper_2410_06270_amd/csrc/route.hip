@@ -8,10 +8,11 @@
 // (fp64).  Sec. 3.3.2: a protected token keeps every selected expert.  The
 // kept weights are renormalised over the kept ranks.
 //
-// Phase 1 (one wavefront per token): lanes hold the logits, k rounds of a
-// 64-bit max-reduction pick the experts.  Phase 2 (one workgroup): per-expert
-// token lists in ascending token order, built with ballots and popcount
-// prefixes (no atomics, so the lists are deterministic).
+// Selection (one wavefront per token): lanes hold the logits, k rounds of a
+// 64-bit max-reduction pick the experts, lane r then evaluates rank r.
+// Lists (one workgroup): per-expert token lists in ascending token order,
+// built with ballots and popcount prefixes (no atomics, so deterministic).
+// Small batches run both phases in one launch with everything kept in LDS.
 #include "mc_internal.hpp"
 
 namespace mc {
@@ -29,6 +30,12 @@ __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v)
   return v;
 }
 
+// Sum over lanes 0..7 (the ranks) in a fixed butterfly order.
+__device__ __forceinline__ double rank_sum(double v) {
+  for (int off = 1; off < MC_MAX_TOPK; off <<= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
 // Order-preserving integer image of a float, with -0 mapped onto +0.
 __device__ __forceinline__ uint32_t ordered_bits(float f) {
   uint32_t u = __float_as_uint(f);
@@ -36,10 +43,13 @@ __device__ __forceinline__ uint32_t ordered_bits(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Selects and prunes token t.  Lane r < k writes rank r's outputs; when
+// s_ent/s_w are given it also records them in LDS (expert or 0xffff if pruned).
 __device__ void select_token(const float* __restrict__ logits, const uint8_t* __restrict__ important,
                              int t, int E, int k, float delta32, double tau,
                              int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
-                             uint8_t* __restrict__ kept, int32_t* __restrict__ pair_pos) {
+                             uint8_t* __restrict__ kept, int32_t* __restrict__ pair_pos,
+                             uint16_t* s_ent, float* s_w) {
   const int lane = threadIdx.x & 63;
   const float* l = logits + (size_t)t * E;
   unsigned long long key[4];
@@ -48,87 +58,140 @@ __device__ void select_token(const float* __restrict__ logits, const uint8_t* __
     const int e = lane + 64 * j;
     key[j] = (e < E) ? (((unsigned long long)ordered_bits(l[e]) << 32) | (unsigned)(0xffff - e)) : 0ull;
   }
-  int sel[MC_MAX_TOPK];
+  int my_e = 0;
+  for (int r = 0; r < k; ++r) {
+    unsigned long long best = key[0];
 #pragma unroll
-  for (int r = 0; r < MC_MAX_TOPK; ++r) {
-    if (r < k) {
-      unsigned long long best = key[0];
+    for (int j = 1; j < 4; ++j) best = key[j] > best ? key[j] : best;
+    best = wave_max_u64(best);
+    const int e = 0xffff - (int)(best & 0xffffu);
+    if (lane == r) my_e = e;
 #pragma unroll
-      for (int j = 1; j < 4; ++j) best = key[j] > best ? key[j] : best;
-      best = wave_max_u64(best);
-      const int e = 0xffff - (int)(best & 0xffffu);
-      sel[r] = e;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (lane + 64 * j == e) key[j] = 0ull;
-    } else {
-      sel[r] = 0;
-    }
+    for (int j = 0; j < 4; ++j)
+      if (lane + 64 * j == e) key[j] = 0ull;
   }
-  // weights and pruning: every lane evaluates the same k terms
-  const float l0 = l[sel[0]];
-  double ex[MC_MAX_TOPK];
-  double sum_all = 0.0;
-#pragma unroll
-  for (int r = 0; r < MC_MAX_TOPK; ++r) {
-    ex[r] = (r < k) ? exp((double)l[sel[r]] - (double)l0) : 0.0;
-    sum_all += ex[r];
-  }
+  const int e0 = __shfl(my_e, 0);
+  const int e1 = __shfl(my_e, 1 < k ? 1 : 0);
+  const float l0 = l[e0];
+  const bool mine = lane < k;
+  const double ex = mine ? exp((double)l[my_e] - (double)l0) : 0.0;
+  const double sum_all = rank_sum(ex);
   const bool prot = important != nullptr && important[t] != 0;
-  bool keep[MC_MAX_TOPK];
-  double sum_kept = 0.0;
-#pragma unroll
-  for (int r = 0; r < MC_MAX_TOPK; ++r) {
-    bool kp = r < k;
-    if (kp && r > 0 && !prot) {
-      if (k == 2) {
-        const float gap = l0 - l[sel[1]];
-        kp = !(gap > delta32);
-      } else {
-        kp = !(ex[r] < tau * sum_all);
-      }
+  bool keep = mine;
+  if (mine && lane > 0 && !prot) {
+    if (k == 2) {
+      const float gap = l0 - l[e1];
+      keep = !(gap > delta32);
+    } else {
+      keep = !(ex < tau * sum_all);
     }
-    keep[r] = kp;
-    if (kp) sum_kept += ex[r];
   }
-#pragma unroll
-  for (int r = 0; r < MC_MAX_TOPK; ++r) {
-    if (r < k && lane == r) {
-      const size_t o = (size_t)t * k + r;
-      topk_idx[o] = sel[r];
-      kept[o] = keep[r] ? 1 : 0;
-      topk_w[o] = keep[r] ? (float)(ex[r] / sum_kept) : 0.0f;
-      pair_pos[o] = -1;
+  const double sum_kept = rank_sum(keep ? ex : 0.0);
+  if (mine) {
+    const size_t o = (size_t)t * k + lane;
+    const float w = keep ? (float)(ex / sum_kept) : 0.0f;
+    topk_idx[o] = my_e;
+    kept[o] = keep ? 1 : 0;
+    topk_w[o] = w;
+    if (!keep) pair_pos[o] = -1;
+    if (s_ent) {
+      s_ent[o] = keep ? (uint16_t)my_e : (uint16_t)0xffff;
+      s_w[o] = w;
     }
   }
 }
 
-// Per-expert lists.  Runs in one workgroup of kCsrThreads threads.
-__device__ void build_lists(int T, int E, int k, const int32_t* __restrict__ topk_idx,
-                            const uint8_t* __restrict__ kept, const float* __restrict__ topk_w,
+// Exclusive scan of cnt[0..E) into base[] and the global counts/offsets
+// (one wave: each lane owns 4 consecutive experts).
+__device__ void scan_counts(int T, int E, int k, const int* cnt, int* base,
                             int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
-                            int32_t* __restrict__ pair_token, int32_t* __restrict__ pair_rank,
-                            float* __restrict__ pair_w, int32_t* __restrict__ pair_pos,
                             int32_t* __restrict__ n_pruned) {
-  __shared__ uint16_t ent[kCsrChunk * MC_MAX_TOPK];   // expert of (t, r), 0xffff if pruned
+  const int lane = threadIdx.x & 63;
+  int c[4], local = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = 4 * lane + j;
+    c[j] = e < E ? cnt[e] : 0;
+    local += c[j];
+  }
+  int incl = local;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(incl, off);
+    if (lane >= off) incl += v;
+  }
+  int run = incl - local;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = 4 * lane + j;
+    if (e < E) {
+      base[e] = run;
+      offsets[e] = run;
+      counts[e] = c[j];
+    }
+    run += c[j];
+  }
+  if (lane == 63) {
+    offsets[E] = incl;
+    *n_pruned = T * k - incl;
+  }
+}
+
+// One pass over the tokens [c0, c0+nc) of expert e held in ent (LDS, indexed
+// from token c0): counts (pass 0) or writes the list entries from run (pass 1).
+__device__ __forceinline__ int list_pass(int pass, int e, int run, int c0, int nc, int k,
+                                         const uint16_t* ent, const float* w_src, bool w_in_lds,
+                                         const float* __restrict__ topk_w,
+                                         int32_t* __restrict__ pair_token,
+                                         int32_t* __restrict__ pair_rank, float* __restrict__ pair_w,
+                                         int32_t* __restrict__ pair_pos) {
+  const int lane = threadIdx.x & 63;
+  for (int t0 = 0; t0 < nc; t0 += 64) {
+    const int tl = t0 + lane;
+    int rr = -1;
+    if (tl < nc)
+      for (int r = 0; r < k; ++r)
+        if (ent[tl * k + r] == e) rr = r;
+    const unsigned long long m = __ballot(rr >= 0);
+    if (pass == 1 && rr >= 0) {
+      const int pos = run + __popcll(m & ((1ull << lane) - 1ull));
+      const int t = c0 + tl;
+      pair_token[pos] = t;
+      pair_rank[pos] = rr;
+      pair_w[pos] = w_in_lds ? w_src[tl * k + rr] : topk_w[(size_t)t * k + rr];
+      pair_pos[(size_t)t * k + rr] = pos;
+    }
+    run += __popcll(m);
+  }
+  return run;
+}
+
+__global__ void __launch_bounds__(256) route_select_kernel(const float* __restrict__ logits,
+                                                           const uint8_t* __restrict__ important,
+                                                           int T, int E, int k, float delta32,
+                                                           double tau, int32_t* topk_idx,
+                                                           float* topk_w, uint8_t* kept,
+                                                           int32_t* pair_pos) {
+  const int t = blockIdx.x * (blockDim.x >> 6) + wave_id();
+  if (t >= T) return;
+  select_token(logits, important, t, E, k, delta32, tau, topk_idx, topk_w, kept, pair_pos,
+               nullptr, nullptr);
+}
+
+// Lists for any T (one workgroup), reading the selection from global memory
+// in chunks of kCsrChunk tokens.
+__global__ void __launch_bounds__(kCsrThreads) route_lists_kernel(
+    int T, int E, int k, const int32_t* __restrict__ topk_idx, const uint8_t* __restrict__ kept,
+    const float* __restrict__ topk_w, int32_t* counts, int32_t* offsets, int32_t* pair_token,
+    int32_t* pair_rank, float* pair_w, int32_t* pair_pos, int32_t* n_pruned) {
+  __shared__ uint16_t ent[kCsrChunk * MC_MAX_TOPK];
   __shared__ int cnt[MC_MAX_EXPERTS];
   __shared__ int base[MC_MAX_EXPERTS];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nwaves = blockDim.x >> 6;
+  const int tid = threadIdx.x, wave = wave_id(), nwaves = blockDim.x >> 6;
   for (int e = tid; e < E; e += blockDim.x) cnt[e] = 0;
   for (int pass = 0; pass < 2; ++pass) {
     if (pass == 1) {
       __syncthreads();
-      if (tid == 0) {
-        int acc = 0;
-        for (int e = 0; e < E; ++e) {
-          offsets[e] = acc;
-          counts[e] = cnt[e];
-          base[e] = acc;
-          acc += cnt[e];
-        }
-        offsets[E] = acc;
-        *n_pruned = T * k - acc;
-      }
+      if (wave == 0) scan_counts(T, E, k, cnt, base, counts, offsets, n_pruned);
     }
     for (int c0 = 0; c0 < T; c0 += kCsrChunk) {
       const int nc = (T - c0) < kCsrChunk ? (T - c0) : kCsrChunk;
@@ -139,25 +202,9 @@ __device__ void build_lists(int T, int E, int k, const int32_t* __restrict__ top
       }
       __syncthreads();
       for (int e = wave; e < E; e += nwaves) {
-        int run = (pass == 0) ? 0 : base[e];
-        for (int t0 = 0; t0 < nc; t0 += 64) {
-          const int tl = t0 + lane;
-          int rr = -1;
-          if (tl < nc)
-            for (int r = 0; r < k; ++r)
-              if (ent[tl * k + r] == e) rr = r;
-          const unsigned long long m = __ballot(rr >= 0);
-          if (pass == 1 && rr >= 0) {
-            const int pos = run + __popcll(m & ((1ull << lane) - 1ull));
-            const int t = c0 + tl;
-            pair_token[pos] = t;
-            pair_rank[pos] = rr;
-            pair_w[pos] = topk_w[(size_t)t * k + rr];
-            pair_pos[(size_t)t * k + rr] = pos;
-          }
-          run += __popcll(m);
-        }
-        if (lane == 0) {
+        const int run = list_pass(pass, e, pass == 0 ? 0 : base[e], c0, nc, k, ent, nullptr, false,
+                                  topk_w, pair_token, pair_rank, pair_w, pair_pos);
+        if ((threadIdx.x & 63) == 0) {
           if (pass == 0) cnt[e] += run;
           else base[e] = run;
         }
@@ -166,38 +213,33 @@ __device__ void build_lists(int T, int E, int k, const int32_t* __restrict__ top
   }
 }
 
-__global__ void __launch_bounds__(256) route_select_kernel(const float* __restrict__ logits,
-                                                           const uint8_t* __restrict__ important,
-                                                           int T, int E, int k, float delta32,
-                                                           double tau, int32_t* topk_idx,
-                                                           float* topk_w, uint8_t* kept,
-                                                           int32_t* pair_pos) {
-  const int t = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  if (t >= T) return;
-  select_token(logits, important, t, E, k, delta32, tau, topk_idx, topk_w, kept, pair_pos);
-}
-
-__global__ void __launch_bounds__(kCsrThreads) route_lists_kernel(
-    int T, int E, int k, const int32_t* topk_idx, const uint8_t* kept, const float* topk_w,
-    int32_t* counts, int32_t* offsets, int32_t* pair_token, int32_t* pair_rank, float* pair_w,
-    int32_t* pair_pos, int32_t* n_pruned) {
-  build_lists(T, E, k, topk_idx, kept, topk_w, counts, offsets, pair_token, pair_rank, pair_w,
-              pair_pos, n_pruned);
-}
-
-// Small batches: both phases in one workgroup (one launch).
+// Small batches (T <= kRouteFusedMaxT): selection and lists in one launch, the
+// selection kept in LDS; global outputs are only written.
 __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
     const float* __restrict__ logits, const uint8_t* __restrict__ important, int T, int E, int k,
     float delta32, double tau, int32_t* topk_idx, float* topk_w, uint8_t* kept, int32_t* counts,
     int32_t* offsets, int32_t* pair_token, int32_t* pair_rank, float* pair_w, int32_t* pair_pos,
     int32_t* n_pruned) {
-  const int nwaves = blockDim.x >> 6;
-  for (int t = threadIdx.x >> 6; t < T; t += nwaves)
-    select_token(logits, important, t, E, k, delta32, tau, topk_idx, topk_w, kept, pair_pos);
-  __threadfence_block();
+  __shared__ uint16_t ent[kRouteFusedMaxT * MC_MAX_TOPK];
+  __shared__ float wsel[kRouteFusedMaxT * MC_MAX_TOPK];
+  __shared__ int cnt[MC_MAX_EXPERTS];
+  __shared__ int base[MC_MAX_EXPERTS];
+  const int wave = wave_id(), nwaves = blockDim.x >> 6, lane = threadIdx.x & 63;
+  for (int t = wave; t < T; t += nwaves)
+    select_token(logits, important, t, E, k, delta32, tau, topk_idx, topk_w, kept, pair_pos, ent,
+                 wsel);
   __syncthreads();
-  build_lists(T, E, k, topk_idx, kept, topk_w, counts, offsets, pair_token, pair_rank, pair_w,
-              pair_pos, n_pruned);
+  for (int e = wave; e < E; e += nwaves) {
+    const int n = list_pass(0, e, 0, 0, T, k, ent, wsel, true, topk_w, pair_token, pair_rank,
+                            pair_w, pair_pos);
+    if (lane == 0) cnt[e] = n;
+  }
+  __syncthreads();
+  if (wave == 0) scan_counts(T, E, k, cnt, base, counts, offsets, n_pruned);
+  __syncthreads();
+  for (int e = wave; e < E; e += nwaves)
+    list_pass(1, e, base[e], 0, T, k, ent, wsel, true, topk_w, pair_token, pair_rank, pair_w,
+              pair_pos);
 }
 
 hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,
