@@ -38,6 +38,8 @@ def parse():
     p.add_argument("--copies", type=int, default=4)
     p.add_argument("--sweep", default="1,8", help="extra decode batch sizes to report")
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    p.add_argument("--graph", action="store_true",
+                   help="also time HIP-graph replays of the step (reported as ms_per_step_graph)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run a plain device-to-device copy of MIB MiB 5 times (reference "
                         "for the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -108,20 +110,37 @@ class Workload:
         return dict(gateup=gateup + act, down=down, combine=act, step=gateup + down + 2 * act + logits)
 
 
-def time_steps(mc, torch, wl, steps, warmup):
+def time_steps(mc, torch, wl, steps, warmup, graphs=None):
+    """Average step time in ms (HIP events around the timed steps).  With
+    ``graphs`` (one captured step per layer copy) the steps are graph replays."""
+    run = (lambda i: graphs[i % len(graphs)].replay()) if graphs else (lambda i: wl.step(mc, i))
     for i in range(warmup):
-        wl.step(mc, i)
+        run(i)
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     ev0.record()
     for i in range(steps):
-        wl.step(mc, i)
+        run(i)
     ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     return ev0.elapsed_time(ev1) / steps, wall
+
+
+def capture_steps(mc, torch, wl):
+    """One HIP graph per layer copy holding route_and_prune + moe_forward."""
+    wl.step(mc, 0)                       # first launches set kernel attributes outside capture
+    torch.cuda.synchronize()
+    graphs = []
+    for cp in range(len(wl.layers)):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            wl.step(mc, cp)
+        graphs.append(g)
+    torch.cuda.synchronize()
+    return graphs
 
 
 def kernel_times(mc, torch, wl, steps):
@@ -225,10 +244,14 @@ def main():
     def measure(T):
         wl.set_tokens(mc, torch, synthetic, T)
         ms, wall = time_steps(mc, torch, wl, args.steps, args.warmup)
+        ms_graph = None
+        if args.graph:
+            ms_graph, _ = time_steps(mc, torch, wl, args.steps, args.warmup, capture_steps(mc, torch, wl))
         kt = kernel_times(mc, torch, wl, args.steps)
         ab = wl.alg_bytes()
         touched, pruned = wl.touched()
-        return dict(T=T, ms=ms, wall=wall, kernels=kt, alg=ab, touched=touched, pruned=pruned)
+        return dict(T=T, ms=ms, ms_graph=ms_graph, wall=wall, kernels=kt, alg=ab, touched=touched,
+                    pruned=pruned)
 
     sweep = []
     for t in [int(v) for v in args.sweep.split(",") if v]:
@@ -236,6 +259,7 @@ def main():
             m = measure(t)
             sweep.append(dict(tokens=t, tokens_per_s=round(t / (m["ms"] / 1e3), 1),
                               ms_per_step=round(m["ms"], 5),
+                              ms_per_step_graph=m["ms_graph"] and round(m["ms_graph"], 5),
                               step_hbm_gbs=round(m["alg"]["step"] / (m["ms"] * 1e6), 1),
                               gateup_hbm_frac=round(m["alg"]["gateup"] / (m["kernels"]["gateup"]["avg_us"] * 1e3) / HBM_PEAK_GBS, 4),
                               experts_touched=len(m["touched"])))
@@ -258,6 +282,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 5),
+        "ms_per_step_graph": main_m["ms_graph"] and round(main_m["ms_graph"], 5),
+        "timing": "eager launches of route_and_prune + moe_forward per step, HIP events",
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

@@ -2,6 +2,6 @@
 #include "fwd_kernels.hpp"
 
 namespace mc {
-template hipError_t launch_down<2>(const uint16_t*, size_t, const LayerArgs&, const mc_routing&,
-                                    int, float*, size_t, int, int, hipStream_t);
+template hipError_t launch_down<2>(const Hidden&, const LayerArgs&, const mc_routing&, int,
+                                    float*, size_t, int, int, hipStream_t);
 }  // namespace mc

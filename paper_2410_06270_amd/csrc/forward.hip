@@ -39,34 +39,59 @@ __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ 
 // --------------------------------------------------------------- launchers --
 
 // Split of the down projection's reduction so that small batches still give
-// about 2048 workgroups; one split for prefill-sized batches.
+// about 1024 workgroups; one split for prefill-sized batches.
 int forward_nsplit(int T, int E, int k, int d, int ffn) {
-  const int tiles = d / 128;
+  const int tiles = (d + 255) / 256;
   const int active = (T * k) < E ? (T * k) : E;
-  int s = (2048 + tiles * active - 1) / (tiles * active);
+  int s = (1024 + tiles * active - 1) / (tiles * active);
   const int maxs = (ffn / kTileCols) / 4;
   if (T > kDecodeMaxT) s = 1;
   if (s > maxs) s = maxs;
-  if (s > 8) s = 8;
+  if (s > kMaxNsplit) s = kMaxNsplit;
   if (s < 1) s = 1;
   return s;
 }
 
+// Split of the gate/up reduction (over d) when the active experts give fewer
+// than two workgroups per CU (batches of a few tokens); each split covers at
+// least two 128-column chunks.
+int forward_ksplit(int T, int E, int k, int d, int ffn) {
+  if (T > 16) return 1;
+  const int active = (T * k) < E ? (T * k) : E;
+  const int wgs = (ffn / (16 * kWavesPerWg)) * active;
+  int s = (512 + wgs - 1) / wgs;
+  const int maxs = (d / kTileCols) / 2;
+  if (s > maxs) s = maxs;
+  if (s > kMaxKsplit) s = kMaxKsplit;
+  if (s < 1) s = 1;
+  return s;
+}
+
+// Workspace: h planes (bf16 hi, lo) | gate/up partials (when split) | down
+// partials, each part rounded up to 256 bytes.
+static size_t round256(size_t b) { return ((b + 255) / 256) * 256; }
+
 size_t forward_workspace_bytes(int T, int E, int k, int d, int ffn) {
   const size_t P = (size_t)T * k;
-  const size_t h = 2 * P * ffn * sizeof(uint16_t);
+  const int ks = forward_ksplit(T, E, k, d, ffn);
+  const size_t h = round256(2 * P * ffn * sizeof(uint16_t));
+  const size_t gu = ks > 1 ? round256((size_t)ks * 2 * P * ffn * sizeof(float)) : 0;
   const size_t part = (size_t)forward_nsplit(T, E, k, d, ffn) * P * d * sizeof(float);
-  return ((h + 255) / 256) * 256 + part;
+  return h + gu + part;
 }
 
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
                           void* ws, hipStream_t stream) {
   const int T = r.T, k = r.k;
   const size_t P = (size_t)T * k;
-  uint16_t* h_hi = static_cast<uint16_t*>(ws);
-  const size_t plane = P * L.ffn;
-  const size_t hbytes = ((2 * plane * sizeof(uint16_t) + 255) / 256) * 256;
-  float* partial = reinterpret_cast<float*>(static_cast<char*>(ws) + hbytes);
+  Hidden hid;
+  hid.plane = P * L.ffn;
+  hid.h_hi = static_cast<uint16_t*>(ws);
+  hid.ksplit = forward_ksplit(T, r.E, k, L.d, L.ffn);
+  char* p = static_cast<char*>(ws) + round256(2 * hid.plane * sizeof(uint16_t));
+  hid.gu_part = reinterpret_cast<float*>(p);
+  if (hid.ksplit > 1) p += round256((size_t)hid.ksplit * 2 * hid.plane * sizeof(float));
+  float* partial = reinterpret_cast<float*>(p);
   const size_t part_stride = P * L.d;
   const int nsplit = forward_nsplit(T, r.E, k, L.d, L.ffn);
   // An expert sees at most min(T, 16*ntmax) tokens per workgroup.
@@ -74,15 +99,15 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
   const int xs_bytes = ntmax <= 2 ? kXsBytesSmall : kXsBytesLarge;
   hipError_t err;
   timing_begin(stream, kSiteGateUp);
-  if (L.G == 128) err = launch_gateup<1>(x, L, r, h_hi, h_hi + plane, ntmax, xs_bytes, stream);
-  else if (L.G == 64) err = launch_gateup<2>(x, L, r, h_hi, h_hi + plane, ntmax, xs_bytes, stream);
-  else err = launch_gateup<4>(x, L, r, h_hi, h_hi + plane, ntmax, xs_bytes, stream);
+  if (L.G == 128) err = launch_gateup<1>(x, L, r, hid, ntmax, xs_bytes, stream);
+  else if (L.G == 64) err = launch_gateup<2>(x, L, r, hid, ntmax, xs_bytes, stream);
+  else err = launch_gateup<4>(x, L, r, hid, ntmax, xs_bytes, stream);
   timing_end(stream, kSiteGateUp);
   if (err != hipSuccess) return err;
   timing_begin(stream, kSiteDown);
-  if (L.G == 128) err = launch_down<1>(h_hi, plane, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
-  else if (L.G == 64) err = launch_down<2>(h_hi, plane, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
-  else err = launch_down<4>(h_hi, plane, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
+  if (L.G == 128) err = launch_down<1>(hid, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
+  else if (L.G == 64) err = launch_down<2>(hid, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
+  else err = launch_down<4>(hid, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
   timing_end(stream, kSiteDown);
   if (err != hipSuccess) return err;
   timing_begin(stream, kSiteCombine);

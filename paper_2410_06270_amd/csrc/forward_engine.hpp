@@ -28,16 +28,23 @@ constexpr uint32_t kMagic2 = 0x43004300u;     // bf16 128.0 in both halves
 constexpr int kRowPad = 8;                    // bf16 elements of padding per slab row
 constexpr int kSxBytes = 4 * 1024;            // group sums of the staged slab (LDS)
 
+constexpr int kWavesPerWg = 8;                // workgroups of 512 threads share one slab
+constexpr int kMaxNsplit = 8;                 // largest split of the down reduction
+constexpr int kMaxKsplit = 2;                 // largest split of the gate/up reduction
 // LDS for the staged activation slab.  Batches whose experts see at most 32
-// tokens per workgroup use 36 KB (+4 KB group sums: four workgroups per CU);
-// up to 64 tokens use 68 KB.
-constexpr int kXsBytesSmall = 36 * 1024;
-constexpr int kXsBytesLarge = 68 * 1024;
+// tokens per workgroup are held to 128 registers (four waves per SIMD, two
+// workgroups per CU) and get 75.5 KB; up to 64 tokens one workgroup fits a CU
+// and gets 100 KB.
+constexpr int kXsBytesSmall = 75 * 1024 + 512;
+constexpr int kXsBytesLarge = 100 * 1024;
+constexpr int kLdsPerCu = 160 * 1024;
+static_assert(2 * (kXsBytesSmall + 4 * 1024 + 32 * 4) <= kLdsPerCu, "two workgroups per CU");
+static_assert(kXsBytesLarge + 4 * 1024 + 64 * 4 <= kLdsPerCu, "one workgroup per CU");
 // Chunks (16 rows x 128 columns of codes) kept in flight per stream.  The slab
 // is a multiple of this many chunks, so it is smaller where the slab rows are
-// many (token blocks x planes) or the registers few (groups per chunk).
+// many (token blocks) or the registers few (groups per chunk).
 __host__ __device__ constexpr int prefetch_depth(int ntb, int gpc, int planes) {
-  return (ntb >= 3 || gpc >= 4 || ntb * planes >= 4) ? 2 : 4;
+  return (ntb >= 3 || gpc >= 4) ? 2 : 4;
 }
 // Smallest slab (one ring of chunks) of the worst case of each token-block
 // count must fit its LDS budget: (planes x tokens + zero row) x (columns + pad) x 2 bytes.
@@ -154,13 +161,13 @@ __device__ __forceinline__ void load_chunk(uint32_t (&w)[2][BITS], uint32_t (&s)
   }
 }
 
-// Copy rows [nt][ks, ks+kw) of every plane into LDS and form the sums of each
-// group of G columns (lanes of a wave hold consecutive 8-column pieces of one
-// row, so a group is G/8 neighbouring lanes: butterfly in a fixed order).
-template <int PLANES, typename RowFn>
-__device__ __forceinline__ void stage_slab(uint16_t* xs, float* sxs, RowFn rowsrc,
-                                           size_t plane_stride, int nt, int rows, int ks, int kw,
-                                           int RS, int G) {
+// Fill the slab: rows [nt] x columns [ks, ks+kw) of every plane, 8 columns
+// (16 bytes) per piece from src(m, k, v[PLANES]), and form the sums of each
+// group of G columns (lanes of a wave hold consecutive pieces of one row, so a
+// group is G/8 neighbouring lanes: butterfly in a fixed order).
+template <int PLANES, typename PieceFn>
+__device__ __forceinline__ void stage_slab(uint16_t* xs, float* sxs, PieceFn src, int nt, int rows,
+                                           int ks, int kw, int RS, int G) {
   const int lane = threadIdx.x & 63;
   const int pieces = kw >> 3;
   const int total = nt * pieces;
@@ -173,11 +180,12 @@ __device__ __forceinline__ void stage_slab(uint16_t* xs, float* sxs, RowFn rowsr
     if (valid) {
       m = idx / pieces;
       p = idx - m * pieces;
+      u32x4 v[PLANES];
+      src(m, ks + 8 * p, v);
 #pragma unroll
       for (int pl = 0; pl < PLANES; ++pl) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(rowsrc(m) + pl * plane_stride + ks + 8 * p);
-        *reinterpret_cast<u32x4*>(xs + (size_t)(pl * nt + m) * RS + 8 * p) = v;
-        sum += sum8_bf16(v);
+        *reinterpret_cast<u32x4*>(xs + (size_t)(pl * nt + m) * RS + 8 * p) = v[pl];
+        sum += sum8_bf16(v[pl]);
       }
     }
     for (int off = 1; off < gp; off <<= 1) sum += __shfl_xor(sum, off);
@@ -186,8 +194,6 @@ __device__ __forceinline__ void stage_slab(uint16_t* xs, float* sxs, RowFn rowsr
   __syncthreads();
 }
 
-// One chunk (4 MFMA steps of 32 columns) of both streams.  arow[tb][pl] is
-// this lane's activation row in the slab (a zero row for padding tokens).
 template <int BITS, int NT, int PLANES, int GPC>
 __device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
                                               const uint32_t (&s)[2][GPC], f32x4 (&acc)[2][NT],
@@ -227,9 +233,9 @@ __device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
 // activations of nt (<= 16*NT) tokens; a ring of D chunks of packed words and
 // scale/zero words stays in flight in registers across chunk and slab
 // boundaries.
-template <int BITS, int NT, int PLANES, int GPC, typename RowFn>
+template <int BITS, int NT, int PLANES, int GPC, typename PieceFn>
 __device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int c_end,
-                                            RowFn rowsrc, size_t plane_stride, int nt, int G,
+                                            PieceFn src, int nt, int G,
                                             uint16_t* xs, float* sxs, int xs_elems,
                                             f32x4 (&tot)[2][NT]) {
   constexpr int D = prefetch_depth(NT, GPC, PLANES);
@@ -275,8 +281,7 @@ __device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int 
   for (int c0 = c_begin; c0 < c_end; c0 += slab_chunks) {
     const int c1 = (c0 + slab_chunks) < c_end ? (c0 + slab_chunks) : c_end;
     __syncthreads();
-    stage_slab<PLANES>(xs, sxs, rowsrc, plane_stride, nt, rows, c0 * kTileCols,
-                       (c1 - c0) * kTileCols, RS, G);
+    stage_slab<PLANES>(xs, sxs, src, nt, rows, c0 * kTileCols, (c1 - c0) * kTileCols, RS, G);
     int c = c0;
     for (; c + D <= c1; c += D) {
 #pragma unroll
@@ -300,17 +305,16 @@ __device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int 
 // fixed at compile time (no token-block branches inside the loop).  NTMAX is
 // the largest block count a launch can see; tot[st][tb] for blocks beyond the
 // workgroup's count are left as they were.
-template <int BITS, int GPC, int PLANES, int NTMAX, typename RowFn>
-__device__ __forceinline__ void run_width(const Streams& sp, int c_begin, int c_end, RowFn rowsrc,
-                                          size_t plane_stride, int nt, int G, uint16_t* xs,
-                                          float* sxs, int xs_elems, f32x4 (&tot)[2][NTMAX]) {
+template <int BITS, int GPC, int PLANES, int NTMAX, typename PieceFn>
+__device__ __forceinline__ void run_width(const Streams& sp, int c_begin, int c_end, PieceFn src,
+                                          int nt, int G, uint16_t* xs, float* sxs, int xs_elems,
+                                          f32x4 (&tot)[2][NTMAX]) {
   const int ntb = (nt + 15) >> 4;
   if (NTMAX == 1 || ntb == 1) {
     f32x4 t[2][1];
     t[0][0] = tot[0][0];
     t[1][0] = tot[1][0];
-    stream_pair<BITS, 1, PLANES, GPC>(sp, c_begin, c_end, rowsrc, plane_stride, nt, G, xs, sxs,
-                                      xs_elems, t);
+    stream_pair<BITS, 1, PLANES, GPC>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, t);
     tot[0][0] = t[0][0];
     tot[1][0] = t[1][0];
   } else if (NTMAX == 2 || ntb == 2) {
@@ -320,26 +324,32 @@ __device__ __forceinline__ void run_width(const Streams& sp, int c_begin, int c_
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int b = 0; b < N; ++b) t[j][b] = tot[j][b];
-    stream_pair<BITS, N, PLANES, GPC>(sp, c_begin, c_end, rowsrc, plane_stride, nt, G, xs, sxs,
-                                      xs_elems, t);
+    stream_pair<BITS, N, PLANES, GPC>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, t);
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int b = 0; b < N; ++b) tot[j][b] = t[j][b];
   } else {
-    stream_pair<BITS, NTMAX, PLANES, GPC>(sp, c_begin, c_end, rowsrc, plane_stride, nt, G, xs, sxs,
-                                          xs_elems, tot);
+    stream_pair<BITS, NTMAX, PLANES, GPC>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, tot);
   }
 }
 
 // Launchers (one translation unit per kernel and group size).
+// Hidden activations between the two kernels: bf16 hi/lo planes, or (small
+// batches, gate/up split over d) fp32 partial sums of gate and up per split.
+struct Hidden {
+  uint16_t* h_hi;        // [P][ffn]
+  size_t plane;          // elements per plane (h_lo = h_hi + plane)
+  float* gu_part;        // [ksplit][2][P][ffn] when ksplit > 1
+  int ksplit;
+};
+
 template <int GPC>
 hipError_t launch_gateup(const uint16_t* x, const LayerArgs& L, const mc_routing& r,
-                         uint16_t* h_hi, uint16_t* h_lo, int ntmax, int xs_bytes,
-                         hipStream_t stream);
+                         const Hidden& h, int ntmax, int xs_bytes, hipStream_t stream);
 template <int GPC>
-hipError_t launch_down(const uint16_t* h_hi, size_t plane_stride, const LayerArgs& L,
-                       const mc_routing& r, int nsplit, float* partial, size_t part_stride,
-                       int ntmax, int xs_bytes, hipStream_t stream);
+hipError_t launch_down(const Hidden& h, const LayerArgs& L, const mc_routing& r, int nsplit,
+                       float* partial, size_t part_stride, int ntmax, int xs_bytes,
+                       hipStream_t stream);
 
 }  // namespace mc

@@ -9,17 +9,16 @@
 namespace mc {
 
 // Per-width dispatch: the expert's width is uniform in a workgroup.
-template <int GPC, int PLANES, int NTMAX, typename RowFn>
+template <int GPC, int PLANES, int NTMAX, typename PieceFn>
 __device__ __forceinline__ void run_expert(int bits, const Streams& sp, int c_begin, int c_end,
-                                           RowFn rowsrc, size_t plane_stride, int nt, int G,
-                                           uint16_t* xs, float* sxs, int xs_elems,
-                                           f32x4 (&tot)[2][NTMAX]) {
+                                           PieceFn src, int nt, int G, uint16_t* xs, float* sxs,
+                                           int xs_elems, f32x4 (&tot)[2][NTMAX]) {
   if (bits == 1)
-    run_width<1, GPC, PLANES, NTMAX>(sp, c_begin, c_end, rowsrc, plane_stride, nt, G, xs, sxs, xs_elems, tot);
+    run_width<1, GPC, PLANES, NTMAX>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, tot);
   else if (bits == 2)
-    run_width<2, GPC, PLANES, NTMAX>(sp, c_begin, c_end, rowsrc, plane_stride, nt, G, xs, sxs, xs_elems, tot);
+    run_width<2, GPC, PLANES, NTMAX>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, tot);
   else
-    run_width<3, GPC, PLANES, NTMAX>(sp, c_begin, c_end, rowsrc, plane_stride, nt, G, xs, sxs, xs_elems, tot);
+    run_width<3, GPC, PLANES, NTMAX>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, tot);
 }
 
 // Buffer resources of one stream: row block rb of matrix m of expert e,
@@ -35,26 +34,31 @@ __device__ __forceinline__ void stream_rsrc(const LayerArgs& L, int e, int m, in
   s = make_rsrc(sbase, (uint32_t)(c_end - c_begin) * gpc * 64u);
 }
 
+__device__ __forceinline__ void zero_tot(f32x4* t, int n) {
+  for (int i = 0; i < n; ++i) t[i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+}
+
 // ---------------------------------------------------------------- gate/up --
-// Workgroup: expert e, 64 rows (4 waves x 16) of gate and up, up to
-// 16*NTMAX of the expert's tokens.  Writes h = silu(gate x) * (up x)
-// as bf16 hi/lo planes.
+// Workgroup: expert e, 16*kWavesPerWg rows (one 16-row block per wave) of
+// gate and up, up to 16*NTMAX of the expert's tokens, one of ksplit ranges of
+// the d reduction.  ksplit == 1 writes h = silu(gate x) * (up x) as bf16
+// hi/lo planes; ksplit > 1 writes the fp32 partial sums of gate and up, which
+// the down kernel adds up (in split order) before the SiLU.
 // Up to 32 tokens per workgroup the kernels are held to 128 registers so that
-// four workgroups (16 waves) share a CU.
+// two workgroups (16 waves) share a CU.
 template <int GPC, int NTMAX>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2)))
-gateup_kernel(const uint16_t* __restrict__ x, LayerArgs L,
-                                                     const int32_t* __restrict__ counts,
-                                                     const int32_t* __restrict__ offsets,
-                                                     const int32_t* __restrict__ pair_token,
-                                                     uint16_t* __restrict__ h_hi,
-                                                     uint16_t* __restrict__ h_lo, int xs_bytes) {
+__global__ void __launch_bounds__(64 * kWavesPerWg)
+__attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2))) gateup_kernel(
+    const uint16_t* __restrict__ x, LayerArgs L, const int32_t* __restrict__ counts,
+    const int32_t* __restrict__ offsets, const int32_t* __restrict__ pair_token, Hidden hid,
+    int xs_bytes) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ int toks[16 * NTMAX];
   uint16_t* xs = reinterpret_cast<uint16_t*>(smem);
   float* sxs = reinterpret_cast<float*>(smem + xs_bytes);
   const int e = blockIdx.y;
-  const int t0 = blockIdx.z * 16 * NTMAX;
+  const int chunk = blockIdx.z / hid.ksplit, split = blockIdx.z - chunk * hid.ksplit;
+  const int t0 = chunk * 16 * NTMAX;
   const int ce = counts[e];
   if (t0 >= ce) return;
   const int nt = (ce - t0) < 16 * NTMAX ? (ce - t0) : 16 * NTMAX;
@@ -62,50 +66,60 @@ gateup_kernel(const uint16_t* __restrict__ x, LayerArgs L,
   for (int i = threadIdx.x; i < nt; i += blockDim.x) toks[i] = pair_token[pbase + i];
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int K = L.d, G = L.G, ntiles = K / kTileCols;
+  const int per = (ntiles + hid.ksplit - 1) / hid.ksplit;
+  const int c_begin = split * per;
+  const int c_end = (c_begin + per) < ntiles ? (c_begin + per) : ntiles;
   const int b = L.cum_bits[e + 1] - L.cum_bits[e];
-  const int rb = blockIdx.x * 4 + wave;
-  Streams sp;
-  for (int m = 0; m < 2; ++m) stream_rsrc(L, e, m, rb, K, 0, ntiles, sp.w[m], sp.s[m]);
-  sp.lane_w = (uint32_t)lane * b * 4u;
-  sp.lane_s = (uint32_t)(lane & 15) * 4u;
+  const int rb = blockIdx.x * kWavesPerWg + wave;
   f32x4 tot[2][NTMAX];
-#pragma unroll
-  for (int st = 0; st < 2; ++st)
-#pragma unroll
-    for (int tb = 0; tb < NTMAX; ++tb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) tot[st][tb][i] = 0.0f;
-  auto rowsrc = [&](int m) { return x + (size_t)toks[m] * K; };
-  run_expert<GPC, 1, NTMAX>(b, sp, 0, ntiles, rowsrc, 0, nt, G, xs, sxs, xs_bytes / 2, tot);
+  zero_tot(&tot[0][0], 2 * NTMAX);
+  if (c_begin < c_end) {
+    Streams sp;
+    for (int m = 0; m < 2; ++m) stream_rsrc(L, e, m, rb, K, c_begin, c_end, sp.w[m], sp.s[m]);
+    sp.lane_w = (uint32_t)lane * b * 4u;
+    sp.lane_s = (uint32_t)(lane & 15) * 4u;
+    auto src = [&](int m, int k, u32x4 (&v)[1]) {
+      v[0] = *reinterpret_cast<const u32x4*>(x + (size_t)toks[m] * K + k);
+    };
+    run_expert<GPC, 1, NTMAX>(b, sp, c_begin, c_end, src, nt, G, xs, sxs, xs_bytes / 2, tot);
+  }
   const int n = rb * 16 + (lane & 15);
+  const size_t P = hid.plane / L.ffn;
 #pragma unroll
   for (int tb = 0; tb < NTMAX; ++tb) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = tb * 16 + 4 * (lane >> 4) + i;
       if (m < nt) {
-        const float h = silu(tot[0][tb][i]) * tot[1][tb][i];
-        const uint16_t hi = float_to_bf16(h);
-        const uint16_t lo = float_to_bf16(h - bf16_bits_to_float(hi));
         const size_t o = (size_t)(pbase + m) * L.ffn + n;
-        h_hi[o] = hi;
-        h_lo[o] = lo;
+        if (hid.ksplit == 1) {
+          const float h = silu(tot[0][tb][i]) * tot[1][tb][i];
+          const uint16_t hi = float_to_bf16(h);
+          const uint16_t lo = float_to_bf16(h - bf16_bits_to_float(hi));
+          hid.h_hi[o] = hi;
+          hid.h_hi[hid.plane + o] = lo;
+        } else {
+          float* part = hid.gu_part + (size_t)split * 2 * P * L.ffn;
+          part[o] = tot[0][tb][i];
+          part[P * L.ffn + o] = tot[1][tb][i];
+        }
       }
     }
   }
 }
 
 // ------------------------------------------------------------------- down --
-// Workgroup: expert e, 128 output rows (4 waves x 2 row blocks), one split of
-// the ffn reduction, up to 16*NTMAX of the expert's pairs -> fp32 partials.
+// Workgroup: expert e, 32*kWavesPerWg output rows (two 16-row blocks per
+// wave), one split of the ffn reduction, up to 16*NTMAX of the expert's pairs
+// -> fp32 partials.  When d is not a multiple of the workgroup's rows, the
+// surplus waves of the last workgroup repeat the last row blocks (identical
+// values written twice) so that every wave takes part in the staging barriers.
 template <int GPC, int NTMAX>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2)))
-down_kernel(const uint16_t* __restrict__ h_hi,
-                                                   size_t plane_stride, LayerArgs L,
-                                                   const int32_t* __restrict__ counts,
-                                                   const int32_t* __restrict__ offsets, int nsplit,
-                                                   float* __restrict__ partial, size_t part_stride,
-                                                   int xs_bytes) {
+__global__ void __launch_bounds__(64 * kWavesPerWg)
+__attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2))) down_kernel(
+    Hidden hid, LayerArgs L, const int32_t* __restrict__ counts,
+    const int32_t* __restrict__ offsets, int nsplit, float* __restrict__ partial,
+    size_t part_stride, int xs_bytes) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint16_t* xs = reinterpret_cast<uint16_t*>(smem);
   float* sxs = reinterpret_cast<float*>(smem + xs_bytes);
@@ -122,22 +136,54 @@ down_kernel(const uint16_t* __restrict__ h_hi,
   const int per = (ntiles + nsplit - 1) / nsplit;
   const int c_begin = split * per;
   const int c_end = (c_begin + per) < ntiles ? (c_begin + per) : ntiles;
-  const int rb0 = blockIdx.x * 8 + wave * 2;
+  const int last_rb = L.d / kTileRows - 2;
+  const int rb_want = (blockIdx.x * kWavesPerWg + wave) * 2;
+  const int rb0 = rb_want < last_rb ? rb_want : last_rb;
   f32x4 tot[2][NTMAX];
-#pragma unroll
-  for (int st = 0; st < 2; ++st)
-#pragma unroll
-    for (int tb = 0; tb < NTMAX; ++tb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) tot[st][tb][i] = 0.0f;
+  zero_tot(&tot[0][0], 2 * NTMAX);
   if (c_begin < c_end) {
     Streams sp;
     for (int j = 0; j < 2; ++j) stream_rsrc(L, e, 2, rb0 + j, K, c_begin, c_end, sp.w[j], sp.s[j]);
     sp.lane_w = (uint32_t)lane * b * 4u;
     sp.lane_s = (uint32_t)(lane & 15) * 4u;
-    auto rowsrc = [&](int m) { return h_hi + (size_t)(pbase + m) * K; };
-    run_expert<GPC, 2, NTMAX>(b, sp, c_begin, c_end, rowsrc, plane_stride, nt, G, xs, sxs,
-                              xs_bytes / 2, tot);
+    if (hid.ksplit == 1) {
+      auto src = [&](int m, int k, u32x4 (&v)[2]) {
+        const uint16_t* row = hid.h_hi + (size_t)(pbase + m) * K + k;
+        v[0] = *reinterpret_cast<const u32x4*>(row);
+        v[1] = *reinterpret_cast<const u32x4*>(row + hid.plane);
+      };
+      run_expert<GPC, 2, NTMAX>(b, sp, c_begin, c_end, src, nt, G, xs, sxs, xs_bytes / 2, tot);
+    } else {
+      // h from the gate/up partial sums (added in split order), as the
+      // ksplit == 1 gate/up epilogue would have formed it
+      const size_t P = hid.plane / K;
+      auto src = [&](int m, int k, u32x4 (&v)[2]) {
+        const size_t o = (size_t)(pbase + m) * K + k;
+        f32x4 g0 = {0.f, 0.f, 0.f, 0.f}, g1 = g0, u0 = g0, u1 = g0;
+        for (int s = 0; s < hid.ksplit; ++s) {
+          const float* part = hid.gu_part + (size_t)s * 2 * P * K + o;
+          g0 += *reinterpret_cast<const f32x4*>(part);
+          g1 += *reinterpret_cast<const f32x4*>(part + 4);
+          u0 += *reinterpret_cast<const f32x4*>(part + P * K);
+          u1 += *reinterpret_cast<const f32x4*>(part + P * K + 4);
+        }
+        uint32_t hi[4], lo[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float ha = silu(j < 2 ? g0[2 * j] : g1[2 * j - 4]) * (j < 2 ? u0[2 * j] : u1[2 * j - 4]);
+          const float hb = silu(j < 2 ? g0[2 * j + 1] : g1[2 * j - 3]) *
+                           (j < 2 ? u0[2 * j + 1] : u1[2 * j - 3]);
+          const uint16_t ahi = float_to_bf16(ha), bhi = float_to_bf16(hb);
+          const uint16_t alo = float_to_bf16(ha - bf16_bits_to_float(ahi));
+          const uint16_t blo = float_to_bf16(hb - bf16_bits_to_float(bhi));
+          hi[j] = (uint32_t)ahi | ((uint32_t)bhi << 16);
+          lo[j] = (uint32_t)alo | ((uint32_t)blo << 16);
+        }
+        v[0] = u32x4{hi[0], hi[1], hi[2], hi[3]};
+        v[1] = u32x4{lo[0], lo[1], lo[2], lo[3]};
+      };
+      run_expert<GPC, 2, NTMAX>(b, sp, c_begin, c_end, src, nt, G, xs, sxs, xs_bytes / 2, tot);
+    }
   }
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
@@ -164,56 +210,55 @@ static hipError_t allow_lds(K kernel, int bytes) {
 
 template <int GPC, int NTMAX>
 static hipError_t launch_gateup_nt(const uint16_t* x, const LayerArgs& L, const mc_routing& r,
-                                   uint16_t* h_hi, uint16_t* h_lo, int xs_bytes,
-                                   hipStream_t stream) {
+                                   const Hidden& h, int xs_bytes, hipStream_t stream) {
   static bool attr = false;
   if (!attr) {
-    hipError_t e = allow_lds(&gateup_kernel<GPC, NTMAX>, kXsBytesLarge + kSxBytes);
+    hipError_t e = allow_lds(&gateup_kernel<GPC, NTMAX>, kXsBytesLarge + kSxBytes + 512);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int chunks = (r.T + 16 * NTMAX - 1) / (16 * NTMAX);
-  hipLaunchKernelGGL((gateup_kernel<GPC, NTMAX>), dim3(L.ffn / 64, L.E, chunks), dim3(256),
-                     xs_bytes + kSxBytes, stream, x, L, r.counts, r.offsets, r.pair_token, h_hi,
-                     h_lo, xs_bytes);
+  hipLaunchKernelGGL((gateup_kernel<GPC, NTMAX>),
+                     dim3(L.ffn / (16 * kWavesPerWg), L.E, chunks * h.ksplit),
+                     dim3(64 * kWavesPerWg), xs_bytes + kSxBytes, stream, x, L, r.counts,
+                     r.offsets, r.pair_token, h, xs_bytes);
   return hipGetLastError();
 }
 
 template <int GPC, int NTMAX>
-static hipError_t launch_down_nt(const uint16_t* h_hi, size_t plane_stride, const LayerArgs& L,
-                                 const mc_routing& r, int nsplit, float* partial,
-                                 size_t part_stride, int xs_bytes, hipStream_t stream) {
+static hipError_t launch_down_nt(const Hidden& h, const LayerArgs& L, const mc_routing& r,
+                                 int nsplit, float* partial, size_t part_stride, int xs_bytes,
+                                 hipStream_t stream) {
   static bool attr = false;
   if (!attr) {
-    hipError_t e = allow_lds(&down_kernel<GPC, NTMAX>, kXsBytesLarge + kSxBytes);
+    hipError_t e = allow_lds(&down_kernel<GPC, NTMAX>, kXsBytesLarge + kSxBytes + 512);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int chunks = (r.T + 16 * NTMAX - 1) / (16 * NTMAX);
-  hipLaunchKernelGGL((down_kernel<GPC, NTMAX>), dim3(L.d / 128, L.E, chunks * nsplit), dim3(256),
-                     xs_bytes + kSxBytes, stream, h_hi, plane_stride, L, r.counts, r.offsets,
-                     nsplit, partial, part_stride, xs_bytes);
+  const int rows_per_wg = 32 * kWavesPerWg;
+  hipLaunchKernelGGL((down_kernel<GPC, NTMAX>),
+                     dim3((L.d + rows_per_wg - 1) / rows_per_wg, L.E, chunks * nsplit),
+                     dim3(64 * kWavesPerWg), xs_bytes + kSxBytes, stream, h, L, r.counts,
+                     r.offsets, nsplit, partial, part_stride, xs_bytes);
   return hipGetLastError();
 }
 
 template <int GPC>
 hipError_t launch_gateup(const uint16_t* x, const LayerArgs& L, const mc_routing& r,
-                         uint16_t* h_hi, uint16_t* h_lo, int ntmax, int xs_bytes,
-                         hipStream_t stream) {
-  if (ntmax == 1) return launch_gateup_nt<GPC, 1>(x, L, r, h_hi, h_lo, xs_bytes, stream);
-  if (ntmax == 2) return launch_gateup_nt<GPC, 2>(x, L, r, h_hi, h_lo, xs_bytes, stream);
-  return launch_gateup_nt<GPC, 4>(x, L, r, h_hi, h_lo, xs_bytes, stream);
+                         const Hidden& h, int ntmax, int xs_bytes, hipStream_t stream) {
+  if (ntmax == 1) return launch_gateup_nt<GPC, 1>(x, L, r, h, xs_bytes, stream);
+  if (ntmax == 2) return launch_gateup_nt<GPC, 2>(x, L, r, h, xs_bytes, stream);
+  return launch_gateup_nt<GPC, 4>(x, L, r, h, xs_bytes, stream);
 }
 
 template <int GPC>
-hipError_t launch_down(const uint16_t* h_hi, size_t plane_stride, const LayerArgs& L,
-                       const mc_routing& r, int nsplit, float* partial, size_t part_stride,
-                       int ntmax, int xs_bytes, hipStream_t stream) {
-  if (ntmax == 1)
-    return launch_down_nt<GPC, 1>(h_hi, plane_stride, L, r, nsplit, partial, part_stride, xs_bytes, stream);
-  if (ntmax == 2)
-    return launch_down_nt<GPC, 2>(h_hi, plane_stride, L, r, nsplit, partial, part_stride, xs_bytes, stream);
-  return launch_down_nt<GPC, 4>(h_hi, plane_stride, L, r, nsplit, partial, part_stride, xs_bytes, stream);
+hipError_t launch_down(const Hidden& h, const LayerArgs& L, const mc_routing& r, int nsplit,
+                       float* partial, size_t part_stride, int ntmax, int xs_bytes,
+                       hipStream_t stream) {
+  if (ntmax == 1) return launch_down_nt<GPC, 1>(h, L, r, nsplit, partial, part_stride, xs_bytes, stream);
+  if (ntmax == 2) return launch_down_nt<GPC, 2>(h, L, r, nsplit, partial, part_stride, xs_bytes, stream);
+  return launch_down_nt<GPC, 4>(h, L, r, nsplit, partial, part_stride, xs_bytes, stream);
 }
 
 }  // namespace mc

@@ -3,5 +3,5 @@
 
 namespace mc {
 template hipError_t launch_gateup<1>(const uint16_t*, const LayerArgs&, const mc_routing&,
-                                      uint16_t*, uint16_t*, int, int, hipStream_t);
+                                      const Hidden&, int, int, hipStream_t);
 }  // namespace mc

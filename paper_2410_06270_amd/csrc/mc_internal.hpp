@@ -25,6 +25,7 @@ hipError_t launch_export(const uint32_t* words, const uint32_t* sz, int bits, in
 hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,
                         const mc_routing& r, hipStream_t stream);
 int forward_nsplit(int T, int E, int k, int d, int ffn);
+int forward_ksplit(int T, int E, int k, int d, int ffn);
 size_t forward_workspace_bytes(int T, int E, int k, int d, int ffn);
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
                           void* ws, hipStream_t stream);

@@ -52,35 +52,46 @@ __device__ void select_token(const float* __restrict__ logits, const uint8_t* __
                              uint16_t* s_ent, float* s_w) {
   const int lane = threadIdx.x & 63;
   const float* l = logits + (size_t)t * E;
+  float lv[4];
   unsigned long long key[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + 64 * j;
-    key[j] = (e < E) ? (((unsigned long long)ordered_bits(l[e]) << 32) | (unsigned)(0xffff - e)) : 0ull;
+    lv[j] = (e < E) ? l[e] : 0.0f;
+    key[j] = (e < E) ? (((unsigned long long)ordered_bits(lv[j]) << 32) | (unsigned)(0xffff - e)) : 0ull;
   }
+  const bool prot = important != nullptr && important[t] != 0;
   int my_e = 0;
+  float my_l = 0.0f;
   for (int r = 0; r < k; ++r) {
     unsigned long long best = key[0];
 #pragma unroll
     for (int j = 1; j < 4; ++j) best = key[j] > best ? key[j] : best;
     best = wave_max_u64(best);
     const int e = 0xffff - (int)(best & 0xffffu);
-    if (lane == r) my_e = e;
+    // the owner lane of expert e broadcasts its logit (exact: the key is not decoded)
+    float le = 0.0f;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      if (lane + 64 * j == e) key[j] = 0ull;
+      if (lane + 64 * j == e) {
+        le = lv[j];
+        key[j] = 0ull;
+      }
+    le = __shfl(le, e & 63);
+    if (lane == r) {
+      my_e = e;
+      my_l = le;
+    }
   }
-  const int e0 = __shfl(my_e, 0);
-  const int e1 = __shfl(my_e, 1 < k ? 1 : 0);
-  const float l0 = l[e0];
+  const float l0 = __shfl(my_l, 0);
+  const float l1 = __shfl(my_l, 1 < k ? 1 : 0);
   const bool mine = lane < k;
-  const double ex = mine ? exp((double)l[my_e] - (double)l0) : 0.0;
+  const double ex = mine ? exp((double)my_l - (double)l0) : 0.0;
   const double sum_all = rank_sum(ex);
-  const bool prot = important != nullptr && important[t] != 0;
   bool keep = mine;
   if (mine && lane > 0 && !prot) {
     if (k == 2) {
-      const float gap = l0 - l[e1];
+      const float gap = l0 - l1;
       keep = !(gap > delta32);
     } else {
       keep = !(ex < tau * sum_all);

@@ -212,6 +212,22 @@ def test_forward_tiny_tolerance(mc, tiny, T):
     assert mae < 2e-4, mae
 
 
+@pytest.mark.parametrize("d,T", [(640, 1), (768, 5), (1152, 1), (1152, 16), (1152, 17)])
+def test_forward_split_reduction(mc, d, T):
+    """Batches of at most 16 tokens split the gate/up reduction over d: ragged
+    splits (d = 640: 3 + 2 chunks), an empty last split (d = 1152: 3+3+3+0
+    chunks) and the unsplit path just above (T = 17)."""
+    mats, bits, G, logical = layer_case(1, d=d, ffn=384)
+    L = pack_gpu(mc, mats, bits, G)
+    x = synthetic.activations(1, T, d=d)
+    lg = synthetic.logits(1, T)
+    imp = synthetic.important_mask(1, T)
+    y, _ = forward_gpu(mc, L, x, lg, imp, 2, 0.3)
+    y_ref = oracle.moe_forward(x, oracle.route(lg, imp, 2, 0.3), logical, G)
+    mae, _ = check_tol(y, y_ref)
+    assert mae < 2e-4, mae
+
+
 def test_forward_skewed_and_dense(mc, tiny):
     """All tokens on one expert (full token chunks), then tau = 0 with every
     token protected (dense top-k)."""
@@ -263,3 +279,36 @@ def test_forward_deterministic(mc, tiny):
     y1, _ = forward_gpu(mc, L, x, lg, imp, 2, 0.3)
     y2, _ = forward_gpu(mc, L, x, lg, imp, 2, 0.3)
     np.testing.assert_array_equal(y1, y2)
+
+
+def test_graph_replay_matches_eager(mc, tiny):
+    """route_and_prune + moe_forward captured in a HIP graph: every replay, with
+    eager work and synchronisations between replays, equals the eager result."""
+    L, logical, G = tiny
+    T = 32
+    x = to_dev(synthetic.activations(1, T).view(np.int16))
+    lg = to_dev(synthetic.logits(1, T))
+    imp = to_dev(synthetic.important_mask(1, T))
+    r = mc.Routing(T, 4, 2)
+    y = torch.empty((T, L.d), dtype=torch.int16, device="cuda")
+    ws = torch.empty(mc.forward_workspace(T, 4, 2, L.d, L.ffn), dtype=torch.uint8, device="cuda")
+    mc.route_and_prune(lg, imp, 0.3, r)
+    mc.moe_forward(x, r, L, y, ws)
+    torch.cuda.synchronize()
+    y_eager = y.clone()
+    lists_eager = r.pair_token.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        mc.route_and_prune(lg, imp, 0.3, r)
+        mc.moe_forward(x, r, L, y, ws)
+    for rep in range(4):
+        y.zero_()
+        r.pair_token.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_eager), rep
+        assert torch.equal(r.pair_token[: int(r.offsets[-1])], lists_eager[: int(r.offsets[-1])]), rep
+        mc.moe_forward(x, r, L, y, ws)        # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_eager)
