@@ -39,13 +39,13 @@ __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ 
 // --------------------------------------------------------------- launchers --
 
 // Split of the down projection's reduction so that small batches still give
-// about 1024 workgroups; one split for prefill-sized batches.
+// about 1024 workgroups (the prefill GEMMs choose their own).
 int forward_nsplit(int T, int E, int k, int d, int ffn) {
+  if (T > kDecodeMaxT) return prefill_layout(T, E, k, d, ffn).nsplit;
   const int tiles = (d + 255) / 256;
   const int active = (T * k) < E ? (T * k) : E;
   int s = (1024 + tiles * active - 1) / (tiles * active);
   const int maxs = (ffn / kTileCols) / 4;
-  if (T > kDecodeMaxT) s = 1;
   if (s > maxs) s = maxs;
   if (s > kMaxNsplit) s = kMaxNsplit;
   if (s < 1) s = 1;
@@ -72,6 +72,7 @@ int forward_ksplit(int T, int E, int k, int d, int ffn) {
 static size_t round256(size_t b) { return ((b + 255) / 256) * 256; }
 
 size_t forward_workspace_bytes(int T, int E, int k, int d, int ffn) {
+  if (T > kDecodeMaxT) return prefill_layout(T, E, k, d, ffn).total;
   const size_t P = (size_t)T * k;
   const int ks = forward_ksplit(T, E, k, d, ffn);
   const size_t h = round256(2 * P * ffn * sizeof(uint16_t));
@@ -80,9 +81,39 @@ size_t forward_workspace_bytes(int T, int E, int k, int d, int ffn) {
   return h + gu + part;
 }
 
+static hipError_t launch_combine(const float* partial, size_t part_stride, int nsplit,
+                                 const mc_routing& r, int d, uint16_t* y, hipStream_t stream) {
+  timing_begin(stream, kSiteCombine);
+  const dim3 cgrid((d / 4 + 255) / 256, r.T);
+#define MC_COMBINE(S)                                                                              \
+  hipLaunchKernelGGL(combine_kernel<S>, cgrid, dim3(256), 0, stream, partial, part_stride,         \
+                     r.pair_pos, r.topk_w, r.k, d, y)
+  switch (nsplit) {
+    case 1: MC_COMBINE(1); break;
+    case 2: MC_COMBINE(2); break;
+    case 3: MC_COMBINE(3); break;
+    case 4: MC_COMBINE(4); break;
+    case 5: MC_COMBINE(5); break;
+    case 6: MC_COMBINE(6); break;
+    case 7: MC_COMBINE(7); break;
+    default: MC_COMBINE(8); break;
+  }
+#undef MC_COMBINE
+  timing_end(stream, kSiteCombine);
+  return hipGetLastError();
+}
+
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
                           void* ws, hipStream_t stream) {
   const int T = r.T, k = r.k;
+  if (T > kDecodeMaxT) {
+    float* partial = nullptr;
+    size_t part_stride = 0;
+    int nsplit = 1;
+    const hipError_t err = launch_prefill(x, L, r, ws, &partial, &part_stride, &nsplit, stream);
+    if (err != hipSuccess) return err;
+    return launch_combine(partial, part_stride, nsplit, r, L.d, y, stream);
+  }
   const size_t P = (size_t)T * k;
   Hidden hid;
   hid.plane = P * L.ffn;
@@ -110,24 +141,7 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
   else err = launch_down<4>(hid, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
   timing_end(stream, kSiteDown);
   if (err != hipSuccess) return err;
-  timing_begin(stream, kSiteCombine);
-  const dim3 cgrid((L.d / 4 + 255) / 256, T);
-#define MC_COMBINE(S)                                                                              \
-  hipLaunchKernelGGL(combine_kernel<S>, cgrid, dim3(256), 0, stream, partial, part_stride,         \
-                     r.pair_pos, r.topk_w, k, L.d, y)
-  switch (nsplit) {
-    case 1: MC_COMBINE(1); break;
-    case 2: MC_COMBINE(2); break;
-    case 3: MC_COMBINE(3); break;
-    case 4: MC_COMBINE(4); break;
-    case 5: MC_COMBINE(5); break;
-    case 6: MC_COMBINE(6); break;
-    case 7: MC_COMBINE(7); break;
-    default: MC_COMBINE(8); break;
-  }
-#undef MC_COMBINE
-  timing_end(stream, kSiteCombine);
-  return hipGetLastError();
+  return launch_combine(partial, part_stride, nsplit, r, L.d, y, stream);
 }
 
 }  // namespace mc

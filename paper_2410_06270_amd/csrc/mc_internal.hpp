@@ -10,7 +10,7 @@ constexpr int kDecodeMaxT = 64;        // up to this many tokens one workgroup h
 
 enum TimingSite {
   kSitePackSz, kSitePackCodes, kSiteExport, kSiteRouteFused, kSiteRouteSelect, kSiteRouteLists,
-  kSiteGateUp, kSiteDown, kSiteCombine, kNumSites
+  kSiteGateUp, kSiteDown, kSiteCombine, kSitePrefillPrep, kNumSites
 };
 void timing_begin(hipStream_t stream, int site);
 void timing_end(hipStream_t stream, int site);
@@ -27,6 +27,16 @@ hipError_t launch_route(const float* logits, const uint8_t* important, float del
 int forward_nsplit(int T, int E, int k, int d, int ffn);
 int forward_ksplit(int T, int E, int k, int d, int ffn);
 size_t forward_workspace_bytes(int T, int E, int k, int d, int ffn);
+// Workspace of the prefill path (byte offsets): expert tile tables, the
+// fragment-tiled copies of the routed x rows (bf16) and of h (fp16) with their
+// 32-column sums, and the fp32 down partials [nsplit][T*k][d].
+struct PrefillLayout {
+  size_t tables, x, xsum, h, hsum, part, total;
+  int f_max, mt_max, nsplit;
+};
+PrefillLayout prefill_layout(int T, int E, int k, int d, int ffn);
+hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routing& r, void* ws,
+                          float** partial, size_t* part_stride, int* nsplit, hipStream_t stream);
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
                           void* ws, hipStream_t stream);
 

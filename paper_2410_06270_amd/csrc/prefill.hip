@@ -1,0 +1,180 @@
+// prefill.hip -- set-up of the prefill grouped GEMMs (expert tile tables and
+// the fp16 fragment-tiled copy of the routed token rows) and their launcher.
+// The GEMM kernels are in prefill.hpp, one file per group size.
+#include "prefill.hpp"
+
+namespace mc {
+
+extern template hipError_t launch_prefill_gemm<1>(const LayerArgs&, const int32_t*, const PrefillTables&,
+                                                  const PrefillGemm&, bool, hipStream_t);
+extern template hipError_t launch_prefill_gemm<2>(const LayerArgs&, const int32_t*, const PrefillTables&,
+                                                  const PrefillGemm&, bool, hipStream_t);
+extern template hipError_t launch_prefill_gemm<4>(const LayerArgs&, const int32_t*, const PrefillTables&,
+                                                  const PrefillGemm&, bool, hipStream_t);
+
+// One workgroup: per expert e (thread e), fragment rows ceil(M_e/32) and
+// 256-token m-tiles ceil(M_e/256), exclusive scans, and the tables.
+__global__ void __launch_bounds__(256) prefill_setup_kernel(const int32_t* __restrict__ counts, int E,
+                                                            PrefillTables tb) {
+  __shared__ int snf[256], snm[256];
+  const int t = threadIdx.x;
+  const int c = t < E ? counts[t] : 0;
+  const int nf = (c + kPfFragRows - 1) / kPfFragRows;
+  const int nm = (c + PfCfg::kTokens - 1) / PfCfg::kTokens;
+  snf[t] = nf;
+  snm[t] = nm;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int a = t >= off ? snf[t - off] : 0;
+    const int b = t >= off ? snm[t - off] : 0;
+    __syncthreads();
+    snf[t] += a;
+    snm[t] += b;
+    __syncthreads();
+  }
+  const int fb = snf[t] - nf, mb = snm[t] - nm;
+  if (t < E) {
+    tb.ftile_base[t] = fb;
+    for (int i = 0; i < nf; ++i) tb.ftile_e[fb + i] = t;
+    for (int i = 0; i < nm; ++i) {
+      tb.mt_e[mb + i] = t;
+      tb.mt_j[mb + i] = i;
+    }
+  }
+  if (t == 255) {
+    tb.ftile_base[E] = snf[255];
+    *tb.mt_count = snm[255];
+  }
+}
+
+// One workgroup per fragment row f: its 32 routed rows of x (zero past the
+// expert's count) copied into the fragment layout (bf16, unchanged), and the
+// sums of every 32 columns of each row in fp32 (fixed order).
+__global__ void __launch_bounds__(256) prefill_gather_kernel(const uint16_t* __restrict__ x, int d, int E,
+                                                             const int32_t* __restrict__ offsets,
+                                                             const int32_t* __restrict__ pair_token,
+                                                             PrefillTables tb, uint16_t* __restrict__ xt,
+                                                             float* __restrict__ xsum) {
+  const int f = blockIdx.x;
+  if (f >= tb.ftile_base[E]) return;
+  const int e = tb.ftile_e[f];
+  const int pos0 = offsets[e] + (f - tb.ftile_base[e]) * kPfFragRows;
+  const int pend = offsets[e + 1];
+  const int parts = d / 32;
+  unsigned char* out = reinterpret_cast<unsigned char*>(xt);
+  for (int idx = threadIdx.x; idx < kPfFragRows * parts; idx += blockDim.x) {
+    const int m = idx / parts, p = idx - m * parts;
+    const int pos = pos0 + m;
+    u32x4 v[4] = {{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}};
+    float sum = 0.0f;
+    if (pos < pend) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(x + (size_t)pair_token[pos] * d + 32 * p);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = src[q];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          sum += bf16_bits_to_float(v[q][w] & 0xffffu) + bf16_bits_to_float(v[q][w] >> 16);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) *reinterpret_cast<u32x4*>(out + frag_offset(f, m, 32 * p + 8 * q, d)) = v[q];
+    xsum[((size_t)f * 32 + m) * parts + p] = sum;
+  }
+}
+
+static size_t round256(size_t b) { return ((b + 255) / 256) * 256; }
+
+PrefillLayout prefill_layout(int T, int E, int k, int d, int ffn) {
+  PrefillLayout pl;
+  const size_t P = (size_t)T * k;
+  pl.f_max = (int)((P + (size_t)(kPfFragRows - 1) * E) / kPfFragRows);
+  pl.mt_max = (int)((P + (size_t)(PfCfg::kTokens - 1) * E) / PfCfg::kTokens);
+  const int nt_down = (d + PfCfg::kRowsDown - 1) / PfCfg::kRowsDown;
+  const int wgs = pl.mt_max * nt_down;
+  int s = (1024 + wgs - 1) / wgs;
+  int maxs = (ffn / kTileCols) / 8;
+  if (maxs > 4) maxs = 4;
+  if (s > maxs) s = maxs;
+  if (s < 1) s = 1;
+  pl.nsplit = s;
+  const size_t rows = (size_t)pl.f_max * kPfFragRows;
+  pl.tables = 0;
+  const size_t tab = (size_t)(E + 1 + pl.f_max + 2 * pl.mt_max + 1) * sizeof(int32_t);
+  pl.x = round256(tab);
+  pl.xsum = pl.x + round256(rows * d * sizeof(uint16_t));
+  pl.h = pl.xsum + round256(rows * (d / 32) * sizeof(float));
+  pl.hsum = pl.h + round256(rows * ffn * sizeof(uint16_t));
+  pl.part = pl.hsum + round256(rows * (ffn / 32) * sizeof(float));
+  pl.total = pl.part + (size_t)pl.nsplit * P * d * sizeof(float);
+  return pl;
+}
+
+hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routing& r, void* ws,
+                          float** partial, size_t* part_stride, int* nsplit, hipStream_t stream) {
+  const PrefillLayout pl = prefill_layout(r.T, r.E, r.k, L.d, L.ffn);
+  char* base = static_cast<char*>(ws);
+  PrefillTables tb;
+  int32_t* t = reinterpret_cast<int32_t*>(base + pl.tables);
+  tb.ftile_base = t;
+  tb.ftile_e = t + (r.E + 1);
+  tb.mt_e = tb.ftile_e + pl.f_max;
+  tb.mt_j = tb.mt_e + pl.mt_max;
+  tb.mt_count = tb.mt_j + pl.mt_max;
+  tb.f_max = pl.f_max;
+  tb.mt_max = pl.mt_max;
+  uint16_t* xt = reinterpret_cast<uint16_t*>(base + pl.x);
+  float* xsum = reinterpret_cast<float*>(base + pl.xsum);
+  uint16_t* ht = reinterpret_cast<uint16_t*>(base + pl.h);
+  float* hsum = reinterpret_cast<float*>(base + pl.hsum);
+  *partial = reinterpret_cast<float*>(base + pl.part);
+  *part_stride = (size_t)r.T * r.k * L.d;
+  *nsplit = pl.nsplit;
+
+  timing_begin(stream, kSitePrefillPrep);
+  hipLaunchKernelGGL(prefill_setup_kernel, dim3(1), dim3(256), 0, stream, r.counts, r.E, tb);
+  hipLaunchKernelGGL(prefill_gather_kernel, dim3(pl.f_max), dim3(256), 0, stream, x, L.d, r.E,
+                     r.offsets, r.pair_token, tb, xt, xsum);
+  timing_end(stream, kSitePrefillPrep);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+
+  PrefillGemm gu;
+  gu.a = xt;
+  gu.asum = xsum;
+  gu.K = L.d;
+  gu.n_tiles = L.ffn / PfCfg::kRowsGateUp;
+  gu.c_per_split = L.d / kTileCols;
+  gu.nsplit = 1;
+  gu.h = ht;
+  gu.hsum = hsum;
+  gu.partial = nullptr;
+  gu.part_stride = 0;
+  timing_begin(stream, kSiteGateUp);
+  if (L.G == 128) err = launch_prefill_gemm<1>(L, r.offsets, tb, gu, true, stream);
+  else if (L.G == 64) err = launch_prefill_gemm<2>(L, r.offsets, tb, gu, true, stream);
+  else err = launch_prefill_gemm<4>(L, r.offsets, tb, gu, true, stream);
+  timing_end(stream, kSiteGateUp);
+  if (err != hipSuccess) return err;
+
+  PrefillGemm dn;
+  const int ntk = L.ffn / kTileCols;
+  dn.a = ht;
+  dn.asum = hsum;
+  dn.K = L.ffn;
+  dn.n_tiles = (L.d + PfCfg::kRowsDown - 1) / PfCfg::kRowsDown;
+  dn.c_per_split = (ntk + pl.nsplit - 1) / pl.nsplit;
+  dn.nsplit = pl.nsplit;
+  dn.h = nullptr;
+  dn.hsum = nullptr;
+  dn.partial = *partial;
+  dn.part_stride = *part_stride;
+  timing_begin(stream, kSiteDown);
+  if (L.G == 128) err = launch_prefill_gemm<1>(L, r.offsets, tb, dn, false, stream);
+  else if (L.G == 64) err = launch_prefill_gemm<2>(L, r.offsets, tb, dn, false, stream);
+  else err = launch_prefill_gemm<4>(L, r.offsets, tb, dn, false, stream);
+  timing_end(stream, kSiteDown);
+  return err;
+}
+
+}  // namespace mc

@@ -13,7 +13,7 @@ namespace {
 
 const char* const kSiteNames[kNumSites] = {
     "pack_scale_zero", "pack_codes", "export", "route_fused", "route_select",
-    "route_lists",     "gateup",     "down",   "combine"};
+    "route_lists",     "gateup",     "down",   "combine", "prefill_prep"};
 
 struct Pair {
   hipEvent_t start, stop;

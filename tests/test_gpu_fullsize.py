@@ -64,7 +64,7 @@ def test_mixtral_expert_words_bit_exact(mc, mixtral):
             np.testing.assert_array_equal(sz[sofs[(e, m)]: sofs[(e, m)] + p.size], p)
 
 
-@pytest.mark.parametrize("T", [1, 8, 32, 64])
+@pytest.mark.parametrize("T", [1, 8, 32, 64, 256, 4096])
 def test_mixtral_decode_sampled(mc, mixtral, T):
     c, mats, L = mixtral
     E, d, ffn, k, G, bits, tau = c["E"], c["d"], c["ffn"], c["k"], c["G"], c["bits"], c["tau"][0]

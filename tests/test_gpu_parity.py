@@ -228,6 +228,34 @@ def test_forward_split_reduction(mc, d, T):
     assert mae < 2e-4, mae
 
 
+@pytest.mark.parametrize("cid,E,d,ffn,T,hot", [
+    (1, 4, 256, 512, 300, None),      # G = 32, ragged 32-row fragments
+    (1, 4, 384, 256, 257, None),      # d not a multiple of the 256-row down tile
+    (1, 4, 256, 512, 600, 1),         # one expert takes every token: 600 + ~rest, 3 m-tiles
+    (4, 16, 2048, 1024, 300, None),   # G = 64, 16 experts, top-8, ragged experts
+])
+def test_forward_prefill_shapes(mc, cid, E, d, ffn, T, hot):
+    """Batches above 64 tokens go through the grouped GEMMs: partial 256-token
+    tiles (2, 4, 6, 8 fragment rows), experts with no token, G = 32/64/128."""
+    c = synthetic.config(cid)
+    k = c["k"]
+    mats, bits, G, logical = layer_case(cid, E=E, d=d, ffn=ffn)
+    L = pack_gpu(mc, mats, bits, G)
+    x = synthetic.activations(cid, T, d=d)
+    lg = synthetic.logits(cid, T)[:, :E].copy()
+    if hot is not None:
+        lg[:, hot] += 30.0
+    imp = synthetic.important_mask(cid, T)
+    tau = c["tau"][0]
+    if k > 2:
+        assert_margin(lg, imp, k, tau)
+    y, r = forward_gpu(mc, L, x, lg, imp, k, tau)
+    ref = oracle.route(lg, imp, k, tau)
+    y_ref = oracle.moe_forward(x, ref, logical, G)
+    mae, maxrel = check_tol(y, y_ref)
+    print("prefill cid=%d E=%d d=%d ffn=%d T=%d MAE %.3e MaxRel %.3e" % (cid, E, d, ffn, T, mae, maxrel))
+
+
 def test_forward_skewed_and_dense(mc, tiny):
     """All tokens on one expert (full token chunks), then tau = 0 with every
     token protected (dense top-k)."""
