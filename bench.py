@@ -149,7 +149,7 @@ def kernel_times(mc, torch, wl, steps):
         wl.step(mc, i)
     torch.cuda.synchronize()
     out = {}
-    for name in ("route_fused", "route_select", "route_lists", "gateup", "down", "combine"):
+    for name in ("route_fused", "route_select", "route_lists", "prefill_prep", "gateup", "down", "combine"):
         ms, n = mc.timing_read(name)
         if n:
             out[name] = dict(avg_us=1e3 * ms / n, launches=n)

@@ -49,8 +49,8 @@ __global__ void __launch_bounds__(256) prefill_setup_kernel(const int32_t* __res
 
 // One workgroup per fragment row f: its 32 routed rows of x (zero past the
 // expert's count) copied into the fragment layout (bf16, unchanged), and the
-// sums of every 32 columns of each row in fp32 (fixed order).
-__global__ void __launch_bounds__(256) prefill_gather_kernel(const uint16_t* __restrict__ x, int d, int E,
+// sum of each group of G columns of each row in fp32 (in column order).
+__global__ void __launch_bounds__(256) prefill_gather_kernel(const uint16_t* __restrict__ x, int d, int G, int E,
                                                              const int32_t* __restrict__ offsets,
                                                              const int32_t* __restrict__ pair_token,
                                                              PrefillTables tb, uint16_t* __restrict__ xt,
@@ -60,26 +60,25 @@ __global__ void __launch_bounds__(256) prefill_gather_kernel(const uint16_t* __r
   const int e = tb.ftile_e[f];
   const int pos0 = offsets[e] + (f - tb.ftile_base[e]) * kPfFragRows;
   const int pend = offsets[e + 1];
-  const int parts = d / 32;
+  const int ng = d / G;
   unsigned char* out = reinterpret_cast<unsigned char*>(xt);
-  for (int idx = threadIdx.x; idx < kPfFragRows * parts; idx += blockDim.x) {
-    const int m = idx / parts, p = idx - m * parts;
+  for (int idx = threadIdx.x; idx < kPfFragRows * ng; idx += blockDim.x) {
+    const int m = idx % kPfFragRows, gi = idx / kPfFragRows;
     const int pos = pos0 + m;
-    u32x4 v[4] = {{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}};
+    const bool valid = pos < pend;
+    const u32x4* src = valid ? reinterpret_cast<const u32x4*>(x + (size_t)pair_token[pos] * d + G * gi) : nullptr;
     float sum = 0.0f;
-    if (pos < pend) {
-      const u32x4* src = reinterpret_cast<const u32x4*>(x + (size_t)pair_token[pos] * d + 32 * p);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = src[q];
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
+    for (int q = 0; q < G / 8; ++q) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (valid) {
+        v = src[q];
 #pragma unroll
         for (int w = 0; w < 4; ++w)
-          sum += bf16_bits_to_float(v[q][w] & 0xffffu) + bf16_bits_to_float(v[q][w] >> 16);
+          sum += bf16_bits_to_float(v[w] & 0xffffu) + bf16_bits_to_float(v[w] >> 16);
+      }
+      *reinterpret_cast<u32x4*>(out + frag_offset(f, m, G * gi + 8 * q, d)) = v;
     }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) *reinterpret_cast<u32x4*>(out + frag_offset(f, m, 32 * p + 8 * q, d)) = v[q];
-    xsum[((size_t)f * 32 + m) * parts + p] = sum;
+    xsum[((size_t)f * ng + gi) * 32 + m] = sum;
   }
 }
 
@@ -98,12 +97,13 @@ PrefillLayout prefill_layout(int T, int E, int k, int d, int ffn) {
   if (s > maxs) s = maxs;
   if (s < 1) s = 1;
   pl.nsplit = s;
-  const size_t rows = (size_t)pl.f_max * kPfFragRows;
+  // the GEMMs stage whole m-tiles: kTiles - 1 padding fragment rows past the last one
+  const size_t rows = (size_t)(pl.f_max + PfCfg::kTiles) * kPfFragRows;
   pl.tables = 0;
   const size_t tab = (size_t)(E + 1 + pl.f_max + 2 * pl.mt_max + 1) * sizeof(int32_t);
   pl.x = round256(tab);
   pl.xsum = pl.x + round256(rows * d * sizeof(uint16_t));
-  pl.h = pl.xsum + round256(rows * (d / 32) * sizeof(float));
+  pl.h = pl.xsum + round256(rows * (d / 32) * sizeof(float));   // G >= 32
   pl.hsum = pl.h + round256(rows * ffn * sizeof(uint16_t));
   pl.part = pl.hsum + round256(rows * (ffn / 32) * sizeof(float));
   pl.total = pl.part + (size_t)pl.nsplit * P * d * sizeof(float);
@@ -133,7 +133,7 @@ hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routin
 
   timing_begin(stream, kSitePrefillPrep);
   hipLaunchKernelGGL(prefill_setup_kernel, dim3(1), dim3(256), 0, stream, r.counts, r.E, tb);
-  hipLaunchKernelGGL(prefill_gather_kernel, dim3(pl.f_max), dim3(256), 0, stream, x, L.d, r.E,
+  hipLaunchKernelGGL(prefill_gather_kernel, dim3(pl.f_max), dim3(256), 0, stream, x, L.d, L.G, r.E,
                      r.offsets, r.pair_token, tb, xt, xsum);
   timing_end(stream, kSitePrefillPrep);
   hipError_t err = hipGetLastError();

@@ -43,7 +43,8 @@ constexpr int kPfFragRows = 32;                    // rows of a fragment (MFMA M
 constexpr int kPfFragBytes = 1024;                 // 32 rows x 16 16-bit values
 constexpr int kPfWaves = 8;
 constexpr int kPfWaveTiles = 2;                    // fragment rows per wave (64 tokens)
-constexpr int kPfWtok = 4;                         // token groups per workgroup
+constexpr int kPfWtok = 2;                         // token groups per workgroup
+constexpr int kPfSlots = 4;                        // LDS ring: chunks c-1 .. c+2
 constexpr uint32_t kMagicF16 = 0x64006400u;        // fp16 1024.0 in both halves
 
 template <int WTOK>
@@ -52,13 +53,17 @@ struct PfShape {
   static constexpr int kTiles = WTOK * kPfWaveTiles;             // fragment rows per workgroup
   static constexpr int kTokens = kTiles * kPfFragRows;           // tokens per m-tile
   static constexpr int kFragBytes = kTiles * 8 * kPfFragBytes;   // A fragments of one chunk
-  static constexpr int kSBytes = kTiles * kPfFragRows * 4 * 4;   // group sums, <= 4 groups
-  static constexpr int kStageBytes = kFragBytes + kSBytes;
-  static constexpr int kLdsBytes = 2 * kStageBytes;
+  static constexpr int kSumBytes = 2048;                         // group sums: kTiles x <= 4 groups x 32 rows
+  static constexpr int kStageBytes = kFragBytes + kSumBytes;
+  static constexpr int kLdsBytes = kPfSlots * kStageBytes;
   static constexpr int kRowsGateUp = kWrow * 32;                 // ffn rows per gate/up workgroup
   static constexpr int kRowsDown = kWrow * 64;                   // d rows per down workgroup
+  // every wave issues the same number of staging loads per chunk (counted waits)
+  static constexpr int kFragLoadsPerWave = kTiles * 8 / kPfWaves;
+  static_assert(kTiles * 8 % kPfWaves == 0, "fragments spread evenly over the waves");
+  static_assert(kTiles * 4 * 32 * 4 <= kSumBytes, "group sums of a chunk");
   static_assert(kLdsBytes <= kLdsPerCu, "prefill stages fit the LDS of a CU");
-  static_assert(kTokens <= kPfWaves * 64, "one staging thread per token row");
+  static_assert(kRowsGateUp == 128, "a gate/up workgroup covers whole groups of h columns");
 };
 using PfCfg = PfShape<kPfWtok>;
 
@@ -74,13 +79,13 @@ struct PrefillTables {
 
 struct PrefillGemm {
   const uint16_t* a;     // fragment-tiled operand, K columns (bf16 x or fp16 h)
-  const float* asum;     // [fragment row][32][K/32] sums of the operand over 32 columns
+  const float* asum;     // [fragment row][K/G][32] sums of the operand over each group
   int K;                 // reduction length: d (gate/up) or ffn (down)
   int n_tiles;           // workgroup row tiles of the weight matrix
   int c_per_split;       // 128-column chunks per split of the reduction
   int nsplit;
   uint16_t* h;           // gate/up output: fragment-tiled fp16 h [.][ffn]
-  float* hsum;           // gate/up output: [fragment row][32][ffn/32] sums of the rounded h
+  float* hsum;           // gate/up output: [fragment row][ffn/G][32] group sums of the rounded h
   float* partial;        // down output: [nsplit][P][d] fp32
   size_t part_stride;
 };
@@ -145,136 +150,172 @@ __device__ __forceinline__ f32x16 pf_mfma(u32x4 a, u32x4 b, f32x16 c) {
                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
-// Stage chunk c: the A fragments of the m-tile's nmt fragment rows go
-// straight to LDS; the 32-column sums of its rows are loaded (one row per
-// thread) and written as group sums by pf_store_sums once they have arrived.
-__device__ __forceinline__ void pf_stage_frags(unsigned char* stage, const PrefillGemm& g, int f0, int nmt,
-                                               int c, int wave, int lane) {
-  const int ksteps = g.K / 16;
-  for (int q = wave; q < nmt * 8; q += kPfWaves) {
-    const int mt = q >> 3, v = q & 7;
-    const unsigned char* src = reinterpret_cast<const unsigned char*>(g.a) +
-                               ((size_t)(f0 + mt) * ksteps + (size_t)c * 8 + v) * kPfFragBytes + lane * 16;
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                     (__attribute__((address_space(3))) void*)(stage + q * kPfFragBytes),
-                                     16, 0, 0);
-  }
+// s_waitcnt vmcnt(n) (expcnt and lgkmcnt left alone).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int WTOK>
-__device__ __forceinline__ f32x4 pf_load_sums(const PrefillGemm& g, int f0, int nmt, int c) {
-  using S = PfShape<WTOK>;
-  const int r = threadIdx.x;
-  f32x4 v = {0.f, 0.f, 0.f, 0.f};
-  if (r < S::kTokens && (r >> 5) < nmt)
-    v = *reinterpret_cast<const f32x4*>(g.asum + ((size_t)(f0 + (r >> 5)) * 32 + (r & 31)) * (g.K / 32) + 4 * c);
-  return v;
+__device__ __forceinline__ void lds_dma16(const void* src, unsigned char* dst) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                   (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
 }
 
-// Group sums of the chunk: S[q][row], q < GPC groups of 128/GPC columns.
+// Stage chunk c straight into LDS: the A fragments of all kTiles fragment rows
+// (rows past the m-tile's end read the padding rows of the buffer; their sums
+// are dropped) and the group sums [tile][GPC][32].  Each wave issues
+// kFragLoadsPerWave + 1 loads; the sums are split in two 1 KB halves, and
+// waves loading the same half write identical bytes.
 template <int GPC, int WTOK>
-__device__ __forceinline__ void pf_store_sums(unsigned char* stage, f32x4 p) {
+__device__ __forceinline__ void pf_stage(unsigned char* stage, const PrefillGemm& g, int f0, int c,
+                                         int wave, int lane) {
   using S = PfShape<WTOK>;
-  const int r = threadIdx.x;
-  if (r >= S::kTokens) return;
-  float* s = reinterpret_cast<float*>(stage + S::kFragBytes);
-  if constexpr (GPC == 1) {
-    s[r] = (p[0] + p[1]) + (p[2] + p[3]);
-  } else if constexpr (GPC == 2) {
-    s[r] = p[0] + p[1];
-    s[S::kTokens + r] = p[2] + p[3];
-  } else {
+  const int ksteps = g.K / 16, ng = g.K * GPC / kTileCols;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) s[q * S::kTokens + r] = p[q];
+  for (int i = 0; i < S::kFragLoadsPerWave; ++i) {
+    const int q = wave + kPfWaves * i;
+    const int mt = q >> 3, v = q & 7;
+    lds_dma16(reinterpret_cast<const unsigned char*>(g.a) +
+                  ((size_t)(f0 + mt) * ksteps + (size_t)c * 8 + v) * kPfFragBytes + lane * 16,
+              stage + q * kPfFragBytes);
+  }
+  const int half = wave & 1;
+  const int p = half * 64 + lane;                 // 16-byte piece of the sums area
+  int t = p / (GPC * 8), rest = p - t * GPC * 8;
+  if (t >= S::kTiles) { t = 0; rest = 0; }         // past the sums: any valid address
+  const int q = rest >> 3, r4 = (rest & 7) * 4;
+  lds_dma16(g.asum + ((size_t)(f0 + t) * ng + (size_t)c * GPC + q) * 32 + r4,
+            stage + S::kFragBytes + half * 1024);
+}
+
+// Group epilogue: tot += s * (acc - (magic + z) * S_g); per lane its row's
+// s and z (word sw of each stream), S_g of the tile rows from the stage.
+template <int GPC, bool BF16, int WTOK>
+__device__ __forceinline__ void pf_epilogue(const f32x16 (&acc)[kPfWaveTiles][2], const uint32_t (&sw)[2],
+                                            const unsigned char* stage, int q, int tg, int lane,
+                                            f32x16 (&tot)[kPfWaveTiles][2]) {
+  using S = PfShape<WTOK>;
+  const float mval = BF16 ? 128.0f : 1024.0f;
+  const float* ssum = reinterpret_cast<const float*>(stage + S::kFragBytes);
+  float sj[2], cj[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    sj[j] = half_bits_to_float(sw[j] & 0xffffu);
+    cj[j] = mval + half_bits_to_float(sw[j] >> 16);
+  }
+#pragma unroll
+  for (int t = 0; t < kPfWaveTiles; ++t) {
+    const float* sr = ssum + ((2 * tg + t) * GPC + q) * 32 + 4 * (lane >> 5);
+    f32x4 sx[4];
+#pragma unroll
+    for (int k4 = 0; k4 < 4; ++k4) sx[k4] = *reinterpret_cast<const f32x4*>(sr + 8 * k4);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float u = fmaf(-cj[j], sx[i >> 2][i & 3], acc[t][j][i]);
+        tot[t][j][i] = fmaf(sj[j], u, tot[t][j][i]);
+      }
   }
 }
 
-template <int BITS, int GPC, bool BF16, int WTOK>
-__device__ __forceinline__ void pf_loop(const PfStream (&sp)[2], const PrefillGemm& g, int f0, int nmt,
-                                        int tg, bool active, int c_begin, int c_end,
-                                        unsigned char* smem, int wave, int lane,
-                                        f32x16 (&tot)[kPfWaveTiles][2]) {
-  using S = PfShape<WTOK>;
-  constexpr uint32_t magic = BF16 ? kMagic2 : kMagicF16;
-  const float mval = BF16 ? 128.0f : 1024.0f;
+// MFMAs of group q of the chunk in `stage` with the words `w`.
+template <int BITS, int GPC, bool BF16>
+__device__ __forceinline__ void pf_group(const unsigned char* stage, const uint32_t (&w)[2][2][BITS], int q,
+                                         int tg, int lane, uint32_t magic, f32x16 (&acc)[kPfWaveTiles][2]) {
   constexpr int KV = 8 / GPC;   // MFMA steps per group
-  uint32_t w[2][2][BITS], s[2][GPC];
-  f32x4 part = {0.f, 0.f, 0.f, 0.f};
-  if (c_begin < c_end) {
-    pf_stage_frags(smem, g, f0, nmt, c_begin, wave, lane);
-    pf_store_sums<GPC, WTOK>(smem, pf_load_sums<WTOK>(g, f0, nmt, c_begin));
+  const unsigned char* arow = stage + (2 * tg * 8) * kPfFragBytes + lane * 16;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) pf_load<BITS, GPC>(w[j], s[j], sp[j], c_begin);
+  for (int vv = 0; vv < KV; ++vv) {
+    const int v = q * KV + vv;
+    u32x4 a[kPfWaveTiles];
+#pragma unroll
+    for (int t = 0; t < kPfWaveTiles; ++t) a[t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + v) * kPfFragBytes);
+    const u32x4 b0 = pf_codes<BITS>(w[0][v & 1], v >> 1, magic);
+    const u32x4 b1 = pf_codes<BITS>(w[1][v & 1], v >> 1, magic);
+#pragma unroll
+    for (int t = 0; t < kPfWaveTiles; ++t) {
+      const f32x16 z = {};
+      acc[t][0] = pf_mfma<BF16>(a[t], b0, vv == 0 ? z : acc[t][0]);
+      acc[t][1] = pf_mfma<BF16>(a[t], b1, vv == 0 ? z : acc[t][1]);
+    }
   }
-  for (int c = c_begin; c < c_end; ++c) {
-    unsigned char* cur = smem + ((c - c_begin) & 1) * S::kStageBytes;
-    unsigned char* nxt = smem + (((c - c_begin) & 1) ^ 1) * S::kStageBytes;
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this chunk's fragments have landed
-    __syncthreads();
-    uint32_t wc[2][2][BITS], sc[2][GPC];
+}
+
+// One chunk.  Wait for its stage, issue the words of chunk c+1 into `nw`/`ns`
+// and stage c+2 (chunk indices clamped to the last one, so that every wave has
+// the same loads in flight everywhere: at the top of a chunk only stage c+1
+// may still be outstanding behind the words of c), then the MFMAs and group
+// epilogues.  The two waves of a SIMD run half a phase apart: a "late" wave
+// does the epilogue of the previous chunk's last group first (its acc, its
+// scale words `ps` and its stage, kept by the fourth LDS slot) and defers its
+// own last group's epilogue, so that one wave's epilogue overlaps the other's
+// MFMAs.
+template <int BITS, int GPC, bool BF16, int WTOK>
+__device__ __forceinline__ void pf_chunk(const PfStream (&sp)[2], const PrefillGemm& g, int f0, int tg,
+                                         bool active, bool late, bool first, int c, int last, int slot,
+                                         unsigned char* smem, int wave, int lane,
+                                         const uint32_t (&w)[2][2][BITS], const uint32_t (&s)[2][GPC],
+                                         uint32_t (&nw)[2][2][BITS], uint32_t (&ns)[2][GPC],
+                                         uint32_t (&ps)[2], uint32_t magic, f32x16 (&acc)[kPfWaveTiles][2],
+                                         f32x16 (&tot)[kPfWaveTiles][2]) {
+  using S = PfShape<WTOK>;
+  // Stage c has landed in LDS once at most the loads issued after it (stage
+  // c+1) are outstanding; the plain barrier then publishes it (a fenced
+  // __syncthreads would also wait for stage c+1, which is still in flight).
+  wait_vmcnt<S::kFragLoadsPerWave + 1>();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  const int slotp = slot == 0 ? kPfSlots - 1 : slot - 1;
+  const int slot2 = slot + 2 >= kPfSlots ? slot + 2 - kPfSlots : slot + 2;
+  const unsigned char* cur = smem + slot * S::kStageBytes;
+  if (active && late && !first) pf_epilogue<GPC, BF16, WTOK>(acc, ps, smem + slotp * S::kStageBytes, GPC - 1, tg, lane, tot);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < 2; ++j) pf_load<BITS, GPC>(nw[j], ns[j], sp[j], c + 1 < last ? c + 1 : last);
+  pf_stage<GPC, WTOK>(smem + slot2 * S::kStageBytes, g, f0, c + 2 < last ? c + 2 : last, wave, lane);
+  if (!active) return;
 #pragma unroll
-      for (int p = 0; p < 2; ++p)
-#pragma unroll
-        for (int b = 0; b < BITS; ++b) wc[j][p][b] = w[j][p][b];
-#pragma unroll
-      for (int q = 0; q < GPC; ++q) sc[j][q] = s[j][q];
-    }
-    const bool more = c + 1 < c_end;
-    if (more) {
-      pf_stage_frags(nxt, g, f0, nmt, c + 1, wave, lane);
-      part = pf_load_sums<WTOK>(g, f0, nmt, c + 1);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) pf_load<BITS, GPC>(w[j], s[j], sp[j], c + 1);
-    }
-    if (active) {
-      const unsigned char* arow = cur + (2 * tg * 8) * kPfFragBytes + lane * 16;
-      const float* ssum = reinterpret_cast<const float*>(cur + S::kFragBytes);
-#pragma unroll
-      for (int q = 0; q < GPC; ++q) {
-        f32x16 acc[kPfWaveTiles][2];
-#pragma unroll
-        for (int vv = 0; vv < KV; ++vv) {
-          const int v = q * KV + vv;
-          u32x4 a[kPfWaveTiles];
-#pragma unroll
-          for (int t = 0; t < kPfWaveTiles; ++t)
-            a[t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + v) * kPfFragBytes);
-          const u32x4 b0 = pf_codes<BITS>(wc[0][v & 1], v >> 1, magic);
-          const u32x4 b1 = pf_codes<BITS>(wc[1][v & 1], v >> 1, magic);
-#pragma unroll
-          for (int t = 0; t < kPfWaveTiles; ++t) {
-            const f32x16 z = {};
-            acc[t][0] = pf_mfma<BF16>(a[t], b0, vv == 0 ? z : acc[t][0]);
-            acc[t][1] = pf_mfma<BF16>(a[t], b1, vv == 0 ? z : acc[t][1]);
-          }
-        }
-        // tot += s * (acc - (magic + z) * S_g), per lane: its row's s and z
-        float sj[2], cj[2];
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          sj[j] = half_bits_to_float(sc[j][q] & 0xffffu);
-          cj[j] = mval + half_bits_to_float(sc[j][q] >> 16);
-        }
-#pragma unroll
-        for (int t = 0; t < kPfWaveTiles; ++t) {
-          const float* sr = ssum + q * S::kTokens + (2 * tg + t) * 32 + 4 * (lane >> 5);
-          f32x4 sx[4];
-#pragma unroll
-          for (int k4 = 0; k4 < 4; ++k4) sx[k4] = *reinterpret_cast<const f32x4*>(sr + 8 * k4);
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-              const float u = fmaf(-cj[j], sx[i >> 2][i & 3], acc[t][j][i]);
-              tot[t][j][i] = fmaf(sj[j], u, tot[t][j][i]);
-            }
-        }
-      }
-    }
-    if (more) pf_store_sums<GPC, WTOK>(nxt, part);
+  for (int q = 0; q < GPC; ++q) {
+    pf_group<BITS, GPC, BF16>(cur, w, q, tg, lane, magic, acc);
+    uint32_t sw[2] = {s[0][q], s[1][q]};
+    if (q < GPC - 1 || !late) pf_epilogue<GPC, BF16, WTOK>(acc, sw, cur, q, tg, lane, tot);
+    else { ps[0] = sw[0]; ps[1] = sw[1]; }
   }
+}
+
+// Chunks [c_begin, c_end) of the reduction, two per iteration so that the
+// two register sets of weight words alternate without copies.
+template <int BITS, int GPC, bool BF16, int WTOK>
+__device__ __forceinline__ void pf_loop(const PfStream (&sp)[2], const PrefillGemm& g, int f0, int tg,
+                                        bool active, bool late, int c_begin, int c_end, unsigned char* smem,
+                                        int wave, int lane, f32x16 (&tot)[kPfWaveTiles][2]) {
+  using S = PfShape<WTOK>;
+  if (c_begin >= c_end) return;
+  const uint32_t magic = vgpr_constant(BF16 ? kMagic2 : kMagicF16);
+  const int last = c_end - 1;
+  uint32_t wa[2][2][BITS], sa[2][GPC], wb[2][2][BITS], sb[2][GPC], ps[2] = {0u, 0u};
+  f32x16 acc[kPfWaveTiles][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) pf_load<BITS, GPC>(wa[j], sa[j], sp[j], c_begin);
+  pf_stage<GPC, WTOK>(smem, g, f0, c_begin, wave, lane);
+  pf_stage<GPC, WTOK>(smem + S::kStageBytes, g, f0, c_begin + 1 < last ? c_begin + 1 : last, wave, lane);
+  int slot = 0;
+  for (int c = c_begin; c < c_end; c += 2) {
+    pf_chunk<BITS, GPC, BF16, WTOK>(sp, g, f0, tg, active, late, c == c_begin, c, last, slot, smem, wave, lane,
+                                    wa, sa, wb, sb, ps, magic, acc, tot);
+    slot = slot + 1 == kPfSlots ? 0 : slot + 1;
+    if (c + 1 < c_end)
+      pf_chunk<BITS, GPC, BF16, WTOK>(sp, g, f0, tg, active, late, false, c + 1, last, slot, smem, wave, lane,
+                                      wb, sb, wa, sa, ps, magic, acc, tot);
+    slot = slot + 1 == kPfSlots ? 0 : slot + 1;
+  }
+  // the late waves' last epilogue: the last chunk's stage is the slot before `slot`
+  if (active && late)
+    pf_epilogue<GPC, BF16, WTOK>(acc, ps, smem + (slot == 0 ? kPfSlots - 1 : slot - 1) * S::kStageBytes,
+                                 GPC - 1, tg, lane, tot);
+  wait_vmcnt<0>();   // the clamped re-reads of the last chunks land before LDS is reused
 }
 
 // Grid: mt_max * n_tiles * nsplit workgroups (m-tile major); workgroups past
@@ -295,7 +336,8 @@ prefill_kernel(LayerArgs L, const int32_t* __restrict__ offsets, PrefillTables t
   const int nmt = nf < S::kTiles ? nf : S::kTiles;
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int tg = wave / S::kWrow, rg = wave - tg * S::kWrow;
-  const bool active = 2 * tg < nmt;
+  const bool active = 2 * tg < nmt;   // wave-uniform; idle waves still stage and synchronise
+  const bool late = wave >= kPfWaves / 2;   // shares a SIMD with wave - 4: runs half a phase later
   const int ntiles = g.K / kTileCols;
   const int c_begin = split * g.c_per_split;
   const int c_end = (c_begin + g.c_per_split) < ntiles ? (c_begin + g.c_per_split) : ntiles;
@@ -325,37 +367,52 @@ prefill_kernel(LayerArgs L, const int32_t* __restrict__ offsets, PrefillTables t
       for (int i = 0; i < 16; ++i) tot[t][s][i] = 0.0f;
 
   if (bits == 1)
-    pf_loop<1, GPC, GATEUP, kPfWtok>(sp, g, f0, nmt, tg, active, c_begin, c_end, smem, wave, lane, tot);
+    pf_loop<1, GPC, GATEUP, kPfWtok>(sp, g, f0, tg, active, late, c_begin, c_end, smem, wave, lane, tot);
   else if (bits == 2)
-    pf_loop<2, GPC, GATEUP, kPfWtok>(sp, g, f0, nmt, tg, active, c_begin, c_end, smem, wave, lane, tot);
+    pf_loop<2, GPC, GATEUP, kPfWtok>(sp, g, f0, tg, active, late, c_begin, c_end, smem, wave, lane, tot);
   else
-    pf_loop<3, GPC, GATEUP, kPfWtok>(sp, g, f0, nmt, tg, active, c_begin, c_end, smem, wave, lane, tot);
-  if (!active) return;
+    pf_loop<3, GPC, GATEUP, kPfWtok>(sp, g, f0, tg, active, late, c_begin, c_end, smem, wave, lane, tot);
 
   // D layout: lane holds column n = lane%32 (weight row) and, for i < 16,
   // row m = 8*(i/4) + 4*(lane/32) + i%4 (token) of each 32x32 tile.
   const int n = lane & 31;
   if (GATEUP) {
+    // h = silu(gate) * up rounded to fp16; then the group sums of the rounded
+    // h: per wave over its 32 columns (butterfly in a fixed order), then over
+    // the workgroup's 128 columns in LDS (row groups in order).
     const int col = row[0] + n;
     unsigned char* hb = reinterpret_cast<unsigned char*>(g.h);
+    __syncthreads();                       // the ring is free: reuse it for the partial sums
+    float* part = reinterpret_cast<float*>(smem);   // [tg][rg][64 rows]
 #pragma unroll
     for (int t = 0; t < kPfWaveTiles; ++t) {
       const int f = f0 + 2 * tg + t;
-      if (2 * tg + t < nmt) {
+      if (active && 2 * tg + t < nmt) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int m = 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
           const uint16_t h16 = float_to_half_sat(silu(tot[t][0][i]) * tot[t][1][i]);
           *reinterpret_cast<uint16_t*>(hb + frag_offset(f, m, col, L.ffn)) = h16;
-          // sum of the rounded h over this wave's 32 columns (the lanes of one half), fixed order
           float v = half_bits_to_float(h16);
 #pragma unroll
           for (int off = 1; off < 32; off <<= 1) v += __shfl_xor(v, off);
-          if (n == 0) g.hsum[((size_t)f * 32 + m) * (L.ffn / 32) + row[0] / 32] = v;
+          if (n == 0) part[(tg * S::kWrow + rg) * 64 + t * 32 + m] = v;
         }
       }
     }
+    __syncthreads();
+    const int gpw = L.G / 32;                       // row groups (32 columns each) per group
+    const int ngw = S::kRowsGateUp / L.G;           // groups in this workgroup
+    for (int idx = threadIdx.x; idx < kPfWtok * 64 * ngw; idx += blockDim.x) {
+      const int q = idx % ngw, r = (idx / ngw) % 64, tg2 = idx / (ngw * 64);
+      if (2 * tg2 + r / 32 >= nmt) continue;
+      float v = 0.0f;
+      for (int k = 0; k < gpw; ++k) v += part[(tg2 * S::kWrow + q * gpw + k) * 64 + r];
+      const int f = f0 + 2 * tg2 + r / 32;
+      g.hsum[((size_t)f * (L.ffn / L.G) + (nt * S::kRowsGateUp) / L.G + q) * 32 + (r & 31)] = v;
+    }
   } else {
+    if (!active) return;
     const int pbase = offsets[e] + S::kTokens * j;
     const int pend = offsets[e + 1];
     float* out = g.partial + (size_t)split * g.part_stride;
