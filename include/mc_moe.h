@@ -56,6 +56,7 @@ extern "C" {
 
 #define MC_MAX_EXPERTS 256
 #define MC_MAX_TOPK 8
+#define MC_MAX_TOKENS 65536   /* tokens per routing call (MC_EUNSUPPORTED above) */
 
 typedef enum mc_status {
   MC_OK = 0,

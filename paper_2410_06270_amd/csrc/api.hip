@@ -80,8 +80,7 @@ mc_status check_routing(const mc_routing* r) {
   if (r->E < 1 || r->E > MC_MAX_EXPERTS) return fail(MC_EINVAL, "E=%d outside [1, %d]", r->E, MC_MAX_EXPERTS);
   if (r->k < 1 || r->k > r->E || r->k > MC_MAX_TOPK)
     return fail(MC_EINVAL, "k=%d outside [1, min(E=%d, %d)]", r->k, r->E, MC_MAX_TOPK);
-  if ((long long)r->T * r->k >= (1LL << 31) || (long long)r->T * r->E >= (1LL << 31))
-    return fail(MC_EUNSUPPORTED, "T=%d too large", r->T);
+  if (r->T > MC_MAX_TOKENS) return fail(MC_EUNSUPPORTED, "T=%d above %d", r->T, MC_MAX_TOKENS);
   if (!r->topk_idx || !r->topk_w || !r->kept || !r->counts || !r->offsets || !r->pair_token ||
       !r->pair_rank || !r->pair_w || !r->pair_pos || !r->n_pruned)
     return fail(MC_EINVAL, "a routing output pointer is NULL");
@@ -165,6 +164,7 @@ mc_status mc_forward_workspace(int T, int E, int k, int d, int ffn, size_t* byte
   if (T < 1 || E < 1 || E > MC_MAX_EXPERTS || k < 1 || k > E || k > MC_MAX_TOPK || d <= 0 ||
       ffn <= 0 || d % 128 || ffn % 128)
     return fail(MC_EINVAL, "bad shape T=%d E=%d k=%d d=%d ffn=%d", T, E, k, d, ffn);
+  if (T > MC_MAX_TOKENS) return fail(MC_EUNSUPPORTED, "T=%d above %d", T, MC_MAX_TOKENS);
   if (!bytes) return fail(MC_EINVAL, "bytes pointer is NULL");
   *bytes = mc::forward_workspace_bytes(T, E, k, d, ffn);
   return MC_OK;

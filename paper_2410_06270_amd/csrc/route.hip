@@ -10,15 +10,20 @@
 //
 // Selection (one wavefront per token): lanes hold the logits, k rounds of a
 // 64-bit max-reduction pick the experts, lane r then evaluates rank r.
-// Lists (one workgroup): per-expert token lists in ascending token order,
-// built with ballots and popcount prefixes (no atomics, so deterministic).
-// Small batches run both phases in one launch with everything kept in LDS.
+// Lists: per-expert token lists in ascending token order, built with ballots
+// and popcount prefixes (list positions never depend on timing, so the lists
+// are deterministic).  Small batches run both phases in one launch with
+// everything kept in LDS; larger ones scatter by token blocks, each block
+// counting the selections of all tokens (expert totals) and of the tokens
+// before it (its start in each list).
 #include "mc_internal.hpp"
 
 namespace mc {
 
 constexpr int kCsrThreads = 1024;
-constexpr int kCsrChunk = 2048;     // tokens staged in LDS per pass (k <= 8 -> 32 KB)
+constexpr int kListBlocks = 64;     // at most this many token blocks scatter the lists
+constexpr int kListMaxBlockT = 1024;
+static_assert(kListBlocks * kListMaxBlockT >= MC_MAX_TOKENS, "list blocks cover every token");
 
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v) {
   for (int off = 32; off >= 1; off >>= 1) {
@@ -112,11 +117,11 @@ __device__ void select_token(const float* __restrict__ logits, const uint8_t* __
   }
 }
 
-// Exclusive scan of cnt[0..E) into base[] and the global counts/offsets
-// (one wave: each lane owns 4 consecutive experts).
-__device__ void scan_counts(int T, int E, int k, const int* cnt, int* base,
-                            int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
-                            int32_t* __restrict__ n_pruned) {
+// Exclusive scan of cnt[0..E) into base[] and offsets[0..E] (one wave: each
+// lane owns 4 consecutive experts); with `publish`, also the global counts
+// and the number of pruned pairs.
+__device__ void scan_counts(int T, int E, int k, const int* cnt, int* base, int32_t* counts, int32_t* offsets,
+                            int32_t* n_pruned, bool publish = true) {
   const int lane = threadIdx.x & 63;
   int c[4], local = 0;
 #pragma unroll
@@ -137,13 +142,13 @@ __device__ void scan_counts(int T, int E, int k, const int* cnt, int* base,
     if (e < E) {
       base[e] = run;
       offsets[e] = run;
-      counts[e] = c[j];
+      if (publish) counts[e] = c[j];
     }
     run += c[j];
   }
   if (lane == 63) {
     offsets[E] = incl;
-    *n_pruned = T * k - incl;
+    if (publish) *n_pruned = T * k - incl;
   }
 }
 
@@ -188,40 +193,49 @@ __global__ void __launch_bounds__(256) route_select_kernel(const float* __restri
                nullptr, nullptr);
 }
 
-// Lists for any T (one workgroup), reading the selection from global memory
-// in chunks of kCsrChunk tokens.
-__global__ void __launch_bounds__(kCsrThreads) route_lists_kernel(
-    int T, int E, int k, const int32_t* __restrict__ topk_idx, const uint8_t* __restrict__ kept,
+// Tokens per list block: a multiple of 64, at most kListBlocks blocks.
+static int list_block_tokens(int T) {
+  int bt = (T + kListBlocks - 1) / kListBlocks;
+  bt = ((bt + 63) / 64) * 64;
+  return bt < 64 ? 64 : bt;
+}
+
+// Lists for any T: workgroup b takes tokens [b*BT, (b+1)*BT).  Its histograms
+// (LDS atomics; the counts, not their order, depend on them) give every
+// expert's total and its entries before the block; block 0 publishes the
+// counts and offsets.  The block's entries then go out in token order.
+__global__ void __launch_bounds__(kCsrThreads) route_scatter_kernel(
+    int T, int E, int k, int BT, const int32_t* __restrict__ topk_idx, const uint8_t* __restrict__ kept,
     const float* __restrict__ topk_w, int32_t* counts, int32_t* offsets, int32_t* pair_token,
     int32_t* pair_rank, float* pair_w, int32_t* pair_pos, int32_t* n_pruned) {
-  __shared__ uint16_t ent[kCsrChunk * MC_MAX_TOPK];
-  __shared__ int cnt[MC_MAX_EXPERTS];
-  __shared__ int base[MC_MAX_EXPERTS];
+  __shared__ uint16_t ent[kListMaxBlockT * MC_MAX_TOPK];
+  __shared__ int tot[MC_MAX_EXPERTS], pre[MC_MAX_EXPERTS], base[MC_MAX_EXPERTS];
+  __shared__ int32_t offs[MC_MAX_EXPERTS + 1];
   const int tid = threadIdx.x, wave = wave_id(), nwaves = blockDim.x >> 6;
-  for (int e = tid; e < E; e += blockDim.x) cnt[e] = 0;
-  for (int pass = 0; pass < 2; ++pass) {
-    if (pass == 1) {
-      __syncthreads();
-      if (wave == 0) scan_counts(T, E, k, cnt, base, counts, offsets, n_pruned);
-    }
-    for (int c0 = 0; c0 < T; c0 += kCsrChunk) {
-      const int nc = (T - c0) < kCsrChunk ? (T - c0) : kCsrChunk;
-      __syncthreads();
-      for (int i = tid; i < nc * k; i += blockDim.x) {
-        const size_t o = (size_t)c0 * k + i;
-        ent[i] = kept[o] ? (uint16_t)topk_idx[o] : (uint16_t)0xffff;
-      }
-      __syncthreads();
-      for (int e = wave; e < E; e += nwaves) {
-        const int run = list_pass(pass, e, pass == 0 ? 0 : base[e], c0, nc, k, ent, nullptr, false,
-                                  topk_w, pair_token, pair_rank, pair_w, pair_pos);
-        if ((threadIdx.x & 63) == 0) {
-          if (pass == 0) cnt[e] += run;
-          else base[e] = run;
-        }
-      }
+  const int t0 = blockIdx.x * BT;
+  const int nc = (T - t0) < BT ? (T - t0) : BT;
+  for (int e = tid; e < E; e += blockDim.x) tot[e] = pre[e] = 0;
+  __syncthreads();
+  const int n = T * k, n0 = t0 * k;
+  for (int i = tid; i < n; i += blockDim.x) {
+    if (kept[i]) {
+      const int e = topk_idx[i];
+      atomicAdd(&tot[e], 1);
+      if (i < n0) atomicAdd(&pre[e], 1);
     }
   }
+  for (int i = tid; i < nc * k; i += blockDim.x) {
+    const size_t o = (size_t)n0 + i;
+    ent[i] = kept[o] ? (uint16_t)topk_idx[o] : (uint16_t)0xffff;
+  }
+  __syncthreads();
+  if (wave == 0) scan_counts(T, E, k, tot, base, counts, offs, n_pruned, blockIdx.x == 0);
+  __syncthreads();
+  if (blockIdx.x == 0)
+    for (int e = tid; e <= E; e += blockDim.x) offsets[e] = offs[e];
+  for (int e = wave; e < E; e += nwaves)
+    list_pass(1, e, base[e] + pre[e], t0, nc, k, ent, nullptr, false, topk_w, pair_token, pair_rank,
+              pair_w, pair_pos);
 }
 
 // Small batches (T <= kRouteFusedMaxT): selection and lists in one launch, the
@@ -272,9 +286,10 @@ hipError_t launch_route(const float* logits, const uint8_t* important, float del
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   timing_begin(stream, kSiteRouteLists);
-  hipLaunchKernelGGL(route_lists_kernel, dim3(1), dim3(kCsrThreads), 0, stream, r.T, r.E, r.k,
-                     r.topk_idx, r.kept, r.topk_w, r.counts, r.offsets, r.pair_token,
-                     r.pair_rank, r.pair_w, r.pair_pos, r.n_pruned);
+  const int bt = list_block_tokens(r.T);
+  hipLaunchKernelGGL(route_scatter_kernel, dim3((r.T + bt - 1) / bt), dim3(kCsrThreads), 0, stream, r.T, r.E,
+                     r.k, bt, r.topk_idx, r.kept, r.topk_w, r.counts, r.offsets, r.pair_token, r.pair_rank,
+                     r.pair_w, r.pair_pos, r.n_pruned);
   timing_end(stream, kSiteRouteLists);
   return hipGetLastError();
 }

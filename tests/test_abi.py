@@ -95,6 +95,17 @@ def test_route_rejects(lib, T, E, k, tau):
     assert st == 1
 
 
+def test_token_limit(lib):
+    """Routing and the forward take at most MC_MAX_TOKENS tokens (MC_EUNSUPPORTED = 4)."""
+    T = 65536
+    r = _fake_routing(T + 1, 8, 2)
+    assert lib.mc_route_and_prune(ctypes.c_void_p(0x2000), None, ctypes.c_float(0.3),
+                                  ctypes.byref(r), None) == 4
+    b = ctypes.c_size_t()
+    assert lib.mc_forward_workspace(T + 1, 8, 2, 4096, 14336, ctypes.byref(b)) == 4
+    assert lib.mc_forward_workspace(T, 8, 2, 4096, 14336, ctypes.byref(b)) == 0
+
+
 def test_route_rejects_null_outputs(lib):
     from paper_2410_06270_amd._binding import _Routing
     r = _Routing(4, 8, 2, *([0x1000] * 9 + [0]))

@@ -133,6 +133,7 @@ def assert_margin(logits, imp, k, tau):
 @pytest.mark.parametrize("cid,T,tau", [
     (1, 64, 0.3), (2, 1, 0.3), (2, 8, 0.3), (2, 32, 0.3), (3, 4096, 0.0), (3, 4096, 0.2),
     (3, 4096, 0.4), (4, 2048, 0.05), (4, 16, 0.05), (4, 300, 0.05), (1, 5000, 0.3),
+    (2, 65536, 0.3),                                # the token limit: 64 list blocks of 1024
 ])
 def test_route_bit_exact(mc, cid, T, tau):
     c = synthetic.config(cid)
@@ -149,6 +150,7 @@ def test_route_edge_cases(mc):
     g = np.random.default_rng(9)
     # k = 1 (nothing to prune), k = E, E = 256, signed zeros, no mask, tau = 1
     for T, E, k, tau, imp in ((7, 4, 1, 0.3, None), (9, 8, 8, 0.1, None), (33, 256, 8, 0.02, None),
+                              (3000, 256, 8, 0.02, None), (1000, 256, 1, 0.3, None),
                               (12, 8, 2, 1.0, None), (12, 8, 2, 0.0, None), (3, 1, 1, 0.5, None)):
         lg = g.standard_normal((T, E)).astype(np.float32)
         lg[0, :] = 0.0
