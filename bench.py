@@ -1,17 +1,23 @@
 #!/usr/bin/env python3
 """Benchmark of the MC expert path on one MI355X.
 
-Workload (the paper's Mixtral 8x7b MoE layer shape, synthetic data): d=4096,
-ffn=14336, 8 experts, top-2, expert widths [3,3,3,2,2,2,2,3] (2.5 code bits,
-the paper's 2.54-bit setting), G=128, decode batch of T tokens (default 32),
-bf16 activations N(0,1), logits N(0,1) + per-expert bias N(0,0.5^2),
-prune threshold 0.3, round(0.1*T) protected tokens.
+Main workload (the paper's Mixtral 8x7b MoE layer shape, synthetic data):
+d=4096, ffn=14336, 8 experts, top-2, expert widths [3,3,3,2,2,2,2,3] (2.5 code
+bits, the paper's 2.54-bit setting), G=128, decode batch of T tokens (default
+32), bf16 activations N(0,1), logits N(0,1) + per-expert bias N(0,0.5^2),
+prune threshold 0.3, round(0.1*T) protected tokens.  Also reported in the same
+line: decode at 1 and 8 tokens, prefill of 4096 tokens with the threshold
+swept over {0, 0.2, 0.4} (pruned fraction, tokens/s, MFMA fraction of the
+algorithmic 6*d*ffn FLOPs per kept pair), and the OLMoE-shaped layer (d=2048,
+ffn=1024, 64 experts, top-8, G=64, Zipf-skewed logits, threshold 0.05) in
+decode (16 tokens) and prefill (2048 tokens).
 
 One step = route_and_prune + moe_forward over the batch for one layer.  The
-step rotates over --copies packed copies of the layer (>= 4 x 484 MB) so the
-weights come from HBM, not from the 256 MB Infinity Cache.  Prints ONE JSON
-line.  Per-kernel durations come from the library's HIP-event instrumentation
-on the launch stream, recorded over a second pass of the same timed steps.
+step rotates over packed copies of the layer (4 x 484 MB Mixtral, 3 x 131 MB
+OLMoE) so the weights come from HBM, not from the 256 MB Infinity Cache.
+Prints ONE JSON line.  Per-kernel durations come from the library's HIP-event
+instrumentation on the launch stream, recorded over a second pass of the same
+timed steps.
 """
 from __future__ import annotations
 
@@ -26,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+MFMA_PEAK_TFLOPS = 2500.0      # MI355X dense bf16/fp16 MFMA, vendor figure
 METRIC = "MoE-layer tokens/s + achieved HBM GB/s (decode) / MFMA % (prefill), 1 GPU"
 
 
@@ -38,6 +45,9 @@ def parse():
     p.add_argument("--copies", type=int, default=4)
     p.add_argument("--sweep", default="1,8", help="extra decode batch sizes to report")
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    p.add_argument("--prefill-steps", type=int, default=10)
+    p.add_argument("--no-prefill", action="store_true", help="skip the 4096-token prefill sweep")
+    p.add_argument("--no-olmoe", action="store_true", help="skip the OLMoE-shaped layer")
     p.add_argument("--graph", action="store_true",
                    help="also time HIP-graph replays of the step (reported as ms_per_step_graph)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -61,14 +71,16 @@ def expert_bytes(d, ffn, G, b, mats=(0, 1, 2)):
 
 
 class Workload:
-    def __init__(self, mc, torch, synthetic, T, copies):
-        c = synthetic.config(2)
-        self.c, self.T = c, T
+    """Packed copies of one synthetic layer (config cid) and a batch of T tokens."""
+
+    def __init__(self, mc, torch, synthetic, T, copies, cid=2):
+        c = synthetic.config(cid)
+        self.c, self.cid, self.T, self.tau = c, cid, T, c["tau"][0]
         E, d, ffn, k, G, bits = c["E"], c["d"], c["ffn"], c["k"], c["G"], c["bits"]
         self.layers = []
         for cp in range(copies):
             gen = torch.Generator(device="cuda")
-            gen.manual_seed(synthetic.BASE_SEED + 2 + 1000 * cp)
+            gen.manual_seed(synthetic.BASE_SEED + cid + 1000 * cp)
             w = [torch.randn((E, ffn, d) if m < 2 else (E, d, ffn), generator=gen, device="cuda",
                              dtype=torch.float32).mul_(0.02) for m in range(3)]
             L = mc.PackedLayer(E, d, ffn, bits, G)
@@ -79,25 +91,29 @@ class Workload:
         torch.cuda.empty_cache()
         self.set_tokens(mc, torch, synthetic, T)
 
-    def set_tokens(self, mc, torch, synthetic, T):
-        c = self.c
+    def set_tokens(self, mc, torch, synthetic, T, tau=None):
+        c, cid = self.c, self.cid
         self.T = T
+        self.tau = c["tau"][0] if tau is None else tau
         dev = lambda a: torch.from_numpy(a).cuda()
-        self.x = dev(synthetic.activations(2, T).view("int16"))
-        self.logits = dev(synthetic.logits(2, T))
-        self.imp = dev(synthetic.important_mask(2, T))
+        self.x = dev(synthetic.activations(cid, T).view("int16"))
+        self.logits = dev(synthetic.logits(cid, T))
+        self.imp = dev(synthetic.important_mask(cid, T))
         self.r = mc.Routing(T, c["E"], c["k"])
         self.y = torch.empty((T, c["d"]), dtype=torch.int16, device="cuda")
         self.ws = torch.empty(mc.forward_workspace(T, c["E"], c["k"], c["d"], c["ffn"]),
                               dtype=torch.uint8, device="cuda")
 
     def step(self, mc, i):
-        mc.route_and_prune(self.logits, self.imp, self.c["tau"][0], self.r)
+        mc.route_and_prune(self.logits, self.imp, self.tau, self.r)
         mc.moe_forward(self.x, self.r, self.layers[i % len(self.layers)], self.y, self.ws)
 
     def touched(self):
         counts = self.r.counts.cpu().tolist()
         return [e for e, n in enumerate(counts) if n > 0], int(self.r.n_pruned.cpu()[0])
+
+    def kept_pairs(self):
+        return int(self.r.offsets.cpu()[-1])
 
     def alg_bytes(self):
         c = self.c
@@ -108,6 +124,12 @@ class Workload:
         act = self.T * d * 2            # x in (gate/up) and y out (combine)
         logits = self.T * E * 4
         return dict(gateup=gateup + act, down=down, combine=act, step=gateup + down + 2 * act + logits)
+
+    def alg_flops(self):
+        """6*d*ffn per kept (token, expert) pair: gate, up (4*d*ffn) and down (2*d*ffn)."""
+        P = self.kept_pairs()
+        d, ffn = self.c["d"], self.c["ffn"]
+        return dict(gateup=4 * d * ffn * P, down=2 * d * ffn * P, step=6 * d * ffn * P)
 
 
 def time_steps(mc, torch, wl, steps, warmup, graphs=None):
@@ -212,6 +234,35 @@ def cpu_baseline(synthetic, T):
                        % (T, int(rt["counts"].sum())))
 
 
+def measure_step(mc, torch, wl, steps, warmup):
+    ms, _ = time_steps(mc, torch, wl, steps, warmup)
+    kt = kernel_times(mc, torch, wl, steps)
+    return ms, {k: v["avg_us"] for k, v in kt.items()}
+
+
+def prefill_entry(wl, ms, kus):
+    fl = wl.alg_flops()
+    P, T, k = wl.kept_pairs(), wl.T, wl.c["k"]
+    tf = lambda f, us: f / (us * 1e6)       # TFLOP/s
+    return dict(tokens=T, tau=wl.tau, pairs_kept=P, pruned_frac=round(1 - P / (T * k), 4),
+                tokens_per_s=round(T / (ms / 1e3), 1), ms_per_step=round(ms, 4),
+                step_tflops=round(tf(fl["step"], ms * 1e3), 1),
+                step_mfma_frac=round(tf(fl["step"], ms * 1e3) / MFMA_PEAK_TFLOPS, 4),
+                gateup_mfma_frac=round(tf(fl["gateup"], kus["gateup"]) / MFMA_PEAK_TFLOPS, 4),
+                down_mfma_frac=round(tf(fl["down"], kus["down"]) / MFMA_PEAK_TFLOPS, 4),
+                kernels_us={k2: round(v, 2) for k2, v in kus.items()})
+
+
+def decode_entry(wl, ms, kus):
+    ab = wl.alg_bytes()
+    touched, pruned = wl.touched()
+    return dict(tokens=wl.T, tokens_per_s=round(wl.T / (ms / 1e3), 1), ms_per_step=round(ms, 5),
+                step_hbm_gbs=round(ab["step"] / (ms * 1e6), 1),
+                gateup_hbm_frac=round(ab["gateup"] / (kus["gateup"] * 1e3) / HBM_PEAK_GBS, 4),
+                experts_touched=len(touched), pairs_pruned=pruned,
+                kernels_us={k2: round(v, 2) for k2, v in kus.items()})
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -302,6 +353,26 @@ def main():
         "sweep": sweep,
         "source_hash": hash_now,
     }
+    if not args.no_prefill:
+        pf = []
+        for tau in (0.0, 0.2, 0.4):
+            wl.set_tokens(mc, torch, synthetic, 4096, tau)
+            ms_p, kus = measure_step(mc, torch, wl, args.prefill_steps, 3)
+            pf.append(prefill_entry(wl, ms_p, kus))
+        out["prefill"] = {"workload": "mixtral_8x7b_moe_layer_prefill", "tokens": 4096,
+                          "mfma_peak_tflops": MFMA_PEAK_TFLOPS, "flops": "6*d*ffn per kept pair",
+                          "sweep": pf}
+    if not args.no_olmoe:
+        del wl
+        torch.cuda.empty_cache()
+        wo = Workload(mc, torch, synthetic, 16, 3, cid=4)
+        ms_d, kus = measure_step(mc, torch, wo, args.steps, args.warmup)
+        dec = decode_entry(wo, ms_d, kus)
+        wo.set_tokens(mc, torch, synthetic, 2048)
+        ms_p, kus = measure_step(mc, torch, wo, args.prefill_steps, 3)
+        out["olmoe"] = {"workload": "olmoe_moe_layer", "d": 2048, "ffn": 1024, "experts": 64, "top_k": 8,
+                        "group": 64, "bits": wo.c["bits"], "tau": wo.tau, "layer_copies": 3,
+                        "decode": dec, "prefill": prefill_entry(wo, ms_p, kus)}
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(synthetic, T)
     print(json.dumps(out), flush=True)
