@@ -12,11 +12,12 @@
 //
 // Kernels (all on the caller's stream, no host synchronisation; experts with
 // no kept token exit at once because the counts are read on the device):
-//   gateup_kernel  grid (ffn/64, E, chunks): 4 waves x 16 rows of gate and up,
-//                  up to 16*NTMAX tokens of one expert per chunk -> h planes;
-//   down_kernel    grid (d/128, E, chunks*S): 4 waves x 32 rows, split-K over
+//   gateup_kernel  grid (ffn/128, E, chunks x d-splits): 8 waves x 16 rows of
+//                  gate and up, up to 16*NTMAX tokens of one expert per chunk
+//                  -> h planes (or fp32 gate/up partials when d is split);
+//   down_kernel    grid (d/256, E, chunks*S): 8 waves x 32 rows, split-K over
 //                  ffn -> fp32 partials;
-//   combine_kernel grid (d/256, T): y = bf16(sum_r w_r sum_s partial), fixed
+//   combine_kernel grid (d/1024, T): y = bf16(sum_r w_r sum_s partial), fixed
 //                  order, so the result is deterministic.
 #pragma once
 
