@@ -14,7 +14,10 @@ What it computes (Mixture Compressor for MoE LLMs, ICLR 2025):
 * ``dequant_f16`` / ``dequant_exact`` -- the dequantized value s*(q - z);
 * ``route``         -- Eq. 1 top-k, Eq. 5 pruning, Sec. 3.3.2 protection and
   the per-expert token lists;
-* ``moe_forward``   -- Eq. 1 over SwiGLU experts on exact dequantized weights.
+* ``moe_forward``   -- Eq. 1 over SwiGLU experts on exact dequantized weights;
+* ``token_importance`` -- Eq. 6 importance from causal attention probabilities
+  and the protected set (the top floor(rho*L + 1/2) tokens);
+* ``median_ratio``  -- the pruning threshold mu as the median of w1/w0.
 
 Everything floating point is fp64 except operations whose precision the
 definition fixes (fp32 scale/zero arithmetic, the fp32 k = 2 logit gap).
@@ -44,6 +47,9 @@ PINS = {
     "dequant_f16": "Fraction value rounded by numpy float16 (library RNE)",
     "route": "naive stable sort; tau=0 and protected no-op; k=2 gap == ratio rule",
     "moe_forward": "E=1,k=1 equals numpy SwiGLU; tau=0 all-protected dense top-k; linearity",
+    "token_importance": "diagonal / first-token closed forms; hand example; head linearity; "
+                        "brute-force selection; upper triangle ignored",
+    "median_ratio": "statistics.median of exp(l1 - l0) over a naive sort",
 }
 
 
@@ -93,6 +99,10 @@ def _load():
         lib.orc_route.argtypes = [P, P, I, I, I, ctypes.c_double, ctypes.c_float,
                                   P, P, P, P, P, P, P, P, P, P]
         lib.orc_expert_forward.restype = I
+        lib.orc_token_importance.argtypes = [P, I, I, P, I, I, P, P]
+        lib.orc_token_importance.restype = I
+        lib.orc_median_ratio.argtypes = [P, I, I]
+        lib.orc_median_ratio.restype = ctypes.c_double
         lib.orc_expert_forward.argtypes = [P, I, I, I, I, P, P, P, P, P, P, P, P, P, P, I, P, P]
         _lib = lib
     return _lib
@@ -332,3 +342,37 @@ def moe_forward(x_bf16: np.ndarray, routing, logical, G: int, rows=None, tokens=
         for i, (t, r) in enumerate(sel):
             Y[tpos[t]] += routing["topk_w"][t, r] * Ye[i]
     return Y
+
+
+# ------------------------------------------------------------- importance ---
+
+def protect_count(L: int, rho: float) -> int:
+    """Tokens protected out of L at fraction rho: floor(rho * L + 1/2)."""
+    return int(math.floor(rho * L + 0.5))
+
+
+def token_importance(attn_bits: np.ndarray, x_bits: np.ndarray, rho: float):
+    """Eq. 6 from attention probabilities attn [H][L][L] (bf16 bits, query-major,
+    causal) and tokens x [L][d] (bf16 bits).  Returns (I [L] fp64, mask [L] uint8)."""
+    attn_bits = np.ascontiguousarray(attn_bits, dtype=np.uint16)
+    x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
+    H, L, L2 = attn_bits.shape
+    assert L == L2 and x_bits.shape[0] == L
+    d = x_bits.shape[1]
+    I = np.empty(L, np.float64)
+    mask = np.empty(L, np.uint8)
+    rc = _load().orc_token_importance(_p(attn_bits), H, L, _p(x_bits), d, protect_count(L, rho),
+                                      _p(I), _p(mask))
+    if rc:
+        raise ValueError("bad token_importance arguments")
+    return I, mask
+
+
+def median_ratio(logits: np.ndarray) -> float:
+    """mu = median over tokens of w1/w0 of the top-2 experts (Sec. 3.3.1)."""
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    T, E = logits.shape
+    mu = _load().orc_median_ratio(_p(logits), T, E)
+    if mu < 0:
+        raise ValueError("bad median_ratio arguments")
+    return mu

@@ -14,7 +14,9 @@
  *   Sec. 3.1 Eq. 1                     -- MoE layer output over the top-k;
  *   Sec. 3.3.1 Eq. 5                   -- weight-only expert pruning;
  *   Sec. 3.3.2                         -- protected (important) tokens keep
- *                                         all their experts.
+ *                                         all their experts;
+ *   Sec. 3.3.2 Eq. 6                   -- token importance, protected set;
+ *   Sec. 3.3.1                         -- threshold as the median of w1/w0.
  */
 #include <math.h>
 #include <stdint.h>
@@ -390,4 +392,61 @@ int orc_expert_forward(const double *X, int nt, int d, int ffn, int G,
     free(wd);
   }
   return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Token importance (Sec. 3.3.2, Eq. 6), the protected set, and the pruning */
+/* threshold as a calibration median (Sec. 3.3.1).                          */
+/* ------------------------------------------------------------------------ */
+
+/* attn: [H][L][L] bf16 bits, attn[h][i][j] = attention probability of query i
+ * on key j (causal: only j <= i is read); x: [L][d] bf16 bits (the tokens).
+ * With 0-based j the key is seen by the queries i = j..L-1, L - j of them:
+ *   I_j = ||x_j||_1 * (1/H) * sum_h sum_{i=j}^{L-1} attn[h][i][j] / (L - j)
+ * in fp64.  mask: the n largest I_j, equal values ordered by lower index
+ * (repeated selection of the best remaining token). */
+int orc_token_importance(const uint16_t *attn, int H, int L, const uint16_t *x, int d, int n,
+                         double *I, uint8_t *mask) {
+  if (H <= 0 || L <= 0 || d <= 0 || n < 0 || n > L) return 1;
+  for (int j = 0; j < L; j++) {
+    double col = 0.0;
+    for (int h = 0; h < H; h++)
+      for (int i = j; i < L; i++) col += orc_bf16_to_double(attn[((size_t)h * L + i) * L + j]);
+    double norm = 0.0;
+    for (int c = 0; c < d; c++) norm += fabs(orc_bf16_to_double(x[(size_t)j * d + c]));
+    I[j] = norm * (col / H) / (double)(L - j);
+    mask[j] = 0;
+  }
+  for (int s = 0; s < n; s++) {
+    int best = -1;
+    for (int j = 0; j < L; j++)
+      if (!mask[j] && (best < 0 || I[j] > I[best])) best = j;
+    mask[best] = 1;
+  }
+  return 0;
+}
+
+static int cmp_double(const void *a, const void *b) {
+  const double x = *(const double *)a, y = *(const double *)b;
+  return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+/* mu = the median over tokens of w_1 / w_0 = exp(l_1 - l_0) of the top-2
+ * experts (ranking rule of orc_route); for an even count the mean of the two
+ * middle values.  Returns mu, or -1 on bad arguments. */
+double orc_median_ratio(const float *logits, int T, int E) {
+  if (T <= 0 || E < 2) return -1.0;
+  double *r = (double *)malloc(sizeof(double) * T);
+  for (int t = 0; t < T; t++) {
+    const float *l = logits + (size_t)t * E;
+    int a = 0;
+    for (int e = 1; e < E; e++) if (rank_before(l, e, a)) a = e;
+    int b = a == 0 ? 1 : 0;
+    for (int e = 0; e < E; e++) if (e != a && rank_before(l, e, b)) b = e;
+    r[t] = exp((double)l[b] - (double)l[a]);
+  }
+  qsort(r, T, sizeof(double), cmp_double);
+  const double mu = (T & 1) ? r[T / 2] : 0.5 * (r[T / 2 - 1] + r[T / 2]);
+  free(r);
+  return mu;
 }

@@ -378,3 +378,101 @@ def test_forward_rows_and_tokens_subset():
     toks = [3, 10, 63]
     part = oracle.moe_forward(x, rt, logical, 32, rows=rows, tokens=toks)
     np.testing.assert_array_equal(part, full[np.ix_(toks, rows)])
+
+
+# ------------------------------------------------------- Eq. 6 importance ---
+
+def _causal_attention(g, H, L):
+    """Random causal attention probabilities (row-softmax over keys j <= i), bf16 bits."""
+    s = g.standard_normal((H, L, L))
+    s[:, np.triu_indices(L, 1)[0], np.triu_indices(L, 1)[1]] = -np.inf
+    p = np.exp(s - s.max(axis=2, keepdims=True))
+    p /= p.sum(axis=2, keepdims=True)
+    return oracle.bf16_round_array(p)
+
+
+def test_importance_golden():
+    rows = [l.split() for l in open(os.path.join(GOLD, "importance_small.txt")) if l[0] != "#" and l.strip()]
+    A = np.array([[float(v) for v in r[1:]] for r in rows if r[0] == "attn"])[None]
+    x = np.array([[float(v) for v in r[1:]] for r in rows if r[0] == "token"])
+    want = [float(v) for r in rows if r[0] == "importance" for v in r[1:]]
+    for r in rows:
+        if r[0] == "rho":
+            I, mask = oracle.token_importance(oracle.bf16_round_array(A), oracle.bf16_round_array(x), float(r[1]))
+            np.testing.assert_allclose(I, want, rtol=1e-12)
+            assert mask.tolist() == [int(v) for v in r[3:]]
+
+
+def test_importance_closed_forms():
+    """Self-attention only: column sums 1, I_j = ||t_j||_1 / (L - j).  All
+    attention on the first token: I_0 = ||t_0||_1, every other I_j = 0."""
+    g = np.random.default_rng(11)
+    H, L, d = 3, 37, 16
+    xb = oracle.bf16_round_array(g.standard_normal((L, d)))
+    norms = np.abs(oracle.bf16_to_float64(xb)).sum(axis=1)
+    one = oracle.bf16_round_array(np.ones(1))[0]
+    A = np.zeros((H, L, L), np.uint16)
+    A[:, np.arange(L), np.arange(L)] = one
+    I, _ = oracle.token_importance(A, xb, 0.1)
+    np.testing.assert_allclose(I, norms / (L - np.arange(L)), rtol=1e-14)
+    A = np.zeros((H, L, L), np.uint16)
+    A[:, :, 0] = one
+    I, mask = oracle.token_importance(A, xb, 0.1)
+    np.testing.assert_allclose(I[0], norms[0], rtol=1e-14)
+    assert np.all(I[1:] == 0.0)
+    # n = floor(0.1 * 37 + 1/2) = 4: token 0, then the zero-importance tokens 1, 2, 3 (lowest index)
+    assert mask.tolist() == [1, 1, 1, 1] + [0] * (L - 4)
+
+
+def test_importance_uniform_causal():
+    """Uniform causal attention 1/(i+1) (rounded to bf16 here, so compared to
+    the harmonic closed form at bf16 precision)."""
+    L, d = 50, 8
+    A = np.tril(np.ones((L, L))) / (np.arange(L)[:, None] + 1.0)
+    g = np.random.default_rng(3)
+    xb = oracle.bf16_round_array(g.standard_normal((L, d)))
+    norms = np.abs(oracle.bf16_to_float64(xb)).sum(axis=1)
+    I, _ = oracle.token_importance(oracle.bf16_round_array(A)[None], xb, 0.02)
+    harm = np.array([sum(1.0 / (i + 1) for i in range(j, L)) for j in range(L)])
+    np.testing.assert_allclose(I, norms * harm / (L - np.arange(L)), rtol=2 ** -8)
+
+
+def test_importance_heads_and_triangle():
+    """I over H heads = mean of the single-head I's (the head average); values
+    above the diagonal are never read."""
+    g = np.random.default_rng(5)
+    H, L, d = 4, 29, 12
+    A = _causal_attention(g, H, L)
+    xb = oracle.bf16_round_array(g.standard_normal((L, d)))
+    I, _ = oracle.token_importance(A, xb, 0.1)
+    per = np.mean([oracle.token_importance(A[h:h + 1], xb, 0.1)[0] for h in range(H)], axis=0)
+    np.testing.assert_allclose(I, per, rtol=1e-12)
+    junk = A.copy()
+    iu = np.triu_indices(L, 1)
+    junk[:, iu[0], iu[1]] = 0x7f7f
+    np.testing.assert_array_equal(oracle.token_importance(junk, xb, 0.1)[0], I)
+
+
+@pytest.mark.parametrize("L,rho", [(1, 0.02), (50, 0.02), (100, 0.02), (333, 0.1), (64, 0.5)])
+def test_importance_selection_brute_force(L, rho):
+    g = np.random.default_rng(L)
+    A = _causal_attention(g, 2, L)
+    xb = oracle.bf16_round_array(g.standard_normal((L, 8)))
+    I, mask = oracle.token_importance(A, xb, rho)
+    n = int(np.floor(rho * L + 0.5))
+    assert oracle.protect_count(L, rho) == n
+    top = sorted(range(L), key=lambda j: (-I[j], j))[:n]
+    assert np.flatnonzero(mask).tolist() == sorted(top)
+
+
+def test_median_ratio_brute_force():
+    import statistics
+    g = np.random.default_rng(8)
+    for T, E in ((1, 2), (7, 8), (64, 8), (100, 64)):
+        lg = g.standard_normal((T, E)).astype(np.float32)
+        lg[::3, 1] = lg[::3, 0]                      # ties keep a ratio of 1
+        ratios = []
+        for t in range(T):
+            order = sorted(range(E), key=lambda e: (-float(lg[t, e]), e))
+            ratios.append(math.exp(float(lg[t, order[1]]) - float(lg[t, order[0]])))
+        assert oracle.median_ratio(lg) == pytest.approx(statistics.median(ratios), rel=1e-15)
