@@ -156,12 +156,43 @@ mc_status mc_moe_forward(const uint16_t *x_bf16, const mc_routing *r,
                          const mc_layer *L, uint16_t *y_bf16, void *workspace,
                          size_t ws_bytes, void *stream);
 
+/* Workspace bytes mc_token_importance needs for H heads and L tokens
+ * (about 256*(L/128)^2 + 8*L).  Errors: MC_EINVAL, MC_EUNSUPPORTED (L above
+ * MC_MAX_TOKENS). */
+mc_status mc_importance_workspace(int H, int L, size_t *bytes);
+
+/* Token importance (Sec. 3.3.2, Eq. 6) and the protected set for
+ * mc_route_and_prune.  attn: [H][L][L] bf16 causal attention probabilities
+ * (>= 0), attn[h][i][j] = weight of query i on key j; only j <= i is read.
+ * x: [L][d] bf16 token vectors (the MoE layer input).  With 0-based j:
+ *   I_j = ||x_j||_1 * (1/H) * sum_h sum_{i=j}^{L-1} attn[h][i][j] / (L - j),
+ * the mean attention key j receives from the L - j queries that see it,
+ * averaged over heads; fp32 sums in a fixed order.  important[j] = 1 for the
+ * floor(rho*L + 1/2) largest I_j (equal values: lower j first), 0 otherwise;
+ * the paper protects 2 % (rho = 0.02).  importance ([L] fp32) may be NULL.
+ * workspace: ws_bytes >= mc_importance_workspace(H, L).  Async on `stream`.
+ * Errors: MC_EINVAL (shape, rho outside [0, 1], NULL pointer), MC_ENOSPACE,
+ * MC_EUNSUPPORTED (L above MC_MAX_TOKENS), MC_EHIP. */
+mc_status mc_token_importance(const uint16_t *attn_bf16, int H, int L, const uint16_t *x_bf16, int d,
+                              float rho, float *importance, uint8_t *important, void *workspace,
+                              size_t ws_bytes, void *stream);
+
+/* Pruning threshold from calibration router logits (Sec. 3.3.1: mu is the
+ * median of w_1/w_0 over calibration tokens).  logits_host: [T][E] fp32 in
+ * HOST memory, finite.  w_1/w_0 = exp(l_1 - l_0) of the two largest logits
+ * (equal logits: lower expert index first); *mu = their median (mean of the
+ * two middle values for even T); *tau = mu / (1 + mu), the threshold
+ * mc_route_and_prune takes (identical decision at k = 2).  Offline helper,
+ * pure host computation.  Errors: MC_EINVAL. */
+mc_status mc_odp_threshold(const float *logits_host, int T, int E, double *mu, double *tau);
+
 /* Instrumentation.  mc_timing_enable(1) clears the record and brackets every
  * kernel launch made afterwards by two HIP events on the launch stream;
  * mc_timing_enable(0) stops recording.  mc_timing_read waits for the recorded
  * events of one kernel and returns the summed duration in ms and the number
  * of launches.  Kernel names: pack_scale_zero, pack_codes, export,
- * route_fused, route_select, route_lists, gateup, down, combine.
+ * route_fused, route_select, route_lists, prefill_prep, gateup, down, combine,
+ * importance_colsum, importance_select.
  * Errors: MC_EINVAL (unknown name, NULL pointer), MC_EHIP. */
 mc_status mc_timing_enable(int on);
 mc_status mc_timing_read(const char *kernel, double *total_ms, int *launches);

@@ -12,12 +12,15 @@ from ._binding import (  # noqa: F401
     codes_export,
     dequant_export,
     forward_workspace,
+    importance_workspace,
     lib_path,
     load,
     moe_forward,
+    odp_threshold,
     pack,
     pack_sizes,
     route_and_prune,
     timing_enable,
     timing_read,
+    token_importance,
 )

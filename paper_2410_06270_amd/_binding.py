@@ -73,6 +73,13 @@ def load():
         lib.mc_moe_forward.restype = st
         lib.mc_moe_forward.argtypes = [P, ctypes.POINTER(_Routing), ctypes.POINTER(_Layer), P, P,
                                        S, P]
+        lib.mc_importance_workspace.restype = st
+        lib.mc_importance_workspace.argtypes = [I, I, ctypes.POINTER(S)]
+        lib.mc_token_importance.restype = st
+        lib.mc_token_importance.argtypes = [P, I, I, P, I, ctypes.c_float, P, P, P, S, P]
+        lib.mc_odp_threshold.restype = st
+        lib.mc_odp_threshold.argtypes = [P, I, I, ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(ctypes.c_double)]
         lib.mc_timing_enable.restype = st
         lib.mc_timing_enable.argtypes = [I]
         lib.mc_timing_read.restype = st
@@ -182,6 +189,33 @@ def moe_forward(x, routing: Routing, layer: PackedLayer, y, workspace, stream=No
     _check(load().mc_moe_forward(_ptr(x), ctypes.byref(routing.desc), ctypes.byref(layer.desc),
                                  _ptr(y), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                  _stream(stream)))
+
+
+def importance_workspace(H: int, L: int) -> int:
+    b = ctypes.c_size_t()
+    _check(load().mc_importance_workspace(H, L, ctypes.byref(b)))
+    return b.value
+
+
+def token_importance(attn, x, rho: float, important, workspace, importance=None, stream=None):
+    """attn: [H][L][L] bf16 bits (int16 tensor), x: [L][d] bf16 bits; writes the
+    protected mask (uint8 [L]) and, if given, the importance (float32 [L])."""
+    H, L, _ = attn.shape
+    d = x.shape[1]
+    _check(load().mc_token_importance(_ptr(attn), H, L, _ptr(x), d, ctypes.c_float(rho),
+                                      None if importance is None else _ptr(importance), _ptr(important),
+                                      _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                      _stream(stream)))
+
+
+def odp_threshold(logits_host):
+    """(mu, tau) from calibration logits (a C-contiguous float32 numpy array [T][E])."""
+    import numpy as np
+    lg = np.ascontiguousarray(logits_host, dtype=np.float32)
+    mu, tau = ctypes.c_double(), ctypes.c_double()
+    _check(load().mc_odp_threshold(lg.ctypes.data_as(ctypes.c_void_p), lg.shape[0], lg.shape[1],
+                                   ctypes.byref(mu), ctypes.byref(tau)))
+    return mu.value, tau.value
 
 
 def timing_enable(on: bool = True):

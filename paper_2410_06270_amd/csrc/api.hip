@@ -1,9 +1,11 @@
 // api.hip -- the extern "C" boundary: argument validation, descriptors,
 // launches on the caller's stream.  No allocation anywhere.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <vector>
 
 #include "mc_internal.hpp"
 
@@ -185,6 +187,53 @@ mc_status mc_moe_forward(const uint16_t* x_bf16, const mc_routing* r, const mc_l
   return hip_status(mc::launch_forward(x_bf16, a, *r, y_bf16, workspace,
                                        static_cast<hipStream_t>(stream)),
                     "mc_moe_forward launch");
+}
+
+mc_status mc_importance_workspace(int H, int L, size_t* bytes) {
+  if (H < 1 || L < 1) return fail(MC_EINVAL, "bad shape H=%d L=%d", H, L);
+  if (L > MC_MAX_TOKENS) return fail(MC_EUNSUPPORTED, "L=%d above %d", L, MC_MAX_TOKENS);
+  if (!bytes) return fail(MC_EINVAL, "bytes pointer is NULL");
+  *bytes = mc::importance_workspace_bytes(H, L);
+  return MC_OK;
+}
+
+mc_status mc_token_importance(const uint16_t* attn_bf16, int H, int L, const uint16_t* x_bf16, int d,
+                              float rho, float* importance, uint8_t* important, void* workspace,
+                              size_t ws_bytes, void* stream) {
+  if (H < 1 || L < 1 || d < 1) return fail(MC_EINVAL, "bad shape H=%d L=%d d=%d", H, L, d);
+  if (L > MC_MAX_TOKENS) return fail(MC_EUNSUPPORTED, "L=%d above %d", L, MC_MAX_TOKENS);
+  if (!(rho >= 0.0f && rho <= 1.0f)) return fail(MC_EINVAL, "rho %g outside [0, 1]", (double)rho);
+  if (!attn_bf16 || !x_bf16 || !important || !workspace)
+    return fail(MC_EINVAL, "attn, x, important or workspace is NULL");
+  const size_t need = mc::importance_workspace_bytes(H, L);
+  if (ws_bytes < need) return fail(MC_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+  (void)hipGetLastError();
+  return hip_status(mc::launch_importance(attn_bf16, H, L, x_bf16, d, rho, importance, important, workspace,
+                                          static_cast<hipStream_t>(stream)),
+                    "mc_token_importance launch");
+}
+
+mc_status mc_odp_threshold(const float* logits_host, int T, int E, double* mu, double* tau) {
+  if (!logits_host || !mu || !tau) return fail(MC_EINVAL, "NULL argument");
+  if (T < 1 || E < 2) return fail(MC_EINVAL, "bad shape T=%d E=%d (need E >= 2)", T, E);
+  std::vector<double> r(T);
+  for (int t = 0; t < T; ++t) {
+    const float* l = logits_host + (size_t)t * E;
+    // top-2 by (logit descending, expert index ascending); -0 == +0 as floats
+    int a = 0;
+    for (int e = 1; e < E; ++e)
+      if (l[e] > l[a]) a = e;
+    int b = a == 0 ? 1 : 0;
+    for (int e = 0; e < E; ++e)
+      if (e != a && l[e] > l[b]) b = e;
+    if (!std::isfinite(l[a]) || !std::isfinite(l[b])) return fail(MC_EINVAL, "non-finite logit at token %d", t);
+    r[t] = std::exp((double)l[b] - (double)l[a]);
+  }
+  std::sort(r.begin(), r.end());
+  const double m = (T & 1) ? r[T / 2] : 0.5 * (r[T / 2 - 1] + r[T / 2]);
+  *mu = m;
+  *tau = m / (1.0 + m);
+  return MC_OK;
 }
 
 mc_status mc_timing_enable(int on) {

@@ -10,7 +10,7 @@ constexpr int kDecodeMaxT = 64;        // up to this many tokens one workgroup h
 
 enum TimingSite {
   kSitePackSz, kSitePackCodes, kSiteExport, kSiteRouteFused, kSiteRouteSelect, kSiteRouteLists,
-  kSiteGateUp, kSiteDown, kSiteCombine, kSitePrefillPrep, kNumSites
+  kSiteGateUp, kSiteDown, kSiteCombine, kSitePrefillPrep, kSiteImpColsum, kSiteImpSelect, kNumSites
 };
 void timing_begin(hipStream_t stream, int site);
 void timing_end(hipStream_t stream, int site);
@@ -39,5 +39,8 @@ hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routin
                           float** partial, size_t* part_stride, int* nsplit, hipStream_t stream);
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
                           void* ws, hipStream_t stream);
+size_t importance_workspace_bytes(int H, int L);
+hipError_t launch_importance(const uint16_t* attn, int H, int L, const uint16_t* x, int d, float rho,
+                             float* importance, uint8_t* mask, void* ws, hipStream_t stream);
 
 }  // namespace mc

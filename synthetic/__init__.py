@@ -22,6 +22,9 @@ Workloads (the paper's Mixtral 8x7b and OLMoE shapes; no dataset is used):
 
 Weights are N(0, 0.02^2) fp32, activations N(0,1) rounded once to bfloat16,
 and round(0.1*T) tokens (a seeded permutation) are marked important.
+Attention maps (the input of token importance) are causal row softmaxes of
+scores N(0, 1.5^2) with +4 on the first key (an attention sink), rounded to
+bfloat16.
 """
 from __future__ import annotations
 
@@ -41,7 +44,7 @@ CONFIGS = {
 }
 
 # stream ids inside a config's seed
-_S_X, _S_BIAS, _S_LOGITS, _S_MASK, _S_BITS = 1, 2, 3, 4, 5
+_S_X, _S_BIAS, _S_LOGITS, _S_MASK, _S_BITS, _S_ATTN = 1, 2, 3, 4, 5, 6
 _S_WEIGHT = 1000
 
 
@@ -126,3 +129,22 @@ def important_mask(config_id: int, T: int, frac: float = 0.1) -> np.ndarray:
     m = np.zeros(T, np.uint8)
     m[g.permutation(T)[:n]] = 1
     return m
+
+
+def attention(config_id: int, H: int, L: int) -> np.ndarray:
+    """Causal attention probabilities [H][L][L] as bfloat16 bits, query-major:
+    row i is a softmax over keys 0..i of N(0, 1.5^2) scores with +4 on key 0,
+    zeros above the diagonal."""
+    g = rng(config_id, _S_ATTN + 100 * L + 100000 * H)
+    out = np.empty((H, L, L), np.uint16)
+    above = np.triu(np.ones((L, L), bool), 1)
+    for h in range(H):
+        s = g.standard_normal(size=(L, L), dtype=np.float32)
+        s *= np.float32(1.5)
+        s[:, 0] += np.float32(4.0)
+        s[above] = -np.inf
+        s -= s.max(axis=1, keepdims=True)
+        np.exp(s, out=s)
+        s /= s.sum(axis=1, keepdims=True)
+        out[h] = to_bf16_bits(s)
+    return out

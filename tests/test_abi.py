@@ -2,6 +2,7 @@
 host-side validation rejects bad arguments before any HIP call (so these run
 without a GPU: every call here returns from validation)."""
 import ctypes
+import math
 import os
 import re
 
@@ -163,3 +164,36 @@ def test_pack_rejects(lib):
     assert lib.mc_pack(None, P(2), P(3), ctypes.byref(L), None) == 1
     assert lib.mc_dequant_export(ctypes.byref(L), 8, 0, P(5), None) == 1
     assert lib.mc_codes_export(ctypes.byref(L), 0, 3, P(5), None) == 1
+
+
+def test_importance_rejects(lib):
+    """Shape, rho, NULL and workspace checks of mc_token_importance (no launch)."""
+    P = ctypes.c_void_p
+    b = ctypes.c_size_t()
+    assert lib.mc_importance_workspace(4, 4096, ctypes.byref(b)) == 0
+    need = b.value
+    assert need >= 32 * 33 // 2 * 128 * 4 + 4096 * 8
+    assert lib.mc_importance_workspace(0, 16, ctypes.byref(b)) == 1
+    assert lib.mc_importance_workspace(1, 65537, ctypes.byref(b)) == 4
+    f = ctypes.c_float
+    args = lambda H, L, d, rho, ws: (P(0x10), H, L, P(0x20), d, f(rho), None, P(0x30), P(0x40), ws, None)
+    assert lib.mc_token_importance(*args(4, 4096, 64, 0.02, need - 1)) == 2
+    assert lib.mc_token_importance(*args(4, 4096, 64, 1.5, need)) == 1
+    assert lib.mc_token_importance(*args(4, 4096, 0, 0.02, need)) == 1
+    assert lib.mc_token_importance(*args(4, 65537, 64, 0.02, 1 << 40)) == 4
+    assert lib.mc_token_importance(None, 4, 4096, P(0x20), 64, f(0.02), None, P(0x30), P(0x40), need, None) == 1
+
+
+def test_odp_threshold_host(lib):
+    """Median of w1/w0 on the host: odd and even counts, ties, bad arguments."""
+    import numpy as np
+    from paper_2410_06270_amd import odp_threshold
+    lg = np.array([[0, 1, 2], [0, 0, 3], [1, 2, 0]], np.float32)
+    mu, tau = odp_threshold(lg)
+    assert mu == pytest.approx(math.exp(-1.0), rel=1e-15)
+    assert tau == pytest.approx(mu / (1 + mu), rel=1e-15)
+    mu, _ = odp_threshold(lg[:2])
+    assert mu == pytest.approx(0.5 * (math.exp(-1.0) + math.exp(-3.0)), rel=1e-15)
+    d = ctypes.c_double()
+    assert lib.mc_odp_threshold(ctypes.c_void_p(lg.ctypes.data), 3, 1, ctypes.byref(d), ctypes.byref(d)) == 1
+    assert lib.mc_odp_threshold(None, 3, 3, ctypes.byref(d), ctypes.byref(d)) == 1

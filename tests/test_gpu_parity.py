@@ -342,3 +342,64 @@ def test_graph_replay_matches_eager(mc, tiny):
         mc.moe_forward(x, r, L, y, ws)        # eager work between replays
         torch.cuda.synchronize()
         assert torch.equal(y, y_eager)
+
+
+# ------------------------------------------------------- Eq. 6 importance ---
+
+def importance_gpu(mc, attn_bits, x_bits, rho):
+    H, L, _ = attn_bits.shape
+    a = to_dev(attn_bits.view(np.int16))
+    x = to_dev(x_bits.view(np.int16))
+    imp = torch.empty(L, dtype=torch.float32, device="cuda")
+    mask = torch.empty(L, dtype=torch.uint8, device="cuda")
+    ws = torch.empty(mc.importance_workspace(H, L), dtype=torch.uint8, device="cuda")
+    mc.token_importance(a, x, rho, mask, ws, importance=imp)
+    torch.cuda.synchronize()
+    return imp.cpu().numpy(), mask.cpu().numpy()
+
+
+def assert_selection_margin(I, n):
+    """The n-th and (n+1)-th largest importances differ by more than fp32 noise."""
+    if 0 < n < len(I):
+        s = np.sort(I)[::-1]
+        assert s[n - 1] - s[n] > 1e-5 * s[n - 1], (s[n - 1], s[n])
+
+
+@pytest.mark.parametrize("H,L,d,rho", [
+    (1, 4, 2, 0.5), (2, 300, 64, 0.02), (4, 512, 128, 0.1), (3, 1000, 96, 0.02), (1, 129, 8, 0.5),
+    (2, 256, 4096, 0.02), (1, 1, 4, 1.0), (1, 1, 4, 0.4),
+])
+def test_importance_parity(mc, H, L, d, rho):
+    A = synthetic.attention(1, H, L)
+    xb = synthetic.activations(1, L, d=d)
+    I_ref, m_ref = oracle.token_importance(A, xb, rho)
+    assert_selection_margin(I_ref, oracle.protect_count(L, rho))
+    I, m = importance_gpu(mc, A, xb, rho)
+    np.testing.assert_allclose(I, I_ref, rtol=2e-5, atol=0)
+    np.testing.assert_array_equal(m, m_ref)
+
+
+def test_importance_ties_and_edges(mc):
+    """All attention on the first token: every other importance is exactly 0 and
+    the remaining protected slots go to the lowest indices; rho = 0 and 1."""
+    H, L, d = 2, 200, 32
+    A = np.zeros((H, L, L), np.uint16)
+    A[:, :, 0] = 0x3F80          # 1.0
+    xb = synthetic.activations(1, L, d=d)
+    for rho in (0.0, 0.02, 0.1, 1.0):
+        I_ref, m_ref = oracle.token_importance(A, xb, rho)
+        I, m = importance_gpu(mc, A, xb, rho)
+        np.testing.assert_allclose(I, I_ref, rtol=1e-6)
+        np.testing.assert_array_equal(m, m_ref)
+
+
+def test_importance_mixtral_sized(mc):
+    """8 heads over 4096 tokens of d = 4096 (the prefill batch), rho = 2 %."""
+    H, L, d = 8, 4096, 4096
+    A = synthetic.attention(3, H, L)
+    xb = synthetic.activations(3, L)
+    I_ref, m_ref = oracle.token_importance(A, xb, 0.02)
+    assert_selection_margin(I_ref, oracle.protect_count(L, 0.02))
+    I, m = importance_gpu(mc, A, xb, 0.02)
+    np.testing.assert_allclose(I, I_ref, rtol=2e-5)
+    np.testing.assert_array_equal(m, m_ref)
