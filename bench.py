@@ -10,7 +10,8 @@ line: decode at 1 and 8 tokens, prefill of 4096 tokens with the threshold
 swept over {0, 0.2, 0.4} (pruned fraction, tokens/s, MFMA fraction of the
 algorithmic 6*d*ffn FLOPs per kept pair), and the OLMoE-shaped layer (d=2048,
 ffn=1024, 64 experts, top-8, G=64, Zipf-skewed logits, threshold 0.05) in
-decode (16 tokens) and prefill (2048 tokens).
+decode (16 tokens) and prefill (2048 tokens), and the token importance that
+marks the protected tokens (32 heads, 4096 tokens, rho = 0.02).
 
 One step = route_and_prune + moe_forward over the batch for one layer.  The
 step rotates over packed copies of the layer (4 x 484 MB Mixtral, 3 x 131 MB
@@ -48,6 +49,7 @@ def parse():
     p.add_argument("--prefill-steps", type=int, default=10)
     p.add_argument("--no-prefill", action="store_true", help="skip the 4096-token prefill sweep")
     p.add_argument("--no-olmoe", action="store_true", help="skip the OLMoE-shaped layer")
+    p.add_argument("--no-importance", action="store_true", help="skip the token-importance measurement")
     p.add_argument("--graph", action="store_true",
                    help="also time HIP-graph replays of the step (reported as ms_per_step_graph)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -263,6 +265,63 @@ def decode_entry(wl, ms, kus):
                 kernels_us={k2: round(v, 2) for k2, v in kus.items()})
 
 
+def importance_entry(mc, torch, steps, warmup):
+    """Token importance (Eq. 6) + protected set over a 4096-token prefill with
+    Mixtral's 32 attention heads and d=4096, rho=0.02.  Inputs drawn on the
+    device (torch's generator, seed 20241006): causal row softmaxes of
+    N(0, 1.5^2) scores with +4 on the first key, rounded to bf16; x ~ N(0,1)
+    in bf16.  The attention map (1.07 GB) exceeds the Infinity Cache, so every
+    step reads it from HBM.  Roofline of importance_colsum: the lower triangle
+    of bf16 attention, H * L * (L + 1) bytes, plus x (2 * L * d) per launch."""
+    H, L, d, rho = 32, 4096, 4096, 0.02
+    g = torch.Generator(device="cuda")
+    g.manual_seed(20241006)
+    attn = torch.empty((H, L, L), dtype=torch.int16, device="cuda")
+    above = torch.ones((L, L), dtype=torch.bool, device="cuda").triu_(1)
+    for h in range(H):
+        sc = torch.randn((L, L), generator=g, device="cuda") * 1.5
+        sc[:, 0] += 4.0
+        sc.masked_fill_(above, float("-inf"))
+        attn[h] = torch.softmax(sc, dim=1).to(torch.bfloat16).view(torch.int16)
+        del sc
+    x = torch.randn((L, d), generator=g, device="cuda").to(torch.bfloat16).view(torch.int16)
+    ws = torch.empty(mc.importance_workspace(H, L), dtype=torch.uint8, device="cuda")
+    mask = torch.empty(L, dtype=torch.uint8, device="cuda")
+    imp = torch.empty(L, dtype=torch.float32, device="cuda")
+    run = lambda: mc.token_importance(attn, x, rho, mask, ws, importance=imp)
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(steps):
+        run()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    mc.timing_enable(True)
+    for _ in range(steps):
+        run()
+    torch.cuda.synchronize()
+    kus = {}
+    for name in ("importance_colsum", "importance_finish", "importance_select"):
+        t, n = mc.timing_read(name)
+        kus[name] = 1e3 * t / max(n, 1)
+    mc.timing_enable(False)
+    protected = int(mask.sum().item())
+    del attn
+    torch.cuda.empty_cache()
+    tri = H * L * (L + 1)                        # bytes of the bf16 lower triangle
+    colsum_bytes = tri + L * d * 2               # + x, read by the norm workgroups of the same launch
+    step_bytes = colsum_bytes + L * 5
+    return dict(workload="mixtral_8x7b_token_importance", heads=H, tokens=L, d=d, rho=rho,
+                protected=protected, ms_per_step=round(ms, 5), tokens_per_s=round(L / (ms / 1e3), 1),
+                step_hbm_gbs=round(step_bytes / (ms * 1e6), 1),
+                colsum_alg_bytes=colsum_bytes,
+                colsum_hbm_frac=round(colsum_bytes / (kus["importance_colsum"] * 1e3) / HBM_PEAK_GBS, 4),
+                kernels_us={k: round(v, 2) for k, v in kus.items()})
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -373,6 +432,8 @@ def main():
         out["olmoe"] = {"workload": "olmoe_moe_layer", "d": 2048, "ffn": 1024, "experts": 64, "top_k": 8,
                         "group": 64, "bits": wo.c["bits"], "tau": wo.tau, "layer_copies": 3,
                         "decode": dec, "prefill": prefill_entry(wo, ms_p, kus)}
+    if not args.no_importance:
+        out["importance"] = importance_entry(mc, torch, 20, 3)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(synthetic, T)
     print(json.dumps(out), flush=True)

@@ -10,7 +10,8 @@ constexpr int kDecodeMaxT = 64;        // up to this many tokens one workgroup h
 
 enum TimingSite {
   kSitePackSz, kSitePackCodes, kSiteExport, kSiteRouteFused, kSiteRouteSelect, kSiteRouteLists,
-  kSiteGateUp, kSiteDown, kSiteCombine, kSitePrefillPrep, kSiteImpColsum, kSiteImpSelect, kNumSites
+  kSiteGateUp, kSiteDown, kSiteCombine, kSitePrefillPrep, kSiteImpColsum, kSiteImpFinish, kSiteImpSelect,
+  kNumSites
 };
 void timing_begin(hipStream_t stream, int site);
 void timing_end(hipStream_t stream, int site);

@@ -393,11 +393,12 @@ def test_importance_ties_and_edges(mc):
         np.testing.assert_array_equal(m, m_ref)
 
 
-def test_importance_mixtral_sized(mc):
-    """8 heads over 4096 tokens of d = 4096 (the prefill batch), rho = 2 %."""
-    H, L, d = 8, 4096, 4096
+@pytest.mark.parametrize("H,L,d", [(32, 4096, 4096), (3, 8192, 64)])
+def test_importance_large(mc, H, L, d):
+    """Mixtral's 32 heads over a 4096-token prefill of d = 4096 (four heads per
+    workgroup), and 3 heads over 8192 tokens (head slices of 2 and 1); rho = 2 %."""
     A = synthetic.attention(3, H, L)
-    xb = synthetic.activations(3, L)
+    xb = synthetic.activations(3, L, d=d)
     I_ref, m_ref = oracle.token_importance(A, xb, 0.02)
     assert_selection_margin(I_ref, oracle.protect_count(L, 0.02))
     I, m = importance_gpu(mc, A, xb, 0.02)
