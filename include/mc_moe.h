@@ -156,9 +156,10 @@ mc_status mc_moe_forward(const uint16_t *x_bf16, const mc_routing *r,
                          const mc_layer *L, uint16_t *y_bf16, void *workspace,
                          size_t ws_bytes, void *stream);
 
-/* Workspace bytes mc_token_importance needs for H heads and L tokens
- * (about 256*(L/128)^2 + 8*L).  Errors: MC_EINVAL, MC_EUNSUPPORTED (L above
- * MC_MAX_TOKENS). */
+/* Workspace bytes mc_token_importance needs for H heads and L tokens: fp32
+ * partial sums, 512 B per 128x128 tile of the lower triangle and slice of
+ * heads (about 2 MB up to 8192 tokens, 67 MB at 65,536), plus 12 B per token.
+ * Errors: MC_EINVAL, MC_EUNSUPPORTED (L above MC_MAX_TOKENS). */
 mc_status mc_importance_workspace(int H, int L, size_t *bytes);
 
 /* Token importance (Sec. 3.3.2, Eq. 6) and the protected set for
@@ -192,7 +193,7 @@ mc_status mc_odp_threshold(const float *logits_host, int T, int E, double *mu, d
  * events of one kernel and returns the summed duration in ms and the number
  * of launches.  Kernel names: pack_scale_zero, pack_codes, export,
  * route_fused, route_select, route_lists, prefill_prep, gateup, down, combine,
- * importance_colsum, importance_select.
+ * importance_colsum, importance_finish, importance_select.
  * Errors: MC_EINVAL (unknown name, NULL pointer), MC_EHIP. */
 mc_status mc_timing_enable(int on);
 mc_status mc_timing_read(const char *kernel, double *total_ms, int *launches);
