@@ -67,15 +67,15 @@ int forward_ksplit(int T, int E, int k, int d, int ffn) {
   return s;
 }
 
-// Workspace: h planes (bf16 hi, lo) | gate/up partials (when split) | down
-// partials, each part rounded up to 256 bytes.
+// Workspace: h (fp16) | gate/up partials (when split) | down partials, each
+// part rounded up to 256 bytes.
 static size_t round256(size_t b) { return ((b + 255) / 256) * 256; }
 
 size_t forward_workspace_bytes(int T, int E, int k, int d, int ffn) {
   if (T > kDecodeMaxT) return prefill_layout(T, E, k, d, ffn).total;
   const size_t P = (size_t)T * k;
   const int ks = forward_ksplit(T, E, k, d, ffn);
-  const size_t h = round256(2 * P * ffn * sizeof(uint16_t));
+  const size_t h = round256(P * ffn * sizeof(uint16_t));
   const size_t gu = ks > 1 ? round256((size_t)ks * 2 * P * ffn * sizeof(float)) : 0;
   const size_t part = (size_t)forward_nsplit(T, E, k, d, ffn) * P * d * sizeof(float);
   return h + gu + part;
@@ -116,12 +116,12 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
   }
   const size_t P = (size_t)T * k;
   Hidden hid;
-  hid.plane = P * L.ffn;
-  hid.h_hi = static_cast<uint16_t*>(ws);
+  hid.P = (int)P;
+  hid.h = static_cast<uint16_t*>(ws);
+  char* p = static_cast<char*>(ws) + round256(P * L.ffn * sizeof(uint16_t));
   hid.ksplit = forward_ksplit(T, r.E, k, L.d, L.ffn);
-  char* p = static_cast<char*>(ws) + round256(2 * hid.plane * sizeof(uint16_t));
   hid.gu_part = reinterpret_cast<float*>(p);
-  if (hid.ksplit > 1) p += round256((size_t)hid.ksplit * 2 * hid.plane * sizeof(float));
+  if (hid.ksplit > 1) p += round256((size_t)hid.ksplit * 2 * P * L.ffn * sizeof(float));
   float* partial = reinterpret_cast<float*>(p);
   const size_t part_stride = P * L.d;
   const int nsplit = forward_nsplit(T, r.E, k, L.d, L.ffn);

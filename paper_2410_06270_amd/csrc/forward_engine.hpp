@@ -3,18 +3,19 @@
 // y_t = sum over kept ranks r of w_r * E_{e_r}(x_t),
 // E_e(x) = W_down (silu(W_gate x) * (W_up x)), weights s*(q - z) per group.
 //
-// The codes go straight into bf16 MFMA operands as 128 + q (exact), so the
-// dequantized weight is never rounded: for each group g of G inputs
-//   sum_k s (q_k - z) x_k = s * (acc_g - (128 + z) * sum_k x_k),
-// acc_g = sum_k (128 + q_k) x_k from the MFMA; the group sums of x are formed
-// once per workgroup in LDS.  The hidden vector h is kept as two bf16 planes
-// (h = hi + lo, ~16 significant bits) for the down projection.
+// The codes go straight into 16-bit MFMA operands as an exact integer offset
+// by a power of two -- bf16 128 + q against the bf16 activations x (gate, up),
+// fp16 1024 + q against the fp16 hidden vector h (down) -- so the dequantized
+// weight is never rounded: for each group g of G inputs a_k
+//   sum_k s (q_k - z) a_k = s * (acc_g - (o + z) * sum_k a_k),
+// acc_g = sum_k (o + q_k) a_k from the MFMA, o the offset.  The group sums of
+// the activations (of the fp16 values, for h) are formed while they are staged.
 //
 // Kernels (all on the caller's stream, no host synchronisation; experts with
 // no kept token exit at once because the counts are read on the device):
 //   gateup_kernel  grid (ffn/128, E, chunks x d-splits): 8 waves x 16 rows of
 //                  gate and up, up to 16*NTMAX tokens of one expert per chunk
-//                  -> h planes (or fp32 gate/up partials when d is split);
+//                  -> h (fp16), or fp32 gate/up partials when d is split;
 //   down_kernel    grid (d/256, E, chunks*S): 8 waves x 32 rows, split-K over
 //                  ffn -> fp32 partials;
 //   combine_kernel grid (d/1024, T): y = bf16(sum_r w_r sum_s partial), fixed
@@ -25,8 +26,7 @@
 
 namespace mc {
 
-constexpr uint32_t kMagic2 = 0x43004300u;     // bf16 128.0 in both halves
-constexpr int kRowPad = 8;                    // bf16 elements of padding per slab row
+constexpr int kRowPad = 8;                    // elements of padding per slab row
 constexpr int kSxBytes = 4 * 1024;            // group sums of the staged slab (LDS)
 
 constexpr int kWavesPerWg = 8;                // workgroups of 512 threads share one slab
@@ -44,19 +44,18 @@ static_assert(kXsBytesLarge + 4 * 1024 + 64 * 4 <= kLdsPerCu, "one workgroup per
 // Chunks (16 rows x 128 columns of codes) kept in flight per stream.  The slab
 // is a multiple of this many chunks, so it is smaller where the slab rows are
 // many (token blocks) or the registers few (groups per chunk).
-__host__ __device__ constexpr int prefetch_depth(int ntb, int gpc, int planes) {
+__host__ __device__ constexpr int prefetch_depth(int ntb, int gpc) {
   return (ntb >= 3 || gpc >= 4) ? 2 : 4;
 }
 // Smallest slab (one ring of chunks) of the worst case of each token-block
-// count must fit its LDS budget: (planes x tokens + zero row) x (columns + pad) x 2 bytes.
-constexpr int slab_floor_bytes(int ntb, int planes) {
-  return (planes * 16 * ntb + 1) * (prefetch_depth(ntb, 1, planes) * kTileCols + kRowPad) * 2;
+// count must fit its LDS budget: (tokens + zero row) x (columns + pad) x 2 bytes.
+constexpr int slab_floor_bytes(int ntb) {
+  return (16 * ntb + 1) * (prefetch_depth(ntb, 1) * kTileCols + kRowPad) * 2;
 }
-static_assert(slab_floor_bytes(1, 2) <= kXsBytesSmall, "LDS budget (<= 16 tokens)");
-static_assert(slab_floor_bytes(2, 1) <= kXsBytesSmall, "LDS budget (<= 32 tokens, 1 plane)");
-static_assert(slab_floor_bytes(2, 2) <= kXsBytesSmall, "LDS budget (<= 32 tokens, 2 planes)");
-static_assert(slab_floor_bytes(3, 2) <= kXsBytesLarge, "LDS budget (<= 48 tokens)");
-static_assert(slab_floor_bytes(4, 2) <= kXsBytesLarge, "LDS budget (<= 64 tokens)");
+static_assert(slab_floor_bytes(1) <= kXsBytesSmall, "LDS budget (<= 16 tokens)");
+static_assert(slab_floor_bytes(2) <= kXsBytesSmall, "LDS budget (<= 32 tokens)");
+static_assert(slab_floor_bytes(3) <= kXsBytesLarge, "LDS budget (<= 48 tokens)");
+static_assert(slab_floor_bytes(4) <= kXsBytesLarge, "LDS budget (<= 64 tokens)");
 // Group sums: 16*ntb rows x (slab / G) groups x 4 bytes; the slab is capped by
 // kSxBytes, which must allow at least one ring of chunks at G = 32.
 static_assert((kSxBytes / (4 * 64)) * 32 >= 2 * kTileCols, "group-sum budget (64 tokens)");
@@ -64,8 +63,22 @@ static_assert((kSxBytes / (4 * 32)) * 32 >= 4 * kTileCols, "group-sum budget (32
 
 __device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
 
-__device__ __forceinline__ bf16x8 load_a(const uint16_t* p) {
-  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
+// Operand format of the activations: bf16 (x) or fp16 (h).  The code offset o
+// is the power of two whose 16-bit pattern ORs with a code in bits 0..2.
+template <bool F16>
+struct Fmt {
+  static constexpr uint32_t kMagic2 = F16 ? 0x64006400u : 0x43004300u;   // o in both halves
+  static constexpr float kOffset = F16 ? 1024.0f : 128.0f;
+};
+
+template <bool F16>
+__device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
+  if constexpr (F16)
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
 // A constant the compiler keeps in a VGPR: with the mask in an SGPR it lets
@@ -78,29 +91,37 @@ __device__ __forceinline__ uint32_t vgpr_constant(uint32_t c) {
 }
 
 template <int BITS>
-__device__ __forceinline__ bf16x8 b_operand(const uint32_t* w, int u, uint32_t magic) {
+__device__ __forceinline__ u32x4 b_operand(const uint32_t* w, int u, uint32_t magic) {
   u32x4 v;
   v[0] = extract_pair<BITS>(w, 4 * u + 0, magic);
   v[1] = extract_pair<BITS>(w, 4 * u + 1, magic);
   v[2] = extract_pair<BITS>(w, 4 * u + 2, magic);
   v[3] = extract_pair<BITS>(w, 4 * u + 3, magic);
-  return __builtin_bit_cast(bf16x8, v);
+  return v;
 }
 
-__device__ __forceinline__ float sum8_bf16(u32x4 v) {
+// Sum of the eight 16-bit values of a piece, in element order.
+template <bool F16>
+__device__ __forceinline__ float sum8(u32x4 v) {
   float s = 0.0f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    s += __uint_as_float(v[i] << 16);
-    s += __uint_as_float(v[i] & 0xffff0000u);
+    if constexpr (F16) {
+      s += half_bits_to_float(v[i] & 0xffffu);
+      s += half_bits_to_float(v[i] >> 16);
+    } else {
+      s += __uint_as_float(v[i] << 16);
+      s += __uint_as_float(v[i] & 0xffff0000u);
+    }
   }
   return s;
 }
 
-// Group epilogue: tot += s * (acc - (128 + z) * sum_x); acc = 0.
+// Group epilogue: tot += s * (acc - (o + z) * sum_a); acc = 0.
+template <bool F16>
 __device__ __forceinline__ void group_end(f32x4& acc, f32x4& tot, uint32_t szw, const float* sx4p) {
   const float s = half_bits_to_float(szw & 0xffffu);
-  const float c = 128.0f + half_bits_to_float(szw >> 16);
+  const float c = Fmt<F16>::kOffset + half_bits_to_float(szw >> 16);
   const f32x4 sx = *reinterpret_cast<const f32x4*>(sx4p);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -162,13 +183,58 @@ __device__ __forceinline__ void load_chunk(uint32_t (&w)[2][BITS], uint32_t (&s)
   }
 }
 
-// Fill the slab: rows [nt] x columns [ks, ks+kw) of every plane, 8 columns
-// (16 bytes) per piece from src(m, k, v[PLANES]), and form the sums of each
-// group of G columns (lanes of a wave hold consecutive pieces of one row, so a
-// group is G/8 neighbouring lanes: butterfly in a fixed order).
-template <int PLANES, typename PieceFn>
-__device__ __forceinline__ void stage_slab(uint16_t* xs, float* sxs, PieceFn src, int nt, int rows,
-                                           int ks, int kw, int RS, int G) {
+// ------------------------------------------------------------------ slabs --
+// A slab holds columns [ks, ks + kw) of the nt token rows (row stride RS =
+// slab width + kRowPad elements; a zero row follows for padding tokens) and
+// the sums of each group of G columns, sxs[group][rows].
+
+// Rows that are plain copies of global memory (x; h when the gate/up reduction
+// was not split), row m starting at row_src(m): direct-to-LDS 16-byte loads,
+// 64 consecutive pieces of a row per wave instruction, so every wave has all
+// its loads in flight at once.  With SUMS each wave then forms the group sums
+// of its own row segments (a segment is 512 columns, a whole number of groups;
+// the G/8 lanes of a group add in a fixed butterfly order); otherwise the sums
+// are read from sum_src(m, g) for the slab's groups g.
+template <bool F16, bool SUMS, typename RowFn, typename SumFn>
+__device__ __forceinline__ void stage_rows(uint16_t* xs, float* sxs, RowFn row_src, SumFn sum_src,
+                                           int nt, int rows, int ks, int kw, int RS, int G) {
+  const int lane = threadIdx.x & 63, wave = wave_id(), nwaves = blockDim.x >> 6;
+  const int pieces = kw >> 3;
+  const int segs = (pieces + 63) >> 6;
+  const int nseg = nt * segs;
+  for (int s = wave; s < nseg; s += nwaves) {
+    const int m = s / segs, sg = s - m * segs;
+    const int p = sg * 64 + lane;
+    if (p < pieces) lds_dma16(row_src(m) + ks + 8 * p, xs + (size_t)m * RS + sg * 512);
+  }
+  if constexpr (!SUMS) {
+    const int ngs = kw / G;
+    for (int i = threadIdx.x; i < nt * ngs; i += blockDim.x) {
+      const int m = i / ngs, g = i - m * ngs;
+      sxs[g * rows + m] = sum_src(m, g);
+    }
+  }
+  wait_vmcnt<0>();
+  asm volatile("" ::: "memory");
+  if constexpr (SUMS) {
+    const int gp = G >> 3;
+    for (int s = wave; s < nseg; s += nwaves) {
+      const int m = s / segs, sg = s - m * segs;
+      const int p = sg * 64 + lane;
+      float sum = 0.0f;
+      if (p < pieces) sum = sum8<F16>(*reinterpret_cast<const u32x4*>(xs + (size_t)m * RS + 8 * p));
+      for (int off = 1; off < gp; off <<= 1) sum += __shfl_xor(sum, off);
+      if (p < pieces && (p % gp) == 0) sxs[(p / gp) * rows + m] = sum;
+    }
+  }
+  __syncthreads();
+}
+
+// Rows computed piece by piece (8 columns, 16 bytes) by src(m, k); the group
+// sums are those of the computed values.
+template <bool F16, typename PieceFn>
+__device__ __forceinline__ void stage_pieces(uint16_t* xs, float* sxs, PieceFn src, int nt, int rows,
+                                             int ks, int kw, int RS, int G) {
   const int lane = threadIdx.x & 63;
   const int pieces = kw >> 3;
   const int total = nt * pieces;
@@ -181,13 +247,9 @@ __device__ __forceinline__ void stage_slab(uint16_t* xs, float* sxs, PieceFn src
     if (valid) {
       m = idx / pieces;
       p = idx - m * pieces;
-      u32x4 v[PLANES];
-      src(m, ks + 8 * p, v);
-#pragma unroll
-      for (int pl = 0; pl < PLANES; ++pl) {
-        *reinterpret_cast<u32x4*>(xs + (size_t)(pl * nt + m) * RS + 8 * p) = v[pl];
-        sum += sum8_bf16(v[pl]);
-      }
+      const u32x4 v = src(m, ks + 8 * p);
+      *reinterpret_cast<u32x4*>(xs + (size_t)m * RS + 8 * p) = v;
+      sum = sum8<F16>(v);
     }
     for (int off = 1; off < gp; off <<= 1) sum += __shfl_xor(sum, off);
     if (valid && (p % gp) == 0) sxs[(p / gp) * rows + m] = sum;
@@ -195,27 +257,23 @@ __device__ __forceinline__ void stage_slab(uint16_t* xs, float* sxs, PieceFn src
   __syncthreads();
 }
 
-template <int BITS, int NT, int PLANES, int GPC>
+template <int BITS, int NT, int GPC, bool F16>
 __device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
                                               const uint32_t (&s)[2][GPC], f32x4 (&acc)[2][NT],
-                                              f32x4 (&tot)[2][NT],
-                                              const uint16_t* const (&arow)[NT][PLANES],
+                                              f32x4 (&tot)[2][NT], const uint16_t* const (&arow)[NT],
                                               const float* sxs, int lc, int lane, uint32_t magic) {
   constexpr int SPG = 4 / GPC;   // MFMA steps per quantization group
   constexpr int rows = 16 * NT;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const bf16x8 b0 = b_operand<BITS>(w[0], u, magic);
-    const bf16x8 b1 = b_operand<BITS>(w[1], u, magic);
+    const u32x4 b0 = b_operand<BITS>(w[0], u, magic);
+    const u32x4 b1 = b_operand<BITS>(w[1], u, magic);
     const int kk = lc * kTileCols + 32 * u;
 #pragma unroll
     for (int tb = 0; tb < NT; ++tb) {
-#pragma unroll
-      for (int pl = 0; pl < PLANES; ++pl) {
-        const bf16x8 a = load_a(arow[tb][pl] + kk);
-        acc[0][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b0, acc[0][tb], 0, 0, 0);
-        acc[1][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b1, acc[1][tb], 0, 0, 0);
-      }
+      const u32x4 a = *reinterpret_cast<const u32x4*>(arow[tb] + kk);
+      acc[0][tb] = mfma16<F16>(a, b0, acc[0][tb]);
+      acc[1][tb] = mfma16<F16>(a, b1, acc[1][tb]);
     }
     if ((u + 1) % SPG == 0) {
       const int q = (u + 1) / SPG - 1;
@@ -223,8 +281,8 @@ __device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
 #pragma unroll
       for (int tb = 0; tb < NT; ++tb) {
         const float* sxp = sxs + gl * rows + tb * 16 + 4 * (lane >> 4);
-        group_end(acc[0][tb], tot[0][tb], s[0][q], sxp);
-        group_end(acc[1][tb], tot[1][tb], s[1][q], sxp);
+        group_end<F16>(acc[0][tb], tot[0][tb], s[0][q], sxp);
+        group_end<F16>(acc[1][tb], tot[1][tb], s[1][q], sxp);
       }
     }
   }
@@ -233,16 +291,16 @@ __device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
 // Stream chunks [c_begin, c_end) of two weight streams against the staged
 // activations of nt (<= 16*NT) tokens; a ring of D chunks of packed words and
 // scale/zero words stays in flight in registers across chunk and slab
-// boundaries.
-template <int BITS, int NT, int PLANES, int GPC, typename PieceFn>
+// boundaries.  stage(xs, sxs, rows, ks, kw, RS) fills a slab.
+template <int BITS, int NT, int GPC, bool F16, typename StageFn>
 __device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int c_end,
-                                            PieceFn src, int nt, int G,
+                                            StageFn stage, int nt, int G,
                                             uint16_t* xs, float* sxs, int xs_elems,
                                             f32x4 (&tot)[2][NT]) {
-  constexpr int D = prefetch_depth(NT, GPC, PLANES);
+  constexpr int D = prefetch_depth(NT, GPC);
   constexpr int rows = 16 * NT;
   const int lane = threadIdx.x & 63;
-  int ks = xs_elems / (PLANES * nt + 1) - kRowPad;   // + one zero row for padding tokens
+  int ks = xs_elems / (nt + 1) - kRowPad;   // + one zero row for padding tokens
   const int ks_sx = (kSxBytes / (4 * rows)) * G;
   ks = ks < ks_sx ? ks : ks_sx;
   const int unit = D * kTileCols;
@@ -266,38 +324,33 @@ __device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int 
   for (int j = 0; j < D; ++j) load_chunk<BITS, GPC>(wr[j], sr[j], sp, j, last);
 
   // zero row after the staged rows; lanes of tokens >= nt read it
-  uint16_t* zrow = xs + (size_t)PLANES * nt * RS;
+  uint16_t* zrow = xs + (size_t)nt * RS;
   for (int i = threadIdx.x; i < RS / 8; i += blockDim.x)
     *reinterpret_cast<u32x4*>(zrow + 8 * i) = u32x4{0u, 0u, 0u, 0u};
-  const uint16_t* arow[NT][PLANES];
+  const uint16_t* arow[NT];
 #pragma unroll
   for (int tb = 0; tb < NT; ++tb) {
     const int m = tb * 16 + (lane & 15);
-#pragma unroll
-    for (int pl = 0; pl < PLANES; ++pl)
-      arow[tb][pl] = (m < nt ? xs + (size_t)(pl * nt + m) * RS : zrow) + 8 * (lane >> 4);
+    arow[tb] = (m < nt ? xs + (size_t)m * RS : zrow) + 8 * (lane >> 4);
   }
-  const uint32_t magic = vgpr_constant(kMagic2);
+  const uint32_t magic = vgpr_constant(Fmt<F16>::kMagic2);
 
   for (int c0 = c_begin; c0 < c_end; c0 += slab_chunks) {
     const int c1 = (c0 + slab_chunks) < c_end ? (c0 + slab_chunks) : c_end;
     __syncthreads();
-    stage_slab<PLANES>(xs, sxs, src, nt, rows, c0 * kTileCols, (c1 - c0) * kTileCols, RS, G);
+    stage(xs, sxs, rows, c0 * kTileCols, (c1 - c0) * kTileCols, RS);
     int c = c0;
     for (; c + D <= c1; c += D) {
 #pragma unroll
       for (int j = 0; j < D; ++j) {
-        compute_chunk<BITS, NT, PLANES, GPC>(wr[j], sr[j], acc, tot, arow, sxs, c + j - c0, lane,
-                                             magic);
+        compute_chunk<BITS, NT, GPC, F16>(wr[j], sr[j], acc, tot, arow, sxs, c + j - c0, lane, magic);
         load_chunk<BITS, GPC>(wr[j], sr[j], sp, c + j + D - c_begin, last);
       }
     }
 #pragma unroll
     for (int j = 0; j < D; ++j) {        // remainder of the last slab
-      if (c + j < c1) {
-        compute_chunk<BITS, NT, PLANES, GPC>(wr[j], sr[j], acc, tot, arow, sxs, c + j - c0, lane,
-                                             magic);
-      }
+      if (c + j < c1)
+        compute_chunk<BITS, NT, GPC, F16>(wr[j], sr[j], acc, tot, arow, sxs, c + j - c0, lane, magic);
     }
   }
 }
@@ -306,8 +359,8 @@ __device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int 
 // fixed at compile time (no token-block branches inside the loop).  NTMAX is
 // the largest block count a launch can see; tot[st][tb] for blocks beyond the
 // workgroup's count are left as they were.
-template <int BITS, int GPC, int PLANES, int NTMAX, typename PieceFn>
-__device__ __forceinline__ void run_width(const Streams& sp, int c_begin, int c_end, PieceFn src,
+template <int BITS, int GPC, int NTMAX, bool F16, typename StageFn>
+__device__ __forceinline__ void run_width(const Streams& sp, int c_begin, int c_end, StageFn stage,
                                           int nt, int G, uint16_t* xs, float* sxs, int xs_elems,
                                           f32x4 (&tot)[2][NTMAX]) {
   const int ntb = (nt + 15) >> 4;
@@ -315,7 +368,7 @@ __device__ __forceinline__ void run_width(const Streams& sp, int c_begin, int c_
     f32x4 t[2][1];
     t[0][0] = tot[0][0];
     t[1][0] = tot[1][0];
-    stream_pair<BITS, 1, PLANES, GPC>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, t);
+    stream_pair<BITS, 1, GPC, F16>(sp, c_begin, c_end, stage, nt, G, xs, sxs, xs_elems, t);
     tot[0][0] = t[0][0];
     tot[1][0] = t[1][0];
   } else if (NTMAX == 2 || ntb == 2) {
@@ -325,23 +378,24 @@ __device__ __forceinline__ void run_width(const Streams& sp, int c_begin, int c_
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int b = 0; b < N; ++b) t[j][b] = tot[j][b];
-    stream_pair<BITS, N, PLANES, GPC>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, t);
+    stream_pair<BITS, N, GPC, F16>(sp, c_begin, c_end, stage, nt, G, xs, sxs, xs_elems, t);
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int b = 0; b < N; ++b) tot[j][b] = t[j][b];
   } else {
-    stream_pair<BITS, NTMAX, PLANES, GPC>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, tot);
+    stream_pair<BITS, NTMAX, GPC, F16>(sp, c_begin, c_end, stage, nt, G, xs, sxs, xs_elems, tot);
   }
 }
 
 // Launchers (one translation unit per kernel and group size).
-// Hidden activations between the two kernels: bf16 hi/lo planes, or (small
-// batches, gate/up split over d) fp32 partial sums of gate and up per split.
+// Hidden activations between the two kernels: h = fp16(silu(gate) * up), or
+// (small batches, gate/up split over d) fp32 partial sums of gate and up per
+// split.
 struct Hidden {
-  uint16_t* h_hi;        // [P][ffn]
-  size_t plane;          // elements per plane (h_lo = h_hi + plane)
+  uint16_t* h;           // [P][ffn] fp16
   float* gu_part;        // [ksplit][2][P][ffn] when ksplit > 1
+  int P;                 // T * k
   int ksplit;
 };
 

@@ -9,16 +9,16 @@
 namespace mc {
 
 // Per-width dispatch: the expert's width is uniform in a workgroup.
-template <int GPC, int PLANES, int NTMAX, typename PieceFn>
+template <int GPC, int NTMAX, bool F16, typename StageFn>
 __device__ __forceinline__ void run_expert(int bits, const Streams& sp, int c_begin, int c_end,
-                                           PieceFn src, int nt, int G, uint16_t* xs, float* sxs,
+                                           StageFn stage, int nt, int G, uint16_t* xs, float* sxs,
                                            int xs_elems, f32x4 (&tot)[2][NTMAX]) {
   if (bits == 1)
-    run_width<1, GPC, PLANES, NTMAX>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, tot);
+    run_width<1, GPC, NTMAX, F16>(sp, c_begin, c_end, stage, nt, G, xs, sxs, xs_elems, tot);
   else if (bits == 2)
-    run_width<2, GPC, PLANES, NTMAX>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, tot);
+    run_width<2, GPC, NTMAX, F16>(sp, c_begin, c_end, stage, nt, G, xs, sxs, xs_elems, tot);
   else
-    run_width<3, GPC, PLANES, NTMAX>(sp, c_begin, c_end, src, nt, G, xs, sxs, xs_elems, tot);
+    run_width<3, GPC, NTMAX, F16>(sp, c_begin, c_end, stage, nt, G, xs, sxs, xs_elems, tot);
 }
 
 // Buffer resources of one stream: row block rb of matrix m of expert e,
@@ -41,9 +41,9 @@ __device__ __forceinline__ void zero_tot(f32x4* t, int n) {
 // ---------------------------------------------------------------- gate/up --
 // Workgroup: expert e, 16*kWavesPerWg rows (one 16-row block per wave) of
 // gate and up, up to 16*NTMAX of the expert's tokens, one of ksplit ranges of
-// the d reduction.  ksplit == 1 writes h = silu(gate x) * (up x) as bf16
-// hi/lo planes; ksplit > 1 writes the fp32 partial sums of gate and up, which
-// the down kernel adds up (in split order) before the SiLU.
+// the d reduction.  ksplit == 1 writes h = fp16(silu(gate x) * (up x));
+// ksplit > 1 writes the fp32 partial sums of gate and up, which the down
+// kernel adds up (in split order) before the SiLU.
 // Up to 32 tokens per workgroup the kernels are held to 128 registers so that
 // two workgroups (16 waves) share a CU.
 template <int GPC, int NTMAX>
@@ -78,28 +78,34 @@ __attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2))) gateup_kernel(
     for (int m = 0; m < 2; ++m) stream_rsrc(L, e, m, rb, K, c_begin, c_end, sp.w[m], sp.s[m]);
     sp.lane_w = (uint32_t)lane * b * 4u;
     sp.lane_s = (uint32_t)(lane & 15) * 4u;
-    auto src = [&](int m, int k, u32x4 (&v)[1]) {
-      v[0] = *reinterpret_cast<const u32x4*>(x + (size_t)toks[m] * K + k);
+    auto stage = [&](uint16_t* xs_, float* sxs_, int rows, int ks, int kw, int RS) {
+      stage_rows<false, true>(
+          xs_, sxs_, [&](int m) { return x + (size_t)toks[m] * K; },
+          [](int, int) { return 0.0f; }, nt, rows, ks, kw, RS, G);
     };
-    run_expert<GPC, 1, NTMAX>(b, sp, c_begin, c_end, src, nt, G, xs, sxs, xs_bytes / 2, tot);
+    run_expert<GPC, NTMAX, false>(b, sp, c_begin, c_end, stage, nt, G, xs, sxs, xs_bytes / 2, tot);
   }
   const int n = rb * 16 + (lane & 15);
-  const size_t P = hid.plane / L.ffn;
+  const size_t P = hid.P;
+  if (hid.ksplit == 1) {
 #pragma unroll
-  for (int tb = 0; tb < NTMAX; ++tb) {
+    for (int tb = 0; tb < NTMAX; ++tb) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = tb * 16 + 4 * (lane >> 4) + i;
-      if (m < nt) {
-        const size_t o = (size_t)(pbase + m) * L.ffn + n;
-        if (hid.ksplit == 1) {
-          const float h = silu(tot[0][tb][i]) * tot[1][tb][i];
-          const uint16_t hi = float_to_bf16(h);
-          const uint16_t lo = float_to_bf16(h - bf16_bits_to_float(hi));
-          hid.h_hi[o] = hi;
-          hid.h_hi[hid.plane + o] = lo;
-        } else {
-          float* part = hid.gu_part + (size_t)split * 2 * P * L.ffn;
+      for (int i = 0; i < 4; ++i) {
+        const int m = tb * 16 + 4 * (lane >> 4) + i;
+        if (m < nt)
+          hid.h[(size_t)(pbase + m) * L.ffn + n] = float_to_half_sat(silu(tot[0][tb][i]) * tot[1][tb][i]);
+      }
+    }
+  } else {
+    float* part = hid.gu_part + (size_t)split * 2 * P * L.ffn;
+#pragma unroll
+    for (int tb = 0; tb < NTMAX; ++tb) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = tb * 16 + 4 * (lane >> 4) + i;
+        if (m < nt) {
+          const size_t o = (size_t)(pbase + m) * L.ffn + n;
           part[o] = tot[0][tb][i];
           part[P * L.ffn + o] = tot[1][tb][i];
         }
@@ -147,17 +153,17 @@ __attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2))) down_kernel(
     sp.lane_w = (uint32_t)lane * b * 4u;
     sp.lane_s = (uint32_t)(lane & 15) * 4u;
     if (hid.ksplit == 1) {
-      auto src = [&](int m, int k, u32x4 (&v)[2]) {
-        const uint16_t* row = hid.h_hi + (size_t)(pbase + m) * K + k;
-        v[0] = *reinterpret_cast<const u32x4*>(row);
-        v[1] = *reinterpret_cast<const u32x4*>(row + hid.plane);
+      auto stage = [&](uint16_t* xs_, float* sxs_, int rows, int ks, int kw, int RS) {
+        stage_rows<true, true>(
+            xs_, sxs_, [&](int m) { return hid.h + (size_t)(pbase + m) * K; },
+            [](int, int) { return 0.0f; }, nt, rows, ks, kw, RS, G);
       };
-      run_expert<GPC, 2, NTMAX>(b, sp, c_begin, c_end, src, nt, G, xs, sxs, xs_bytes / 2, tot);
+      run_expert<GPC, NTMAX, true>(b, sp, c_begin, c_end, stage, nt, G, xs, sxs, xs_bytes / 2, tot);
     } else {
-      // h from the gate/up partial sums (added in split order), as the
-      // ksplit == 1 gate/up epilogue would have formed it
-      const size_t P = hid.plane / K;
-      auto src = [&](int m, int k, u32x4 (&v)[2]) {
+      // h from the gate/up partial sums (added in split order), rounded to
+      // fp16 as the ksplit == 1 gate/up epilogue would have formed it
+      const size_t P = hid.P;
+      auto piece = [&](int m, int k) {
         const size_t o = (size_t)(pbase + m) * K + k;
         f32x4 g0 = {0.f, 0.f, 0.f, 0.f}, g1 = g0, u0 = g0, u1 = g0;
         for (int s = 0; s < hid.ksplit; ++s) {
@@ -167,22 +173,20 @@ __attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2))) down_kernel(
           u0 += *reinterpret_cast<const f32x4*>(part + P * K);
           u1 += *reinterpret_cast<const f32x4*>(part + P * K + 4);
         }
-        uint32_t hi[4], lo[4];
+        u32x4 v;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const float ha = silu(j < 2 ? g0[2 * j] : g1[2 * j - 4]) * (j < 2 ? u0[2 * j] : u1[2 * j - 4]);
           const float hb = silu(j < 2 ? g0[2 * j + 1] : g1[2 * j - 3]) *
                            (j < 2 ? u0[2 * j + 1] : u1[2 * j - 3]);
-          const uint16_t ahi = float_to_bf16(ha), bhi = float_to_bf16(hb);
-          const uint16_t alo = float_to_bf16(ha - bf16_bits_to_float(ahi));
-          const uint16_t blo = float_to_bf16(hb - bf16_bits_to_float(bhi));
-          hi[j] = (uint32_t)ahi | ((uint32_t)bhi << 16);
-          lo[j] = (uint32_t)alo | ((uint32_t)blo << 16);
+          v[j] = (uint32_t)float_to_half_sat(ha) | ((uint32_t)float_to_half_sat(hb) << 16);
         }
-        v[0] = u32x4{hi[0], hi[1], hi[2], hi[3]};
-        v[1] = u32x4{lo[0], lo[1], lo[2], lo[3]};
+        return v;
       };
-      run_expert<GPC, 2, NTMAX>(b, sp, c_begin, c_end, src, nt, G, xs, sxs, xs_bytes / 2, tot);
+      auto stage = [&](uint16_t* xs_, float* sxs_, int rows, int ks, int kw, int RS) {
+        stage_pieces<true>(xs_, sxs_, piece, nt, rows, ks, kw, RS, G);
+      };
+      run_expert<GPC, NTMAX, true>(b, sp, c_begin, c_end, stage, nt, G, xs, sxs, xs_bytes / 2, tot);
     }
   }
 #pragma unroll

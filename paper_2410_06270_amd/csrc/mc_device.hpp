@@ -11,6 +11,7 @@
 namespace mc {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 
@@ -67,6 +68,23 @@ __device__ __forceinline__ uint16_t double_to_half_rne(double v) {
   uint16_t r;
   __builtin_memcpy(&r, &h, 2);
   return r;
+}
+
+// ------------------------------------------------------- memory helpers --
+
+// s_waitcnt vmcnt(n) (expcnt and lgkmcnt left alone).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Direct-to-LDS 16-byte load: lane l reads 16 bytes at src (its own address)
+// and the wave writes them to dst + 16*l (dst is wave-uniform).  Counted by
+// vmcnt; lanes outside EXEC neither read nor write.
+__device__ __forceinline__ void lds_dma16(const void* src, void* dst) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                   (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
 }
 
 // ------------------------------------------------------------------ layout --

@@ -35,7 +35,6 @@
 
 namespace mc {
 
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8e __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
@@ -45,7 +44,6 @@ constexpr int kPfWaves = 8;
 constexpr int kPfWaveTiles = 2;                    // fragment rows per wave (64 tokens)
 constexpr int kPfWtok = 2;                         // token groups per workgroup
 constexpr int kPfSlots = 4;                        // LDS ring: chunks c-1 .. c+2
-constexpr uint32_t kMagicF16 = 0x64006400u;        // fp16 1024.0 in both halves
 
 template <int WTOK>
 struct PfShape {
@@ -148,18 +146,6 @@ __device__ __forceinline__ f32x16 pf_mfma(u32x4 a, u32x4 b, f32x16 c) {
   else
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
-}
-
-// s_waitcnt vmcnt(n) (expcnt and lgkmcnt left alone).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-__device__ __forceinline__ void lds_dma16(const void* src, unsigned char* dst) {
-  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                   (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
 }
 
 // Stage chunk c straight into LDS: the A fragments of all kTiles fragment rows
@@ -293,7 +279,7 @@ __device__ __forceinline__ void pf_loop(const PfStream (&sp)[2], const PrefillGe
                                         int wave, int lane, f32x16 (&tot)[kPfWaveTiles][2]) {
   using S = PfShape<WTOK>;
   if (c_begin >= c_end) return;
-  const uint32_t magic = vgpr_constant(BF16 ? kMagic2 : kMagicF16);
+  const uint32_t magic = vgpr_constant(Fmt<!BF16>::kMagic2);
   const int last = c_end - 1;
   uint32_t wa[2][2][BITS], sa[2][GPC], wb[2][2][BITS], sb[2][GPC], ps[2] = {0u, 0u};
   f32x16 acc[kPfWaveTiles][2];
