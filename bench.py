@@ -50,6 +50,8 @@ def parse():
     p.add_argument("--no-prefill", action="store_true", help="skip the 4096-token prefill sweep")
     p.add_argument("--no-olmoe", action="store_true", help="skip the OLMoE-shaped layer")
     p.add_argument("--no-importance", action="store_true", help="skip the token-importance measurement")
+    p.add_argument("--no-stack", action="store_true", help="skip the 32-layer stack")
+    p.add_argument("--stack-steps", type=int, default=10)
     p.add_argument("--graph", action="store_true",
                    help="also time HIP-graph replays of the step (reported as ms_per_step_graph)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -322,6 +324,77 @@ def importance_entry(mc, torch, steps, warmup):
                 kernels_us={k: round(v, 2) for k, v in kus.items()})
 
 
+def stack_entry(mc, torch, synthetic, steps, warmup):
+    """The 32-layer Mixtral-shaped expert stack resident in HBM: 32 packed
+    layers (widths [3,3,3,2,2,2,2,3] in a seeded order per layer, weights
+    N(0, 0.02^2) drawn on the device with a seeded torch generator), each
+    layer routed from its own logits (N(0,1) + per-layer expert bias
+    N(0, 0.5^2)) with 10 % protected tokens and tau = 0.3, each behind an
+    RMSNorm and joined by residual connections (no attention).  One step =
+    one mc_moe_stack_forward over all 32 layers.  Algorithmic bytes: packed
+    bytes of every expert a layer routes at least one token to, plus per layer
+    the bf16 activations read (norm input, expert input, residual) and written
+    (normalised input, output) and the logits."""
+    import numpy as np
+    c = synthetic.config(5)
+    E, d, ffn, k, G, n, tau = c["E"], c["d"], c["ffn"], c["k"], c["G"], c["layers"], c["tau"][0]
+    layers, bits = [], []
+    for l in range(n):
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(synthetic.BASE_SEED + 5 + 1000 * l)
+        w = [torch.randn((E, ffn, d) if m < 2 else (E, d, ffn), generator=gen, device="cuda",
+                         dtype=torch.float32).mul_(0.02) for m in range(3)]
+        b = synthetic.stack_bits(5, l)
+        L = mc.PackedLayer(E, d, ffn, b, G)
+        mc.pack(w[0], w[1], w[2], L)
+        del w
+        layers.append(L)
+        bits.append(b)
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    resident = sum(L.nbytes for L in layers)
+    runs = []
+    for T in c["T"]:
+        lg = torch.from_numpy(np.stack([synthetic.stack_logits(5, l, T) for l in range(n)])).cuda()
+        mk = torch.from_numpy(np.stack([synthetic.stack_mask(5, l, T) for l in range(n)])).cuda()
+        x = torch.from_numpy(synthetic.activations(5, T).view("int16")).cuda()
+        r = mc.Routing(T, E, k)
+        y = torch.empty((T, d), dtype=torch.int16, device="cuda")
+        tmp = torch.empty_like(y)
+        ws = torch.empty(mc.stack_workspace(T, E, k, d, ffn), dtype=torch.uint8, device="cuda")
+        wbytes, kept = 0, 0
+        for l in range(n):                      # the library's routing, to count what each layer touches
+            mc.route_and_prune(lg[l], mk[l], tau, r)
+            counts = r.counts.cpu().tolist()
+            wbytes += sum(expert_bytes(d, ffn, G, bits[l][e]) for e in range(E) if counts[e] > 0)
+            kept += sum(counts)
+        act = n * (5 * T * d * 2 + T * E * 4)
+        run = lambda: mc.stack_forward(x, layers, lg, mk, tau, r, y, tmp, ws)
+        for _ in range(warmup):
+            run()
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(steps):
+            run()
+        ev1.record()
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / steps
+        flops = 6 * d * ffn * kept
+        runs.append(dict(tokens=T, path="decode" if T <= 64 else "prefill", ms_per_step=round(ms, 4),
+                         tokens_per_s=round(T / (ms / 1e3), 1),
+                         alg_bytes=wbytes + act, hbm_gbs=round((wbytes + act) / (ms * 1e6), 1),
+                         hbm_frac=round((wbytes + act) / (ms * 1e6) / HBM_PEAK_GBS, 4),
+                         pairs_kept=kept, pruned_frac=round(1 - kept / (n * T * k), 4),
+                         tflops=round(flops / (ms * 1e9), 1),
+                         mfma_frac=round(flops / (ms * 1e9) / MFMA_PEAK_TFLOPS, 4)))
+        del lg, mk, x, r, y, tmp, ws
+    del layers
+    torch.cuda.empty_cache()
+    return dict(workload="mixtral_8x7b_moe_stack", layers=n, d=d, ffn=ffn, experts=E, top_k=k,
+                group=G, tau=tau, resident_bytes=resident, steps=steps, runs=runs)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -434,6 +507,8 @@ def main():
                         "decode": dec, "prefill": prefill_entry(wo, ms_p, kus)}
     if not args.no_importance:
         out["importance"] = importance_entry(mc, torch, 20, 3)
+    if not args.no_stack:
+        out["stack"] = stack_entry(mc, torch, synthetic, args.stack_steps, 2)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(synthetic, T)
     print(json.dumps(out), flush=True)

@@ -12,6 +12,7 @@
  *   mc_route_and_prune router logits -> top-k, Eq. 5 pruning, protection,
  *                      per-expert token lists (CSR)
  *   mc_moe_forward     Eq. 1 over the packed SwiGLU experts
+ *   mc_moe_stack_forward  a stack of MoE layers with residual connections
  *
  * Conventions for every call
  *   - Pointers are DEVICE pointers unless the comment says "host".
@@ -156,6 +157,36 @@ mc_status mc_moe_forward(const uint16_t *x_bf16, const mc_routing *r,
                          const mc_layer *L, uint16_t *y_bf16, void *workspace,
                          size_t ws_bytes, void *stream);
 
+/* Workspace bytes mc_moe_stack_forward needs: the normalised layer input
+ * (T*d bf16, rounded up to 256 bytes) + mc_forward_workspace.
+ * Errors: MC_EINVAL. */
+mc_status mc_stack_workspace(int T, int E, int k, int d, int ffn, size_t *bytes);
+
+/* A stack of n_layers MoE layers joined by residual connections: the expert
+ * half of Mixtral-style decoder blocks, each with its pre-MoE RMSNorm (unit
+ * gain, eps = 1e-5); attention is not part of this library.
+ *   h_0 = x;  for l = 0 .. n_layers-1:
+ *     xn_l    = bf16(h_l / sqrt(mean_j h_l[j]^2 + 1e-5))   (per token; the
+ *               sum of squares and the quotient in fp64, one rounding),
+ *     route layer l's logits (as mc_route_and_prune, same threshold),
+ *     h_{l+1} = bf16(h_l + sum_r w_r * E_{e_r}(xn_l))   (Eq. 1 + residual,
+ *               the sum in fp32, one round-to-nearest-even);
+ *   y = h_{n_layers}.
+ * layers: HOST array [n_layers] of descriptors sharing E, d, ffn and group
+ * (each layer has its own widths and buffers).  logits: [n_layers][T][E]
+ * fp32; important: [n_layers][T] uint8 or NULL.  r: routing buffers for T
+ * tokens (k taken from it), reused by every layer; after the call it holds
+ * the last layer's routing.  x, y, tmp: [T][d] bf16, three distinct,
+ * non-overlapping buffers (tmp holds every other layer's output; it may be
+ * NULL when n_layers == 1).  workspace: ws_bytes >= mc_stack_workspace(T, E,
+ * k, d, ffn), reused by every layer.  Everything runs in order on `stream`.
+ * Errors: MC_EINVAL (shape mismatch between layers, null or overlapping
+ * buffers, tau outside [0, 1]), MC_ENOSPACE, MC_EHIP. */
+mc_status mc_moe_stack_forward(const uint16_t *x_bf16, int n_layers, const mc_layer *layers,
+                               const float *logits, const uint8_t *important, float threshold,
+                               const mc_routing *r, uint16_t *y_bf16, uint16_t *tmp_bf16,
+                               void *workspace, size_t ws_bytes, void *stream);
+
 /* Workspace bytes mc_token_importance needs for H heads and L tokens: fp32
  * partial sums, 512 B per 128x128 tile of the lower triangle and slice of
  * heads (about 2 MB up to 8192 tokens, 67 MB at 65,536), plus 12 B per token.
@@ -193,7 +224,7 @@ mc_status mc_odp_threshold(const float *logits_host, int T, int E, double *mu, d
  * events of one kernel and returns the summed duration in ms and the number
  * of launches.  Kernel names: pack_scale_zero, pack_codes, export,
  * route_fused, route_select, route_lists, prefill_prep, gateup, down, combine,
- * importance_colsum, importance_finish, importance_select.
+ * importance_colsum, importance_finish, importance_select, rmsnorm.
  * Errors: MC_EINVAL (unknown name, NULL pointer), MC_EHIP. */
 mc_status mc_timing_enable(int on);
 mc_status mc_timing_read(const char *kernel, double *total_ms, int *launches);

@@ -15,6 +15,9 @@ What it computes (Mixture Compressor for MoE LLMs, ICLR 2025):
 * ``route``         -- Eq. 1 top-k, Eq. 5 pruning, Sec. 3.3.2 protection and
   the per-expert token lists;
 * ``moe_forward``   -- Eq. 1 over SwiGLU experts on exact dequantized weights;
+* ``rms_norm`` / ``moe_stack`` -- layers of Eq. 1, each behind an RMSNorm,
+  joined by residual connections, the stream rounded to bfloat16 after each
+  layer;
 * ``token_importance`` -- Eq. 6 importance from causal attention probabilities
   and the protected set (the top floor(rho*L + 1/2) tokens);
 * ``median_ratio``  -- the pruning threshold mu as the median of w1/w0.
@@ -47,6 +50,9 @@ PINS = {
     "dequant_f16": "Fraction value rounded by numpy float16 (library RNE)",
     "route": "naive stable sort; tau=0 and protected no-op; k=2 gap == ratio rule",
     "moe_forward": "E=1,k=1 equals numpy SwiGLU; tau=0 all-protected dense top-k; linearity",
+    "rms_norm": "torch.nn.functional.rms_norm in float64; scale invariance; unit mean square",
+    "moe_stack": "numpy residual SwiGLU stack at E=1,k=1; zero experts are the identity; "
+                 "tokens are independent (a subset matches the full run)",
     "token_importance": "diagonal / first-token closed forms; hand example; head linearity; "
                         "brute-force selection; upper triangle ignored",
     "median_ratio": "statistics.median of exp(l1 - l0) over a naive sort",
@@ -342,6 +348,39 @@ def moe_forward(x_bf16: np.ndarray, routing, logical, G: int, rows=None, tokens=
         for i, (t, r) in enumerate(sel):
             Y[tpos[t]] += routing["topk_w"][t, r] * Ye[i]
     return Y
+
+
+RMS_EPS = 1e-5
+
+
+def rms_norm(h_bf16: np.ndarray, eps: float = RMS_EPS) -> np.ndarray:
+    """Per row: bf16(h / sqrt(mean(h^2) + eps)) (unit gain), the value formed
+    in fp64 and rounded once; returns bf16 bits."""
+    H = bf16_to_float64(np.asarray(h_bf16, dtype=np.uint16))
+    r = 1.0 / np.sqrt((H * H).mean(axis=1, keepdims=True) + eps)
+    return bf16_round_array(H * r)
+
+
+def moe_stack(x_bf16: np.ndarray, layers, G: int, tokens=None):
+    """Residual stack of MoE layers, each behind its RMSNorm:
+    h_0 = x, xn_l = rms_norm(h_l), h_{l+1} = RNE_bf16(h_l + y_l) with y_l =
+    Eq. 1 of layer l on xn_l (fp64, exact dequantized weights).
+    ``layers``: list of (routing, logical) with routing from ``route``.
+    ``tokens`` restricts the computation to those tokens (each token's path
+    depends only on its own row).  Returns the list of bf16 bit arrays
+    h_1 .. h_n, rows in the order of ``tokens`` (all tokens by default)."""
+    x_bf16 = np.asarray(x_bf16, dtype=np.uint16)
+    T = x_bf16.shape[0]
+    toks = np.arange(T) if tokens is None else np.asarray(tokens)
+    H = x_bf16.copy()
+    outs = []
+    for routing, logical in layers:
+        XN = H.copy()
+        XN[toks] = rms_norm(H[toks])
+        Y = moe_forward(XN, routing, logical, G, tokens=toks)
+        H[toks] = bf16_round_array(bf16_to_float64(H[toks]) + Y)
+        outs.append(H[toks].copy())
+    return outs
 
 
 # ------------------------------------------------------------- importance ---

@@ -20,6 +20,8 @@ from ._binding import (  # noqa: F401
     pack,
     pack_sizes,
     route_and_prune,
+    stack_forward,
+    stack_workspace,
     timing_enable,
     timing_read,
     token_importance,

@@ -73,6 +73,11 @@ def load():
         lib.mc_moe_forward.restype = st
         lib.mc_moe_forward.argtypes = [P, ctypes.POINTER(_Routing), ctypes.POINTER(_Layer), P, P,
                                        S, P]
+        lib.mc_stack_workspace.restype = st
+        lib.mc_stack_workspace.argtypes = [I, I, I, I, I, ctypes.POINTER(S)]
+        lib.mc_moe_stack_forward.restype = st
+        lib.mc_moe_stack_forward.argtypes = [P, I, ctypes.POINTER(_Layer), P, P, ctypes.c_float,
+                                             ctypes.POINTER(_Routing), P, P, P, S, P]
         lib.mc_importance_workspace.restype = st
         lib.mc_importance_workspace.argtypes = [I, I, ctypes.POINTER(S)]
         lib.mc_token_importance.restype = st
@@ -189,6 +194,28 @@ def moe_forward(x, routing: Routing, layer: PackedLayer, y, workspace, stream=No
     _check(load().mc_moe_forward(_ptr(x), ctypes.byref(routing.desc), ctypes.byref(layer.desc),
                                  _ptr(y), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                  _stream(stream)))
+
+
+def stack_workspace(T: int, E: int, k: int, d: int, ffn: int) -> int:
+    b = ctypes.c_size_t()
+    _check(load().mc_stack_workspace(T, E, k, d, ffn, ctypes.byref(b)))
+    return b.value
+
+
+def stack_forward(x, layers, logits, important, threshold: float, routing: Routing, y, tmp,
+                  workspace, stream=None):
+    """Residual MoE stack: y = h_n with h_{l+1} = bf16(h_l + MoE_l(RMSNorm(h_l))).
+    x, y, tmp: bf16 bits [T][d]; logits: float32 [n][T][E]; important: uint8
+    [n][T] or None; layers: list of PackedLayer sharing E, d, ffn, group."""
+    n = len(layers)
+    arr = (_Layer * n)(*[l.desc for l in layers])
+    assert logits.dtype == torch.float32 and logits.is_contiguous()
+    for t in (x, y) + (() if tmp is None else (tmp,)):
+        assert t.is_contiguous() and t.element_size() == 2
+    _check(load().mc_moe_stack_forward(_ptr(x), n, arr, _ptr(logits), _ptr(important),
+                                       float(threshold), ctypes.byref(routing.desc), _ptr(y), _ptr(tmp),
+                                       _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                       _stream(stream)))
 
 
 def importance_workspace(H: int, L: int) -> int:

@@ -144,6 +144,12 @@ mc_status mc_codes_export(const mc_layer* L, int e, int mat, uint8_t* out, void*
   return export_common(L, e, mat, out, false, stream);
 }
 
+static float prune_delta32(double tau) {
+  if (tau == 0.0) return INFINITY;
+  if (tau == 1.0) return -INFINITY;
+  return (float)std::log((1.0 - tau) / tau);
+}
+
 mc_status mc_route_and_prune(const float* logits, const uint8_t* important, float threshold,
                              const mc_routing* r, void* stream) {
   mc_status s = check_routing(r);
@@ -152,12 +158,8 @@ mc_status mc_route_and_prune(const float* logits, const uint8_t* important, floa
   if (!(threshold >= 0.0f && threshold <= 1.0f))
     return fail(MC_EINVAL, "threshold %g outside [0, 1]", (double)threshold);
   const double tau = (double)threshold;
-  float delta32;
-  if (tau == 0.0) delta32 = INFINITY;
-  else if (tau == 1.0) delta32 = -INFINITY;
-  else delta32 = (float)std::log((1.0 - tau) / tau);
   (void)hipGetLastError();
-  return hip_status(mc::launch_route(logits, important, delta32, tau, *r,
+  return hip_status(mc::launch_route(logits, important, prune_delta32(tau), tau, *r,
                                      static_cast<hipStream_t>(stream)),
                     "mc_route_and_prune launch");
 }
@@ -184,9 +186,76 @@ mc_status mc_moe_forward(const uint16_t* x_bf16, const mc_routing* r, const mc_l
   if (ws_bytes < need) return fail(MC_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
   (void)hipGetLastError();
   const mc::LayerArgs a = layer_args(L);
-  return hip_status(mc::launch_forward(x_bf16, a, *r, y_bf16, workspace,
+  return hip_status(mc::launch_forward(x_bf16, a, *r, y_bf16, workspace, nullptr,
                                        static_cast<hipStream_t>(stream)),
                     "mc_moe_forward launch");
+}
+
+mc_status mc_stack_workspace(int T, int E, int k, int d, int ffn, size_t* bytes) {
+  mc_status s = mc_forward_workspace(T, E, k, d, ffn, bytes);
+  if (s != MC_OK) return s;
+  *bytes = mc::stack_workspace_bytes(T, E, k, d, ffn);
+  return MC_OK;
+}
+
+static bool overlaps(const void* a, const void* b, size_t bytes) {
+  const char* pa = static_cast<const char*>(a);
+  const char* pb = static_cast<const char*>(b);
+  return pa < pb + bytes && pb < pa + bytes;
+}
+
+mc_status mc_moe_stack_forward(const uint16_t* x_bf16, int n_layers, const mc_layer* layers,
+                               const float* logits, const uint8_t* important, float threshold,
+                               const mc_routing* r, uint16_t* y_bf16, uint16_t* tmp_bf16,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  mc_status s = check_routing(r);
+  if (s != MC_OK) return s;
+  if (n_layers < 1) return fail(MC_EINVAL, "n_layers=%d must be >= 1", n_layers);
+  if (!layers) return fail(MC_EINVAL, "layers array is NULL");
+  for (int l = 0; l < n_layers; ++l) {
+    s = check_layer(&layers[l], true);
+    if (s != MC_OK) return s;
+    const mc_layer& a = layers[l];
+    if (a.E != layers[0].E || a.d != layers[0].d || a.ffn != layers[0].ffn || a.group != layers[0].group)
+      return fail(MC_EINVAL, "layer %d shape (E=%d d=%d ffn=%d G=%d) differs from layer 0", l, a.E, a.d,
+                  a.ffn, a.group);
+  }
+  if (r->E != layers[0].E) return fail(MC_EINVAL, "routing has E=%d, layers have E=%d", r->E, layers[0].E);
+  if (!logits) return fail(MC_EINVAL, "logits pointer is NULL");
+  if (!(threshold >= 0.0f && threshold <= 1.0f))
+    return fail(MC_EINVAL, "threshold %g outside [0, 1]", (double)threshold);
+  if (!x_bf16 || !y_bf16 || !workspace) return fail(MC_EINVAL, "x, y or workspace is NULL");
+  if (n_layers > 1 && !tmp_bf16) return fail(MC_EINVAL, "tmp is NULL with %d layers", n_layers);
+  const size_t act = (size_t)r->T * layers[0].d * sizeof(uint16_t);
+  if (overlaps(x_bf16, y_bf16, act) || (tmp_bf16 && (overlaps(x_bf16, tmp_bf16, act) ||
+                                                     overlaps(y_bf16, tmp_bf16, act))))
+    return fail(MC_EINVAL, "x, y and tmp must not overlap");
+  const size_t need = mc::stack_workspace_bytes(r->T, r->E, r->k, layers[0].d, layers[0].ffn);
+  if (ws_bytes < need) return fail(MC_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+  uint16_t* xn = static_cast<uint16_t*>(workspace);
+  void* fws = static_cast<char*>(workspace) + (need - mc::forward_workspace_bytes(r->T, r->E, r->k,
+                                                                                   layers[0].d, layers[0].ffn));
+  const double tau = (double)threshold;
+  const float delta32 = prune_delta32(tau);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  const uint16_t* in = x_bf16;
+  for (int l = 0; l < n_layers; ++l) {
+    uint16_t* out = ((n_layers - 1 - l) % 2 == 0) ? y_bf16 : tmp_bf16;
+    const size_t te = (size_t)l * r->T;
+    s = hip_status(mc::launch_rmsnorm(in, r->T, layers[0].d, mc::kRmsNormEps, xn, st),
+                   "mc_moe_stack_forward rmsnorm launch");
+    if (s != MC_OK) return s;
+    s = hip_status(mc::launch_route(logits + te * r->E, important ? important + te : nullptr, delta32,
+                                    tau, *r, st),
+                   "mc_moe_stack_forward routing launch");
+    if (s != MC_OK) return s;
+    s = hip_status(mc::launch_forward(xn, layer_args(&layers[l]), *r, out, fws, in, st),
+                   "mc_moe_stack_forward forward launch");
+    if (s != MC_OK) return s;
+    in = out;
+  }
+  return MC_OK;
 }
 
 mc_status mc_importance_workspace(int H, int L, size_t* bytes) {

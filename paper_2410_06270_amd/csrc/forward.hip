@@ -5,18 +5,27 @@
 namespace mc {
 
 // ---------------------------------------------------------------- combine --
-// y[t][i..i+3] = bf16(sum over kept ranks r, in rank order, of
-// w_r * sum over splits s, in order, of partial[s][pos(t, r)][i..i+3]).
+// y[t][i..i+3] = bf16(res[t][i..i+3] + sum over kept ranks r, in rank order,
+// of w_r * sum over splits s, in order, of partial[s][pos(t, r)][i..i+3]);
+// res is the bf16 residual input (none when null).
 template <int NSPLIT>
 __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ partial,
                                                       size_t part_stride,
                                                       const int32_t* __restrict__ pair_pos,
                                                       const float* __restrict__ topk_w, int k, int d,
+                                                      const uint16_t* __restrict__ res,
                                                       uint16_t* __restrict__ y) {
   const int t = blockIdx.y;
   const int i = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
   if (i >= d) return;
   f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (res) {
+    const uint2 rv = *reinterpret_cast<const uint2*>(res + (size_t)t * d + i);
+    acc[0] = bf16_bits_to_float(rv.x & 0xffffu);
+    acc[1] = bf16_bits_to_float(rv.x >> 16);
+    acc[2] = bf16_bits_to_float(rv.y & 0xffffu);
+    acc[3] = bf16_bits_to_float(rv.y >> 16);
+  }
   for (int r = 0; r < k; ++r) {
     const int pos = pair_pos[(size_t)t * k + r];
     if (pos < 0) continue;
@@ -35,6 +44,50 @@ __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ 
   uint32_t hi = (uint32_t)float_to_bf16(acc[2]) | ((uint32_t)float_to_bf16(acc[3]) << 16);
   *reinterpret_cast<uint2*>(y + (size_t)t * d + i) = make_uint2(lo, hi);
 }
+
+// ---------------------------------------------------------------- rmsnorm --
+// xn[t][i] = bf16(h[t][i] / sqrt(mean_j h[t][j]^2 + eps)): the sum of squares
+// in fp64 in a fixed order (lane partials, wave butterfly, waves in order),
+// the quotient in fp64, rounded once.  One workgroup per token.
+constexpr int kNormThreads = 256;
+
+__global__ void __launch_bounds__(kNormThreads) rmsnorm_kernel(const uint16_t* __restrict__ h, int d,
+                                                               double eps, uint16_t* __restrict__ xn) {
+  __shared__ double part[kNormThreads / 64];
+  const size_t base = (size_t)blockIdx.x * d;
+  double ss = 0.0;
+  for (int i = 4 * threadIdx.x; i < d; i += 4 * kNormThreads) {
+    const uint2 v = *reinterpret_cast<const uint2*>(h + base + i);
+    const double a = bf16_bits_to_float(v.x & 0xffffu), b = bf16_bits_to_float(v.x >> 16);
+    const double c = bf16_bits_to_float(v.y & 0xffffu), e = bf16_bits_to_float(v.y >> 16);
+    ss += a * a;
+    ss += b * b;
+    ss += c * c;
+    ss += e * e;
+  }
+  for (int off = 1; off < 64; off <<= 1) ss += __shfl_xor(ss, off);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  double tot = 0.0;
+  for (int w = 0; w < kNormThreads / 64; ++w) tot += part[w];
+  const double r = 1.0 / sqrt(tot / d + eps);
+  for (int i = 4 * threadIdx.x; i < d; i += 4 * kNormThreads) {
+    const uint2 v = *reinterpret_cast<const uint2*>(h + base + i);
+    const uint32_t lo = (uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.x & 0xffffu) * r) |
+                        ((uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.x >> 16) * r) << 16);
+    const uint32_t hi = (uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.y & 0xffffu) * r) |
+                        ((uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.y >> 16) * r) << 16);
+    *reinterpret_cast<uint2*>(xn + base + i) = make_uint2(lo, hi);
+  }
+}
+
+hipError_t launch_rmsnorm(const uint16_t* h, int T, int d, double eps, uint16_t* xn, hipStream_t stream) {
+  timing_begin(stream, kSiteRmsNorm);
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(T), dim3(kNormThreads), 0, stream, h, d, eps, xn);
+  timing_end(stream, kSiteRmsNorm);
+  return hipGetLastError();
+}
+
 
 // --------------------------------------------------------------- launchers --
 
@@ -81,13 +134,18 @@ size_t forward_workspace_bytes(int T, int E, int k, int d, int ffn) {
   return h + gu + part;
 }
 
+size_t stack_workspace_bytes(int T, int E, int k, int d, int ffn) {
+  return round256((size_t)T * d * sizeof(uint16_t)) + forward_workspace_bytes(T, E, k, d, ffn);
+}
+
 static hipError_t launch_combine(const float* partial, size_t part_stride, int nsplit,
-                                 const mc_routing& r, int d, uint16_t* y, hipStream_t stream) {
+                                 const mc_routing& r, int d, const uint16_t* res, uint16_t* y,
+                                 hipStream_t stream) {
   timing_begin(stream, kSiteCombine);
   const dim3 cgrid((d / 4 + 255) / 256, r.T);
 #define MC_COMBINE(S)                                                                              \
   hipLaunchKernelGGL(combine_kernel<S>, cgrid, dim3(256), 0, stream, partial, part_stride,         \
-                     r.pair_pos, r.topk_w, r.k, d, y)
+                     r.pair_pos, r.topk_w, r.k, d, res, y)
   switch (nsplit) {
     case 1: MC_COMBINE(1); break;
     case 2: MC_COMBINE(2); break;
@@ -104,7 +162,7 @@ static hipError_t launch_combine(const float* partial, size_t part_stride, int n
 }
 
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
-                          void* ws, hipStream_t stream) {
+                          void* ws, const uint16_t* residual, hipStream_t stream) {
   const int T = r.T, k = r.k;
   if (T > kDecodeMaxT) {
     float* partial = nullptr;
@@ -112,7 +170,7 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
     int nsplit = 1;
     const hipError_t err = launch_prefill(x, L, r, ws, &partial, &part_stride, &nsplit, stream);
     if (err != hipSuccess) return err;
-    return launch_combine(partial, part_stride, nsplit, r, L.d, y, stream);
+    return launch_combine(partial, part_stride, nsplit, r, L.d, residual, y, stream);
   }
   const size_t P = (size_t)T * k;
   Hidden hid;
@@ -141,7 +199,7 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
   else err = launch_down<4>(hid, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
   timing_end(stream, kSiteDown);
   if (err != hipSuccess) return err;
-  return launch_combine(partial, part_stride, nsplit, r, L.d, y, stream);
+  return launch_combine(partial, part_stride, nsplit, r, L.d, residual, y, stream);
 }
 
 }  // namespace mc

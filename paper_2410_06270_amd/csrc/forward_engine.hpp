@@ -3,13 +3,16 @@
 // y_t = sum over kept ranks r of w_r * E_{e_r}(x_t),
 // E_e(x) = W_down (silu(W_gate x) * (W_up x)), weights s*(q - z) per group.
 //
-// The codes go straight into 16-bit MFMA operands as an exact integer offset
-// by a power of two -- bf16 128 + q against the bf16 activations x (gate, up),
-// fp16 1024 + q against the fp16 hidden vector h (down) -- so the dequantized
-// weight is never rounded: for each group g of G inputs a_k
-//   sum_k s (q_k - z) a_k = s * (acc_g - (o + z) * sum_k a_k),
-// acc_g = sum_k (o + q_k) a_k from the MFMA, o the offset.  The group sums of
-// the activations (of the fp16 values, for h) are formed while they are staged.
+// The codes go straight into 16-bit MFMA operands as the exact value
+// 1 + q * 2^-b (the code in the top b mantissa bits of 1.0; bf16 against the
+// bf16 activations x for gate and up, fp16 against the fp16 hidden vector h
+// for down), so the dequantized weight is never rounded: for each group g of
+// G inputs a_k, with S = sum_k a_k,
+//   sum_k s (q_k - z) a_k = (s * 2^b) * (acc_g - (1 + z * 2^-b) * S),
+// acc_g = sum_k (1 + q_k 2^-b) a_k from the MFMA.  The accumulators stay near
+// the size of the activation sums, so fp32 accumulation loses little.  The
+// group sums of the activations (of the fp16 values, for h) are formed while
+// they are staged.
 //
 // Kernels (all on the caller's stream, no host synchronisation; experts with
 // no kept token exit at once because the counts are read on the device):
@@ -63,12 +66,13 @@ static_assert((kSxBytes / (4 * 32)) * 32 >= 4 * kTileCols, "group-sum budget (32
 
 __device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
 
-// Operand format of the activations: bf16 (x) or fp16 (h).  The code offset o
-// is the power of two whose 16-bit pattern ORs with a code in bits 0..2.
+// Operand format of the activations: bf16 (x) or fp16 (h).  Codes of b bits
+// sit in the top b bits of the mantissa of 1.0 (bit kPos<b> upwards).
 template <bool F16>
 struct Fmt {
-  static constexpr uint32_t kMagic2 = F16 ? 0x64006400u : 0x43004300u;   // o in both halves
-  static constexpr float kOffset = F16 ? 1024.0f : 128.0f;
+  static constexpr uint32_t kMagic2 = F16 ? 0x3c003c00u : 0x3f803f80u;   // 1.0 in both halves
+  template <int BITS>
+  static constexpr int kPos = (F16 ? 10 : 7) - BITS;
 };
 
 template <bool F16>
@@ -90,13 +94,14 @@ __device__ __forceinline__ uint32_t vgpr_constant(uint32_t c) {
   return v;
 }
 
-template <int BITS>
+template <int BITS, bool F16>
 __device__ __forceinline__ u32x4 b_operand(const uint32_t* w, int u, uint32_t magic) {
+  constexpr int POS = Fmt<F16>::template kPos<BITS>;
   u32x4 v;
-  v[0] = extract_pair<BITS>(w, 4 * u + 0, magic);
-  v[1] = extract_pair<BITS>(w, 4 * u + 1, magic);
-  v[2] = extract_pair<BITS>(w, 4 * u + 2, magic);
-  v[3] = extract_pair<BITS>(w, 4 * u + 3, magic);
+  v[0] = code_pair<BITS, POS>(w, 4 * u + 0, magic);
+  v[1] = code_pair<BITS, POS>(w, 4 * u + 1, magic);
+  v[2] = code_pair<BITS, POS>(w, 4 * u + 2, magic);
+  v[3] = code_pair<BITS, POS>(w, 4 * u + 3, magic);
   return v;
 }
 
@@ -117,11 +122,12 @@ __device__ __forceinline__ float sum8(u32x4 v) {
   return s;
 }
 
-// Group epilogue: tot += s * (acc - (o + z) * sum_a); acc = 0.
-template <bool F16>
+// Group epilogue: tot += s 2^b * (acc - (1 + z 2^-b) * sum_a); acc = 0
+// (both scalings by powers of two are exact).
+template <int BITS>
 __device__ __forceinline__ void group_end(f32x4& acc, f32x4& tot, uint32_t szw, const float* sx4p) {
-  const float s = half_bits_to_float(szw & 0xffffu);
-  const float c = Fmt<F16>::kOffset + half_bits_to_float(szw >> 16);
+  const float s = half_bits_to_float(szw & 0xffffu) * (float)(1 << BITS);
+  const float c = fmaf(half_bits_to_float(szw >> 16), 1.0f / (float)(1 << BITS), 1.0f);
   const f32x4 sx = *reinterpret_cast<const f32x4*>(sx4p);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -266,8 +272,8 @@ __device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
   constexpr int rows = 16 * NT;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const u32x4 b0 = b_operand<BITS>(w[0], u, magic);
-    const u32x4 b1 = b_operand<BITS>(w[1], u, magic);
+    const u32x4 b0 = b_operand<BITS, F16>(w[0], u, magic);
+    const u32x4 b1 = b_operand<BITS, F16>(w[1], u, magic);
     const int kk = lc * kTileCols + 32 * u;
 #pragma unroll
     for (int tb = 0; tb < NT; ++tb) {
@@ -281,8 +287,8 @@ __device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
 #pragma unroll
       for (int tb = 0; tb < NT; ++tb) {
         const float* sxp = sxs + gl * rows + tb * 16 + 4 * (lane >> 4);
-        group_end<F16>(acc[0][tb], tot[0][tb], s[0][q], sxp);
-        group_end<F16>(acc[1][tb], tot[1][tb], s[1][q], sxp);
+        group_end<BITS>(acc[0][tb], tot[0][tb], s[0][q], sxp);
+        group_end<BITS>(acc[1][tb], tot[1][tb], s[1][q], sxp);
       }
     }
   }

@@ -70,6 +70,20 @@ __device__ __forceinline__ uint16_t double_to_half_rne(double v) {
   return r;
 }
 
+// bfloat16 bits of the single round-to-nearest-even rounding of a double
+// (finite): round to fp32 with round-to-odd first (24 >= 8 + 2 bits, so the
+// second rounding is correct, by the same argument as double_to_half_rne).
+__device__ __forceinline__ uint16_t double_to_bf16_rne(double v) {
+  float f = (float)v;
+  if ((double)f != v) {
+    uint32_t b = __float_as_uint(f);
+    if (fabs((double)f) > fabs(v)) b -= 1u;
+    b |= 1u;
+    f = __uint_as_float(b);
+  }
+  return float_to_bf16(f);
+}
+
 // ------------------------------------------------------- memory helpers --
 
 // s_waitcnt vmcnt(n) (expcnt and lgkmcnt left alone).
@@ -107,6 +121,30 @@ __device__ __forceinline__ uint32_t extract_pair(const uint32_t* w, int i, uint3
     }
     return ((w[0] >> 15) & 0x00010001u) | ((w[1] >> 14) & 0x00020002u) |
            ((w[2] >> 13) & 0x00040004u) | magic2;
+  }
+}
+
+// MFMA operand pair with the codes at the top of the mantissa: each 16-bit
+// half is magic2's half (1.0) with code q in bits POS .. POS+BITS-1, i.e. the
+// value 1 + q * 2^-BITS when POS + BITS is the format's mantissa width.  The
+// products of a group then sum to S + 2^-BITS * sum(q * a) with S = sum(a), so
+// the fp32 accumulators stay near the size of the activations.
+template <int BITS, int POS>
+__device__ __forceinline__ uint32_t code_pair(const uint32_t* w, int i, uint32_t magic2) {
+  constexpr uint32_t kMask = (((1u << BITS) - 1u) << POS) * 0x00010001u;
+  // moves bit `src` of each half to bit POS (one shift once i is a constant)
+  auto mv = [](uint32_t x, int src) -> uint32_t { return src >= POS ? x >> (src - POS) : x << (POS - src); };
+  if constexpr (BITS == 1) {
+    return (mv(w[0], i) & kMask) | magic2;
+  } else if constexpr (BITS == 2) {
+    return (mv(w[i >> 3], 2 * (i & 7)) & kMask) | magic2;
+  } else {
+    if (i < 15) {
+      const int wi = i / 5, f = i - 5 * wi;
+      return (mv(w[wi], 3 * f) & kMask) | magic2;
+    }
+    constexpr uint32_t b0 = 0x00010001u << POS;
+    return (mv(w[0], 15) & b0) | (mv(w[1], 14) & (b0 << 1)) | (mv(w[2], 13) & (b0 << 2)) | magic2;
   }
 }
 

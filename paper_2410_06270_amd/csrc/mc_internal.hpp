@@ -11,6 +11,7 @@ constexpr int kDecodeMaxT = 64;        // up to this many tokens one workgroup h
 enum TimingSite {
   kSitePackSz, kSitePackCodes, kSiteExport, kSiteRouteFused, kSiteRouteSelect, kSiteRouteLists,
   kSiteGateUp, kSiteDown, kSiteCombine, kSitePrefillPrep, kSiteImpColsum, kSiteImpFinish, kSiteImpSelect,
+  kSiteRmsNorm,
   kNumSites
 };
 void timing_begin(hipStream_t stream, int site);
@@ -38,8 +39,13 @@ struct PrefillLayout {
 PrefillLayout prefill_layout(int T, int E, int k, int d, int ffn);
 hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routing& r, void* ws,
                           float** partial, size_t* part_stride, int* nsplit, hipStream_t stream);
+// residual (may be null): y = bf16(residual + sum_r w_r E_{e_r}(x)).
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
-                          void* ws, hipStream_t stream);
+                          void* ws, const uint16_t* residual, hipStream_t stream);
+// Stack of layers: xn = RMSNorm(h) (fp64, one bf16 rounding) before each layer.
+constexpr double kRmsNormEps = 1e-5;
+hipError_t launch_rmsnorm(const uint16_t* h, int T, int d, double eps, uint16_t* xn, hipStream_t stream);
+size_t stack_workspace_bytes(int T, int E, int k, int d, int ffn);   // xn [T][d] + forward workspace
 size_t importance_workspace_bytes(int H, int L);
 hipError_t launch_importance(const uint16_t* attn, int H, int L, const uint16_t* x, int d, float rho,
                              float* importance, uint8_t* mask, void* ws, hipStream_t stream);

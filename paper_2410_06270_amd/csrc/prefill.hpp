@@ -6,15 +6,14 @@
 // and y_t = sum_r w_r Y[pos(t, r)] by the combine kernel of the decode path.
 //
 // The weights are never rounded.  As in the decode kernels, the codes enter
-// the MFMA as exact integers offset by a power of two (magic), and the scale
-// and zero of each group are applied to the fp32 group sum:
-//   sum_{k in g} x_k s (q_k - z) = s * (acc_g - (magic + z) * S_g),
-//   acc_g = sum_k x_k (magic + q_k) (MFMA),  S_g = sum_{k in g} x_k,
+// the MFMA as the exact values 1 + q 2^-b (code in the top b mantissa bits of
+// 1.0), and the scale and zero of each group are applied to the fp32 group sum:
+//   sum_{k in g} x_k s (q_k - z) = s 2^b * (acc_g - (1 + z 2^-b) * S_g),
+//   acc_g = sum_k x_k (1 + q_k 2^-b) (MFMA),  S_g = sum_{k in g} x_k,
 // so per group of G columns each output costs two fp32 fmas.
-//  * gate/up: x stays bf16 (exact), codes are bf16 128 + q,
-//    v_mfma_f32_32x32x16_bf16;
+//  * gate/up: x stays bf16 (exact), codes in bf16, v_mfma_f32_32x32x16_bf16;
 //  * down: h is rounded once to fp16 (the only rounding on the path besides
-//    fp32 accumulation), codes are fp16 1024 + q, v_mfma_f32_32x32x16_f16.
+//    fp32 accumulation), codes in fp16, v_mfma_f32_32x32x16_f16.
 // Activations are held in a fragment layout: a fragment is 32 rows x 16
 // columns (1 KB), stored in the order the MFMA A operand takes it (lane l:
 // row l%32, columns 8*(l/32) .. +8); a wave stages a fragment into LDS with one
@@ -131,11 +130,12 @@ __device__ __forceinline__ void pf_load(uint32_t (&w)[2][BITS], uint32_t (&s)[GP
     s[q] = __builtin_amdgcn_raw_buffer_load_b32(st.s, st.off_s + ((uint32_t)c * GPC + q) * 64u, 0, 0);
 }
 
-// B operand of MFMA step u of one 64-column piece: 8 codes as magic + q.
-template <int BITS>
+// B operand of MFMA step u of one 64-column piece: 8 codes as 1 + q 2^-b.
+template <int BITS, bool BF16>
 __device__ __forceinline__ u32x4 pf_codes(const uint32_t (&w)[BITS], int u, uint32_t magic) {
-  return u32x4{extract_pair<BITS>(w, 4 * u + 0, magic), extract_pair<BITS>(w, 4 * u + 1, magic),
-               extract_pair<BITS>(w, 4 * u + 2, magic), extract_pair<BITS>(w, 4 * u + 3, magic)};
+  constexpr int POS = Fmt<!BF16>::template kPos<BITS>;
+  return u32x4{code_pair<BITS, POS>(w, 4 * u + 0, magic), code_pair<BITS, POS>(w, 4 * u + 1, magic),
+               code_pair<BITS, POS>(w, 4 * u + 2, magic), code_pair<BITS, POS>(w, 4 * u + 3, magic)};
 }
 
 template <bool BF16>
@@ -175,20 +175,19 @@ __device__ __forceinline__ void pf_stage(unsigned char* stage, const PrefillGemm
             stage + S::kFragBytes + half * 1024);
 }
 
-// Group epilogue: tot += s * (acc - (magic + z) * S_g); per lane its row's
-// s and z (word sw of each stream), S_g of the tile rows from the stage.
-template <int GPC, bool BF16, int WTOK>
+// Group epilogue: tot += s 2^b * (acc - (1 + z 2^-b) * S_g); per lane its
+// row's s and z (word sw of each stream), S_g of the tile rows from the stage.
+template <int BITS, int GPC, bool BF16, int WTOK>
 __device__ __forceinline__ void pf_epilogue(const f32x16 (&acc)[kPfWaveTiles][2], const uint32_t (&sw)[2],
                                             const unsigned char* stage, int q, int tg, int lane,
                                             f32x16 (&tot)[kPfWaveTiles][2]) {
   using S = PfShape<WTOK>;
-  const float mval = BF16 ? 128.0f : 1024.0f;
   const float* ssum = reinterpret_cast<const float*>(stage + S::kFragBytes);
   float sj[2], cj[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    sj[j] = half_bits_to_float(sw[j] & 0xffffu);
-    cj[j] = mval + half_bits_to_float(sw[j] >> 16);
+    sj[j] = half_bits_to_float(sw[j] & 0xffffu) * (float)(1 << BITS);
+    cj[j] = fmaf(half_bits_to_float(sw[j] >> 16), 1.0f / (float)(1 << BITS), 1.0f);
   }
 #pragma unroll
   for (int t = 0; t < kPfWaveTiles; ++t) {
@@ -218,8 +217,8 @@ __device__ __forceinline__ void pf_group(const unsigned char* stage, const uint3
     u32x4 a[kPfWaveTiles];
 #pragma unroll
     for (int t = 0; t < kPfWaveTiles; ++t) a[t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + v) * kPfFragBytes);
-    const u32x4 b0 = pf_codes<BITS>(w[0][v & 1], v >> 1, magic);
-    const u32x4 b1 = pf_codes<BITS>(w[1][v & 1], v >> 1, magic);
+    const u32x4 b0 = pf_codes<BITS, BF16>(w[0][v & 1], v >> 1, magic);
+    const u32x4 b1 = pf_codes<BITS, BF16>(w[1][v & 1], v >> 1, magic);
 #pragma unroll
     for (int t = 0; t < kPfWaveTiles; ++t) {
       const f32x16 z = {};
@@ -257,7 +256,7 @@ __device__ __forceinline__ void pf_chunk(const PfStream (&sp)[2], const PrefillG
   const int slotp = slot == 0 ? kPfSlots - 1 : slot - 1;
   const int slot2 = slot + 2 >= kPfSlots ? slot + 2 - kPfSlots : slot + 2;
   const unsigned char* cur = smem + slot * S::kStageBytes;
-  if (active && late && !first) pf_epilogue<GPC, BF16, WTOK>(acc, ps, smem + slotp * S::kStageBytes, GPC - 1, tg, lane, tot);
+  if (active && late && !first) pf_epilogue<BITS, GPC, BF16, WTOK>(acc, ps, smem + slotp * S::kStageBytes, GPC - 1, tg, lane, tot);
 #pragma unroll
   for (int j = 0; j < 2; ++j) pf_load<BITS, GPC>(nw[j], ns[j], sp[j], c + 1 < last ? c + 1 : last);
   pf_stage<GPC, WTOK>(smem + slot2 * S::kStageBytes, g, f0, c + 2 < last ? c + 2 : last, wave, lane);
@@ -266,7 +265,7 @@ __device__ __forceinline__ void pf_chunk(const PfStream (&sp)[2], const PrefillG
   for (int q = 0; q < GPC; ++q) {
     pf_group<BITS, GPC, BF16>(cur, w, q, tg, lane, magic, acc);
     uint32_t sw[2] = {s[0][q], s[1][q]};
-    if (q < GPC - 1 || !late) pf_epilogue<GPC, BF16, WTOK>(acc, sw, cur, q, tg, lane, tot);
+    if (q < GPC - 1 || !late) pf_epilogue<BITS, GPC, BF16, WTOK>(acc, sw, cur, q, tg, lane, tot);
     else { ps[0] = sw[0]; ps[1] = sw[1]; }
   }
 }
@@ -299,7 +298,7 @@ __device__ __forceinline__ void pf_loop(const PfStream (&sp)[2], const PrefillGe
   }
   // the late waves' last epilogue: the last chunk's stage is the slot before `slot`
   if (active && late)
-    pf_epilogue<GPC, BF16, WTOK>(acc, ps, smem + (slot == 0 ? kPfSlots - 1 : slot - 1) * S::kStageBytes,
+    pf_epilogue<BITS, GPC, BF16, WTOK>(acc, ps, smem + (slot == 0 ? kPfSlots - 1 : slot - 1) * S::kStageBytes,
                                  GPC - 1, tg, lane, tot);
   wait_vmcnt<0>();   // the clamped re-reads of the last chunks land before LDS is reused
 }

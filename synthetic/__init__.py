@@ -19,6 +19,11 @@ Workloads (the paper's Mixtral 8x7b and OLMoE shapes; no dataset is used):
                  p {0.2,0.5,0.3}, G=64, logits N(0,1) + ln Zipf(1.1)
                  popularity over a seeded expert permutation, tau=0.05,
                  prefill T=2048, decode T=16.
+* 5 ``mixtral_stack``: 32 layers of the shape of 2, each layer with the
+                 widths [3,3,3,2,2,2,2,3] in its own seeded order, its own
+                 weights, logits (N(0,1) + its own per-expert bias
+                 N(0, 0.5^2)) and protected tokens; decode T in {1, 64},
+                 prefill T=1024, tau=0.3.
 
 Weights are N(0, 0.02^2) fp32, activations N(0,1) rounded once to bfloat16,
 and round(0.1*T) tokens (a seeded permutation) are marked important.
@@ -41,11 +46,14 @@ CONFIGS = {
             G=128, T=[4096], tau=[0.0, 0.2, 0.4], bias_std=0.5, zipf=None),
     4: dict(name="olmoe", d=2048, ffn=1024, E=64, k=8, bits=None, G=64,
             T=[2048, 16], tau=[0.05], bias_std=0.0, zipf=1.1),
+    5: dict(name="mixtral_stack", d=4096, ffn=14336, E=8, k=2, bits=[3, 3, 3, 2, 2, 2, 2, 3],
+            G=128, T=[1, 64, 1024], tau=[0.3], bias_std=0.5, zipf=None, layers=32),
 }
 
 # stream ids inside a config's seed
 _S_X, _S_BIAS, _S_LOGITS, _S_MASK, _S_BITS, _S_ATTN = 1, 2, 3, 4, 5, 6
 _S_WEIGHT = 1000
+_S_LAYER = 100000       # stream offset per layer of a stack (config 5)
 
 
 def rng(config_id: int, stream: int) -> np.random.Generator:
@@ -148,3 +156,53 @@ def attention(config_id: int, H: int, L: int) -> np.ndarray:
         s /= s.sum(axis=1, keepdims=True)
         out[h] = to_bf16_bits(s)
     return out
+
+
+# ------------------------------------------------------------------ stacks --
+# Layer l of a stack draws every tensor from the streams of a single layer
+# shifted by _S_LAYER * (l + 1), so no two layers share a stream.
+
+def stack_bits(config_id: int, layer: int) -> list:
+    """Expert widths of one layer: the config's widths in a seeded order."""
+    c = CONFIGS[config_id]
+    g = rng(config_id, _S_LAYER * (layer + 1) + _S_BITS)
+    return [int(b) for b in g.permutation(np.asarray(c["bits"]))]
+
+
+def stack_expert_weights(config_id: int, layer: int, e: int, d=None, ffn=None, std: float = 0.02):
+    """fp32 N(0, std^2) gate [ffn][d], up [ffn][d], down [d][ffn] of expert e of one layer."""
+    c = CONFIGS[config_id]
+    d = c["d"] if d is None else d
+    ffn = c["ffn"] if ffn is None else ffn
+    mats = []
+    for m in range(3):
+        g = rng(config_id, _S_LAYER * (layer + 1) + _S_WEIGHT + 3 * e + m)
+        w = g.standard_normal(size=(ffn, d) if m < 2 else (d, ffn), dtype=np.float32)
+        w *= np.float32(std)
+        mats.append(w)
+    return tuple(mats)
+
+
+def stack_layer_weights(config_id: int, layer: int, E=None, d=None, ffn=None, std: float = 0.02):
+    E = CONFIGS[config_id]["E"] if E is None else E
+    return [stack_expert_weights(config_id, layer, e, d, ffn, std) for e in range(E)]
+
+
+def stack_logits(config_id: int, layer: int, T: int, E=None) -> np.ndarray:
+    """Router logits of one layer [T][E] fp32: N(0,1) + the layer's per-expert
+    offset N(0, bias_std^2)."""
+    c = CONFIGS[config_id]
+    E = c["E"] if E is None else E
+    base = _S_LAYER * (layer + 1)
+    offset = rng(config_id, base + _S_BIAS).normal(0.0, c["bias_std"], size=E)
+    g = rng(config_id, base + _S_LOGITS + 100 * T)
+    return (g.standard_normal(size=(T, E)) + offset[None, :]).astype(np.float32)
+
+
+def stack_mask(config_id: int, layer: int, T: int, frac: float = 0.1) -> np.ndarray:
+    """Protected tokens of one layer: floor(frac*T + 0.5) of them, seeded."""
+    n = int(np.floor(frac * T + 0.5))
+    g = rng(config_id, _S_LAYER * (layer + 1) + _S_MASK + 100 * T)
+    m = np.zeros(T, np.uint8)
+    m[g.permutation(T)[:n]] = 1
+    return m

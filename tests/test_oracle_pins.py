@@ -380,6 +380,105 @@ def test_forward_rows_and_tokens_subset():
     np.testing.assert_array_equal(part, full[np.ix_(toks, rows)])
 
 
+# ---------------------------------------------------------- residual stack ---
+
+def _bf16_rne(v):
+    """Round fp64 values to bfloat16 (nearest, ties to even) by exact fp64
+    arithmetic on the two neighbouring bf16 values; returns bits.  Written
+    here independently of the oracle's C rounding."""
+    v = np.asarray(v, dtype=np.float64)
+    m, e = np.frexp(np.abs(v))                     # |v| = m 2^e, m in [0.5, 1)
+    q = np.ldexp(1.0, e - 8)                       # bf16 quantum at |v| (8 significant bits)
+    k = np.floor(np.abs(v) / q)                    # exact: division by a power of two
+    rem = np.abs(v) - k * q                        # exact
+    up = (rem > q / 2) | ((rem == q / 2) & (k % 2 == 1))
+    mag = (k + up) * q
+    out = np.copysign(mag, v).astype(np.float32)   # exact: at most 9 significant bits
+    return (out.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def test_bf16_rne_helper_matches_torch_where_fp32_is_exact():
+    import torch
+    g = np.random.default_rng(5)
+    v = (g.standard_normal(20000) * 10.0 ** g.integers(-3, 4, 20000)).astype(np.float32).astype(np.float64)
+    want = torch.from_numpy(v.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(_bf16_rne(v), want)
+
+
+def test_rms_norm_matches_torch_float64():
+    """xn = bf16(h / sqrt(mean(h^2) + eps)) against torch's rms_norm in
+    float64 (unit gain, eps = 1e-5), rounded by the exact helper above."""
+    import torch
+    x = synthetic.activations(1, 16, d=512)
+    x[3] = synthetic.to_bf16_bits(np.full(512, 1e-3, np.float32))     # eps matters here
+    got = oracle.rms_norm(x)
+    h = torch.from_numpy(oracle.bf16_to_float64(x))
+    ref = torch.nn.functional.rms_norm(h, (512,), eps=1e-5).numpy()
+    np.testing.assert_array_equal(got, _bf16_rne(ref))
+    ms = (oracle.bf16_to_float64(got) ** 2).mean(axis=1)
+    assert np.all(np.abs(ms[np.arange(16) != 3] - 1.0) < 1e-2)
+
+
+def test_stack_single_expert_is_numpy_residual_swiglu():
+    """E = 1, k = 1 layers: h_{l+1} = bf16(h_l + SwiGLU_l(bf16(rms_norm(h_l)))),
+    the norm by torch, the SwiGLU by numpy matmuls on dequantized weights and
+    every rounding by the exact helper above."""
+    import torch
+    nl, T = 3, 12
+    layers = []
+    for l in range(nl):
+        mats = synthetic.stack_layer_weights(5, l, E=1, d=256, ffn=512)
+        _, _, logical = oracle.pack_layer(mats, [2 + l % 2], 32)
+        rt = oracle.route(np.zeros((T, 1), np.float32), None, 1, 0.3)
+        layers.append((rt, logical))
+    x = synthetic.activations(1, T)
+    got = oracle.moe_stack(x, layers, 32)
+    h = oracle.bf16_to_float64(x)
+    for l, (rt, logical) in enumerate(layers):
+        xn = torch.nn.functional.rms_norm(torch.from_numpy(h), (256,), eps=1e-5).numpy()
+        xn = oracle.bf16_to_float64(_bf16_rne(xn))
+        want = _bf16_rne(h + _swiglu_numpy(xn, logical[0], 32))
+        np.testing.assert_array_equal(got[l], want)
+        h = oracle.bf16_to_float64(want)
+
+
+def test_stack_zero_experts_are_identity():
+    """All-zero weights quantize to zero codes with zero dequantized value, so
+    each layer adds nothing and the residual stream passes through unchanged."""
+    T, E = 10, 4
+    zeros = [tuple(np.zeros((512, 256) if m < 2 else (256, 512), np.float32) for m in range(3))
+             for _ in range(E)]
+    _, _, logical = oracle.pack_layer(zeros, [1, 2, 3, 2], 32)
+    layers = [(oracle.route(synthetic.stack_logits(5, l, T, E=E), None, 2, 0.3), logical)
+              for l in range(2)]
+    x = synthetic.activations(1, T)
+    got = oracle.moe_stack(x, layers, 32)
+    for h in got:
+        np.testing.assert_array_equal(h, x)
+
+
+def test_stack_tokens_are_independent():
+    """Each token's path depends only on its own row and routing: a token
+    subset gives the same rows as the full run."""
+    T, E = 16, 4
+    bits = [1, 2, 3, 2]
+    layers = []
+    for l in range(2):
+        mats = synthetic.stack_layer_weights(5, l, E=E, d=256, ffn=512)
+        _, _, logical = oracle.pack_layer(mats, bits, 32)
+        rt = oracle.route(synthetic.stack_logits(5, l, T, E=E), synthetic.stack_mask(5, l, T), 2, 0.3)
+        layers.append((rt, logical))
+    x = synthetic.activations(1, T)
+    full = oracle.moe_stack(x, layers, 32)
+    toks = [0, 5, 15]
+    part = oracle.moe_stack(x, layers, 32, tokens=toks)
+    for a, b in zip(full, part):
+        np.testing.assert_array_equal(a[toks], b)
+    # the residual is really there: the output differs from the MoE output alone
+    y0 = oracle.moe_forward(x, layers[0][0], layers[0][1], 32)
+    assert not np.array_equal(full[0], oracle.bf16_round_array(y0))
+
+
 # ------------------------------------------------------- Eq. 6 importance ---
 
 def _causal_attention(g, H, L):
