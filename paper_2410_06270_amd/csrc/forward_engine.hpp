@@ -17,7 +17,7 @@
 // Kernels (all on the caller's stream, no host synchronisation; experts with
 // no kept token exit at once because the counts are read on the device):
 //   gateup_kernel  grid (ffn/128, E, chunks x d-splits): 8 waves x 16 rows of
-//                  gate and up, up to 16*NTMAX tokens of one expert per chunk
+//                  gate and up, up to 16*NTMAX (<= 32) tokens of one expert per chunk
 //                  -> h (fp16), or fp32 gate/up partials when d is split;
 //   down_kernel    grid (d/256, E, chunks*S): 8 waves x 32 rows, split-K over
 //                  ffn -> fp32 partials;
@@ -35,15 +35,13 @@ constexpr int kSxBytes = 4 * 1024;            // group sums of the staged slab (
 constexpr int kWavesPerWg = 8;                // workgroups of 512 threads share one slab
 constexpr int kMaxNsplit = 8;                 // largest split of the down reduction
 constexpr int kMaxKsplit = 2;                 // largest split of the gate/up reduction
-// LDS for the staged activation slab.  Batches whose experts see at most 32
-// tokens per workgroup are held to 128 registers (four waves per SIMD, two
-// workgroups per CU) and get 75.5 KB; up to 64 tokens one workgroup fits a CU
-// and gets 100 KB.
-constexpr int kXsBytesSmall = 75 * 1024 + 512;
-constexpr int kXsBytesLarge = 100 * 1024;
+// LDS for the staged activation slab.  A workgroup holds at most 32 tokens
+// of one expert (an expert with more gets one workgroup per 32 of its
+// tokens); the kernels are held to 128 registers (four waves per SIMD) and
+// two workgroups of 75.5 KB share a CU.
+constexpr int kXsBytes = 75 * 1024 + 512;
 constexpr int kLdsPerCu = 160 * 1024;
-static_assert(2 * (kXsBytesSmall + 4 * 1024 + 32 * 4) <= kLdsPerCu, "two workgroups per CU");
-static_assert(kXsBytesLarge + 4 * 1024 + 64 * 4 <= kLdsPerCu, "one workgroup per CU");
+static_assert(2 * (kXsBytes + 4 * 1024 + 32 * 4) <= kLdsPerCu, "two workgroups per CU");
 // Chunks (16 rows x 128 columns of codes) kept in flight per stream.  The slab
 // is a multiple of this many chunks, so it is smaller where the slab rows are
 // many (token blocks) or the registers few (groups per chunk).
@@ -55,13 +53,10 @@ __host__ __device__ constexpr int prefetch_depth(int ntb, int gpc) {
 constexpr int slab_floor_bytes(int ntb) {
   return (16 * ntb + 1) * (prefetch_depth(ntb, 1) * kTileCols + kRowPad) * 2;
 }
-static_assert(slab_floor_bytes(1) <= kXsBytesSmall, "LDS budget (<= 16 tokens)");
-static_assert(slab_floor_bytes(2) <= kXsBytesSmall, "LDS budget (<= 32 tokens)");
-static_assert(slab_floor_bytes(3) <= kXsBytesLarge, "LDS budget (<= 48 tokens)");
-static_assert(slab_floor_bytes(4) <= kXsBytesLarge, "LDS budget (<= 64 tokens)");
+static_assert(slab_floor_bytes(1) <= kXsBytes, "LDS budget (<= 16 tokens)");
+static_assert(slab_floor_bytes(2) <= kXsBytes, "LDS budget (<= 32 tokens)");
 // Group sums: 16*ntb rows x (slab / G) groups x 4 bytes; the slab is capped by
 // kSxBytes, which must allow at least one ring of chunks at G = 32.
-static_assert((kSxBytes / (4 * 64)) * 32 >= 2 * kTileCols, "group-sum budget (64 tokens)");
 static_assert((kSxBytes / (4 * 32)) * 32 >= 4 * kTileCols, "group-sum budget (32 tokens)");
 
 __device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }

@@ -44,11 +44,11 @@ __device__ __forceinline__ void zero_tot(f32x4* t, int n) {
 // the d reduction.  ksplit == 1 writes h = fp16(silu(gate x) * (up x));
 // ksplit > 1 writes the fp32 partial sums of gate and up, which the down
 // kernel adds up (in split order) before the SiLU.
-// Up to 32 tokens per workgroup the kernels are held to 128 registers so that
-// two workgroups (16 waves) share a CU.
+// The kernels are held to 128 registers so that two workgroups (16 waves)
+// share a CU.
 template <int GPC, int NTMAX>
 __global__ void __launch_bounds__(64 * kWavesPerWg)
-__attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2))) gateup_kernel(
+__attribute__((amdgpu_waves_per_eu(4))) gateup_kernel(
     const uint16_t* __restrict__ x, LayerArgs L, const int32_t* __restrict__ counts,
     const int32_t* __restrict__ offsets, const int32_t* __restrict__ pair_token, Hidden hid,
     int xs_bytes) {
@@ -122,7 +122,7 @@ __attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2))) gateup_kernel(
 // values written twice) so that every wave takes part in the staging barriers.
 template <int GPC, int NTMAX>
 __global__ void __launch_bounds__(64 * kWavesPerWg)
-__attribute__((amdgpu_waves_per_eu(NTMAX <= 2 ? 4 : 2))) down_kernel(
+__attribute__((amdgpu_waves_per_eu(4))) down_kernel(
     Hidden hid, LayerArgs L, const int32_t* __restrict__ counts,
     const int32_t* __restrict__ offsets, int nsplit, float* __restrict__ partial,
     size_t part_stride, int xs_bytes) {
@@ -217,7 +217,7 @@ static hipError_t launch_gateup_nt(const uint16_t* x, const LayerArgs& L, const 
                                    const Hidden& h, int xs_bytes, hipStream_t stream) {
   static bool attr = false;
   if (!attr) {
-    hipError_t e = allow_lds(&gateup_kernel<GPC, NTMAX>, kXsBytesLarge + kSxBytes + 512);
+    hipError_t e = allow_lds(&gateup_kernel<GPC, NTMAX>, kXsBytes + kSxBytes + 512);
     if (e != hipSuccess) return e;
     attr = true;
   }
@@ -235,7 +235,7 @@ static hipError_t launch_down_nt(const Hidden& h, const LayerArgs& L, const mc_r
                                  hipStream_t stream) {
   static bool attr = false;
   if (!attr) {
-    hipError_t e = allow_lds(&down_kernel<GPC, NTMAX>, kXsBytesLarge + kSxBytes + 512);
+    hipError_t e = allow_lds(&down_kernel<GPC, NTMAX>, kXsBytes + kSxBytes + 512);
     if (e != hipSuccess) return e;
     attr = true;
   }
@@ -252,8 +252,7 @@ template <int GPC>
 hipError_t launch_gateup(const uint16_t* x, const LayerArgs& L, const mc_routing& r,
                          const Hidden& h, int ntmax, int xs_bytes, hipStream_t stream) {
   if (ntmax == 1) return launch_gateup_nt<GPC, 1>(x, L, r, h, xs_bytes, stream);
-  if (ntmax == 2) return launch_gateup_nt<GPC, 2>(x, L, r, h, xs_bytes, stream);
-  return launch_gateup_nt<GPC, 4>(x, L, r, h, xs_bytes, stream);
+  return launch_gateup_nt<GPC, 2>(x, L, r, h, xs_bytes, stream);
 }
 
 template <int GPC>
@@ -261,8 +260,7 @@ hipError_t launch_down(const Hidden& h, const LayerArgs& L, const mc_routing& r,
                        float* partial, size_t part_stride, int ntmax, int xs_bytes,
                        hipStream_t stream) {
   if (ntmax == 1) return launch_down_nt<GPC, 1>(h, L, r, nsplit, partial, part_stride, xs_bytes, stream);
-  if (ntmax == 2) return launch_down_nt<GPC, 2>(h, L, r, nsplit, partial, part_stride, xs_bytes, stream);
-  return launch_down_nt<GPC, 4>(h, L, r, nsplit, partial, part_stride, xs_bytes, stream);
+  return launch_down_nt<GPC, 2>(h, L, r, nsplit, partial, part_stride, xs_bytes, stream);
 }
 
 }  // namespace mc

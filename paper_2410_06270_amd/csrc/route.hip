@@ -8,8 +8,9 @@
 // (fp64).  Sec. 3.3.2: a protected token keeps every selected expert.  The
 // kept weights are renormalised over the kept ranks.
 //
-// Selection (one wavefront per token): lanes hold the logits, k rounds of a
-// 64-bit max-reduction pick the experts, lane r then evaluates rank r.
+// Selection (one wavefront per token): lanes hold the logits, every key's
+// rank is counted against all keys broadcast in turn, lane r then evaluates
+// rank r; the softmax sums add the ranks in order.
 // Lists: per-expert token lists in ascending token order, built with ballots
 // and popcount prefixes (list positions never depend on timing, so the lists
 // are deterministic).  Small batches run both phases in one launch with
@@ -25,22 +26,6 @@ constexpr int kListBlocks = 64;     // at most this many token blocks scatter th
 constexpr int kListMaxBlockT = 1024;
 static_assert(kListBlocks * kListMaxBlockT >= MC_MAX_TOKENS, "list blocks cover every token");
 
-__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v) {
-  for (int off = 32; off >= 1; off >>= 1) {
-    const unsigned lo = __shfl_xor((unsigned)(v & 0xffffffffu), off);
-    const unsigned hi = __shfl_xor((unsigned)(v >> 32), off);
-    const unsigned long long o = ((unsigned long long)hi << 32) | lo;
-    v = o > v ? o : v;
-  }
-  return v;
-}
-
-// Sum over lanes 0..7 (the ranks) in a fixed butterfly order.
-__device__ __forceinline__ double rank_sum(double v) {
-  for (int off = 1; off < MC_MAX_TOPK; off <<= 1) v += __shfl_xor(v, off);
-  return v;
-}
-
 // Order-preserving integer image of a float, with -0 mapped onto +0.
 __device__ __forceinline__ uint32_t ordered_bits(float f) {
   uint32_t u = __float_as_uint(f);
@@ -48,8 +33,21 @@ __device__ __forceinline__ uint32_t ordered_bits(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Selects and prunes token t.  Lane r < k writes rank r's outputs; when
-// s_ent/s_w are given it also records them in LDS (expert or 0xffff if pruned).
+__device__ __forceinline__ double readlane_f64(double v, int src) {
+  const unsigned long long b = __double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, src);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(b >> 32), src);
+  return __longlong_as_double(((long long)hi << 32) | lo);
+}
+
+// Selects and prunes token t (one wavefront).  Lanes hold the logits (lane l
+// has experts l, l+64, ...) as distinct 64-bit keys (ordered logit bits, then
+// the complement of the expert index, so larger key = earlier rank); each
+// key's rank is the number of larger keys, counted against every key
+// broadcast in turn (no cross-lane reductions).  Lane r < k then takes rank r
+// and evaluates it; the softmax sums run over the ranks in order.  Lane r < k
+// writes rank r's outputs; when s_ent/s_w are given it also records them in
+// LDS (expert, or 0xffff if pruned).
 __device__ void select_token(const float* __restrict__ logits, const uint8_t* __restrict__ important,
                              int t, int E, int k, float delta32, double tau,
                              int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
@@ -57,42 +55,58 @@ __device__ void select_token(const float* __restrict__ logits, const uint8_t* __
                              uint16_t* s_ent, float* s_w) {
   const int lane = threadIdx.x & 63;
   const float* l = logits + (size_t)t * E;
+  const int nj = (E + 63) >> 6;                      // logits per lane (wave-uniform)
   float lv[4];
-  unsigned long long key[4];
+  uint32_t khi[4], klo[4];
+  int rank[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + 64 * j;
     lv[j] = (e < E) ? l[e] : 0.0f;
-    key[j] = (e < E) ? (((unsigned long long)ordered_bits(lv[j]) << 32) | (unsigned)(0xffff - e)) : 0ull;
+    khi[j] = (e < E) ? ordered_bits(lv[j]) : 0u;
+    klo[j] = (e < E) ? (uint32_t)(0xffff - e) : 0u;
+    rank[j] = 0;
+  }
+  for (int sj = 0; sj < nj; ++sj) {
+    const int n = (E - 64 * sj) < 64 ? (E - 64 * sj) : 64;
+    for (int src = 0; src < n; ++src) {
+      const uint32_t ohi = __builtin_amdgcn_readlane(khi[sj], src);
+      const uint32_t olo = __builtin_amdgcn_readlane(klo[sj], src);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (j < nj) rank[j] += (ohi > khi[j] || (ohi == khi[j] && olo > klo[j])) ? 1 : 0;
+    }
   }
   const bool prot = important != nullptr && important[t] != 0;
   int my_e = 0;
   float my_l = 0.0f;
+  float l0 = 0.0f, l1 = 0.0f;
   for (int r = 0; r < k; ++r) {
-    unsigned long long best = key[0];
-#pragma unroll
-    for (int j = 1; j < 4; ++j) best = key[j] > best ? key[j] : best;
-    best = wave_max_u64(best);
-    const int e = 0xffff - (int)(best & 0xffffu);
-    // the owner lane of expert e broadcasts its logit (exact: the key is not decoded)
+    int e = 0;
     float le = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (lane + 64 * j == e) {
-        le = lv[j];
-        key[j] = 0ull;
+    for (int j = 0; j < 4; ++j) {
+      if (j < nj) {
+        const unsigned long long b = __ballot(rank[j] == r);
+        if (b) {
+          const int src = __ffsll((long long)b) - 1;
+          e = 64 * j + src;
+          le = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, lv[j]), src));
+        }
       }
-    le = __shfl(le, e & 63);
+    }
+    if (r == 0) l0 = le;
+    if (r == 1) l1 = le;
     if (lane == r) {
       my_e = e;
       my_l = le;
     }
   }
-  const float l0 = __shfl(my_l, 0);
-  const float l1 = __shfl(my_l, 1 < k ? 1 : 0);
+  if (k < 2) l1 = l0;
   const bool mine = lane < k;
   const double ex = mine ? exp((double)my_l - (double)l0) : 0.0;
-  const double sum_all = rank_sum(ex);
+  double sum_all = 0.0;
+  for (int r = 0; r < k; ++r) sum_all += readlane_f64(ex, r);
   bool keep = mine;
   if (mine && lane > 0 && !prot) {
     if (k == 2) {
@@ -102,7 +116,10 @@ __device__ void select_token(const float* __restrict__ logits, const uint8_t* __
       keep = !(ex < tau * sum_all);
     }
   }
-  const double sum_kept = rank_sum(keep ? ex : 0.0);
+  const unsigned long long kb = __ballot(keep);
+  double sum_kept = 0.0;
+  for (int r = 0; r < k; ++r)
+    if ((kb >> r) & 1ull) sum_kept += readlane_f64(ex, r);
   if (mine) {
     const size_t o = (size_t)t * k + lane;
     const float w = keep ? (float)(ex / sum_kept) : 0.0f;
