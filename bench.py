@@ -199,10 +199,12 @@ def traffic_from_profiles(kernel, workload, hash_now):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(synthetic, T):
+def cpu_baseline(synthetic, T, min_seconds=10.0, max_reps=30):
     """The oracle on the same decode batch and layer shape: routing of all T
     tokens and the SwiGLU forward over every kept pair, on random codes and
-    fp16 scale/zero of the real shapes (the timing does not depend on values)."""
+    fp16 scale/zero of the real shapes (the timing does not depend on values).
+    The batch is run repeatedly until at least min_seconds of CPU work have
+    been timed (at most max_reps runs); the rate is tokens over total time."""
     import numpy as np
     import oracle
     c = synthetic.config(2)
@@ -211,9 +213,7 @@ def cpu_baseline(synthetic, T):
     imp = synthetic.important_mask(2, T)
     x = synthetic.activations(2, T)
     g = np.random.default_rng(7)
-    t_route = time.perf_counter()
     rt = oracle.route(lg, imp, k, tau)
-    t_route = time.perf_counter() - t_route
     logical = []
     for e in range(E):
         if rt["counts"][e] == 0:
@@ -227,15 +227,19 @@ def cpu_baseline(synthetic, T):
             z = g.uniform(0, 2 ** bits[e] - 1, (R, K // G)).astype(np.float16).view(np.uint16)
             per.append((q, s, z))
         logical.append(per)
-    t0 = time.perf_counter()
-    oracle.moe_forward(x, rt, logical, G)
-    el = time.perf_counter() - t0 + t_route
+    el, reps = 0.0, 0
+    while el < min_seconds and reps < max_reps:
+        t0 = time.perf_counter()
+        rt = oracle.route(lg, imp, k, tau)
+        oracle.moe_forward(x, rt, logical, G)
+        el += time.perf_counter() - t0
+        reps += 1
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return dict(value=T / el, unit="tokens/s", cores=threads, kind="oracle",
-                seconds=round(el, 3),
-                sample="the full T=%d decode batch: routing + SwiGLU forward over its %d kept "
-                       "pairs on the d=4096/ffn=14336/E=8 layer (random codes, same shapes)"
-                       % (T, int(rt["counts"].sum())))
+    return dict(value=reps * T / el, unit="tokens/s", cores=threads, kind="oracle",
+                seconds=round(el, 3), runs=reps,
+                sample="%d runs of the full T=%d decode batch: routing + SwiGLU forward over its %d kept "
+                       "pairs on the d=4096/ffn=14336/E=8 layer (random codes, same shapes), %d OpenMP threads"
+                       % (reps, T, int(rt["counts"].sum()), threads))
 
 
 def measure_step(mc, torch, wl, steps, warmup):

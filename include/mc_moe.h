@@ -218,6 +218,31 @@ mc_status mc_token_importance(const uint16_t *attn_bf16, int H, int L, const uin
  * pure host computation.  Errors: MC_EINVAL. */
 mc_status mc_odp_threshold(const float *logits_host, int T, int E, double *mu, double *tau);
 
+/* Offline PMQ allocation (Sec. 3.2), pure host computation.
+ * Expert significance (Sec. 3.2.1) from calibration router logits
+ * logits_host [T][E] fp32 (HOST memory, finite): each token's top-k experts
+ * by (logit descending, expert index ascending) with routing weights the
+ * softmax over the selected k (fp64);  phi[e] = (tokens that select e) / T,
+ * w[e] = (sum of e's routing weights) / T  (host [E] each; sum phi = k,
+ * sum w = 1).  Errors: MC_EINVAL. */
+mc_status mc_pmq_significance(const float *logits_host, int T, int E, int k, double *phi, double *w);
+
+/* Expert widths by the integer program of Eq. 4: b_e in {1, 2, 3} minimising
+ *   sum_e phi_e^alpha * w_e^beta * eps[e][b_e - 1]^gamma
+ * subject to sum_e b_e = total_bits (E * target average), at least one expert
+ * at 3 bits and at least one at 2.  phi, w: host [E] (>= 0); eps: host [E][3]
+ * reconstruction errors at 1, 2, 3 bits (>= 0; Eq. 3 measures them as the
+ * F-norm of the output change when only that expert is quantized).  The paper
+ * fixes gamma = 2 and finds alpha, beta in {1, 1.5, 2} equivalent.  Solved
+ * exactly (dynamic programme over experts); the objective of an allocation is
+ * its terms summed in expert order in fp64, and among allocations with equal
+ * objective the lexicographically smallest width vector is returned.
+ * bits: host [E] output; objective (may be NULL): the minimum.
+ * Errors: MC_EINVAL (E < 2, total_bits outside [E + 3, 3E - 1], negative or
+ * non-finite inputs, alpha or beta < 0, gamma <= 0). */
+mc_status mc_pmq_allocate(const double *phi, const double *w, const double *eps, int E, double alpha,
+                          double beta, double gamma, int total_bits, int *bits, double *objective);
+
 /* Instrumentation.  mc_timing_enable(1) clears the record and brackets every
  * kernel launch made afterwards by two HIP events on the launch stream;
  * mc_timing_enable(0) stops recording.  mc_timing_read waits for the recorded

@@ -20,7 +20,9 @@ What it computes (Mixture Compressor for MoE LLMs, ICLR 2025):
   layer;
 * ``token_importance`` -- Eq. 6 importance from causal attention probabilities
   and the protected set (the top floor(rho*L + 1/2) tokens);
-* ``median_ratio``  -- the pruning threshold mu as the median of w1/w0.
+* ``median_ratio``  -- the pruning threshold mu as the median of w1/w0;
+* ``pmq_significance`` / ``pmq_allocate`` -- Sec. 3.2: expert access
+  frequency and mean routing weight, and the Eq. 4 width allocation.
 
 Everything floating point is fp64 except operations whose precision the
 definition fixes (fp32 scale/zero arithmetic, the fp32 k = 2 logit gap).
@@ -56,6 +58,9 @@ PINS = {
     "token_importance": "diagonal / first-token closed forms; hand example; head linearity; "
                         "brute-force selection; upper triangle ignored",
     "median_ratio": "statistics.median of exp(l1 - l0) over a naive sort",
+    "pmq_significance": "hand example (golden); sum phi = k and sum w = 1; tie order",
+    "pmq_allocate": "hand-enumerated example (golden); enumeration of every width vector; "
+                    "constraints; significance ordering",
 }
 
 
@@ -381,6 +386,78 @@ def moe_stack(x_bf16: np.ndarray, layers, G: int, tokens=None):
         H[toks] = bf16_round_array(bf16_to_float64(H[toks]) + Y)
         outs.append(H[toks].copy())
     return outs
+
+
+# -------------------------------------------------------------------- PMQ ---
+
+def pmq_significance(logits: np.ndarray, k: int):
+    """Sec. 3.2.1: over N calibration tokens, phi_e = n_e / N with n_e the
+    tokens whose top-k contains e, and w_e = (sum of e's routing weights) / N,
+    the routing weights being the softmax over the selected k (Eq. 1
+    convention of ``route``).  Plain loops in fp64."""
+    T, E = logits.shape
+    n = [0.0] * E
+    s = [0.0] * E
+    for t in range(T):
+        row = [float(v) for v in logits[t]]
+        order = sorted(range(E), key=lambda e: (-row[e], e))[:k]
+        ex = [math.exp(row[e] - row[order[0]]) for e in order]
+        tot = 0.0
+        for v in ex:
+            tot += v
+        for e, v in zip(order, ex):
+            n[e] += 1.0
+            s[e] += v / tot
+    return np.array([v / T for v in n]), np.array([v / T for v in s])
+
+
+def _pmq_terms(phi, w, eps, alpha, beta, gamma):
+    return [[(float(phi[i]) ** alpha) * (float(w[i]) ** beta) * (float(eps[i][b]) ** gamma)
+             for b in range(3)] for i in range(len(phi))]
+
+
+def _pmq_feasible(bits, total):
+    return sum(bits) == total and 3 in bits and 2 in bits
+
+
+def pmq_allocate_bruteforce(phi, w, eps, total_bits: int, alpha=1.0, beta=1.0, gamma=2.0):
+    """Eq. 4 by enumeration of every width vector in lexicographic order (for
+    small E): minimise sum_i phi_i^alpha w_i^beta eps_{i,b_i}^gamma (terms
+    added in expert order) subject to sum b_i = total_bits, some b_i = 3 and
+    some b_i = 2; the first minimum met (the lexicographically smallest) wins.
+    Returns (bits, objective) or None when infeasible."""
+    import itertools
+    term = _pmq_terms(phi, w, eps, alpha, beta, gamma)
+    best = None
+    for bits in itertools.product((1, 2, 3), repeat=len(phi)):
+        if not _pmq_feasible(bits, total_bits):
+            continue
+        c = 0.0
+        for i, b in enumerate(bits):
+            c += term[i][b - 1]
+        if best is None or c < best[1]:
+            best = (list(bits), c)
+    return best
+
+
+def pmq_allocate(phi, w, eps, total_bits: int, alpha=1.0, beta=1.0, gamma=2.0):
+    """Eq. 4 for any E: dynamic programme over experts in order; a state is
+    (bits used, some expert at 2, some at 3) and keeps its cheapest prefix
+    (cost summed in expert order; equal costs keep the lexicographically
+    smaller prefix).  Same result as the enumeration."""
+    term = _pmq_terms(phi, w, eps, alpha, beta, gamma)
+    states = {(0, False, False): (0.0, [])}
+    for i in range(len(phi)):
+        nxt = {}
+        for (s, h2, h3), (c, pre) in sorted(states.items()):
+            for b in (1, 2, 3):
+                key = (s + b, h2 or b == 2, h3 or b == 3)
+                cand = (c + term[i][b - 1], pre + [b])
+                if key not in nxt or cand[0] < nxt[key][0] or (cand[0] == nxt[key][0] and cand[1] < nxt[key][1]):
+                    nxt[key] = cand
+        states = nxt
+    got = states.get((total_bits, True, True))
+    return None if got is None else (got[1], got[0])
 
 
 # ------------------------------------------------------------- importance ---

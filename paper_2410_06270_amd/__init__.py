@@ -19,6 +19,8 @@ from ._binding import (  # noqa: F401
     odp_threshold,
     pack,
     pack_sizes,
+    pmq_allocate,
+    pmq_significance,
     route_and_prune,
     stack_forward,
     stack_workspace,

@@ -85,6 +85,11 @@ def load():
         lib.mc_odp_threshold.restype = st
         lib.mc_odp_threshold.argtypes = [P, I, I, ctypes.POINTER(ctypes.c_double),
                                          ctypes.POINTER(ctypes.c_double)]
+        D = ctypes.c_double
+        lib.mc_pmq_significance.restype = st
+        lib.mc_pmq_significance.argtypes = [P, I, I, I, P, P]
+        lib.mc_pmq_allocate.restype = st
+        lib.mc_pmq_allocate.argtypes = [P, P, P, I, D, D, D, I, P, ctypes.POINTER(D)]
         lib.mc_timing_enable.restype = st
         lib.mc_timing_enable.argtypes = [I]
         lib.mc_timing_read.restype = st
@@ -243,6 +248,33 @@ def odp_threshold(logits_host):
     _check(load().mc_odp_threshold(lg.ctypes.data_as(ctypes.c_void_p), lg.shape[0], lg.shape[1],
                                    ctypes.byref(mu), ctypes.byref(tau)))
     return mu.value, tau.value
+
+
+def pmq_significance(logits_host, k: int):
+    """(phi, w) per expert from calibration logits (float32 numpy [T][E])."""
+    import numpy as np
+    lg = np.ascontiguousarray(logits_host, dtype=np.float32)
+    T, E = lg.shape
+    phi, w = np.empty(E, np.float64), np.empty(E, np.float64)
+    _check(load().mc_pmq_significance(lg.ctypes.data_as(ctypes.c_void_p), T, E, k,
+                                      phi.ctypes.data_as(ctypes.c_void_p), w.ctypes.data_as(ctypes.c_void_p)))
+    return phi, w
+
+
+def pmq_allocate(phi, w, eps, total_bits: int, alpha: float = 1.0, beta: float = 1.0, gamma: float = 2.0):
+    """Eq. 4 widths: (bits list, objective).  eps: [E][3] errors at 1, 2, 3 bits."""
+    import numpy as np
+    phi = np.ascontiguousarray(phi, dtype=np.float64)
+    w = np.ascontiguousarray(w, dtype=np.float64)
+    eps = np.ascontiguousarray(eps, dtype=np.float64)
+    E = phi.shape[0]
+    bits = np.empty(E, np.int32)
+    obj = ctypes.c_double()
+    _check(load().mc_pmq_allocate(phi.ctypes.data_as(ctypes.c_void_p), w.ctypes.data_as(ctypes.c_void_p),
+                                  eps.ctypes.data_as(ctypes.c_void_p), E, float(alpha), float(beta),
+                                  float(gamma), int(total_bits), bits.ctypes.data_as(ctypes.c_void_p),
+                                  ctypes.byref(obj)))
+    return [int(b) for b in bits], obj.value
 
 
 def timing_enable(on: bool = True):

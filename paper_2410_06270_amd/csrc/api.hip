@@ -305,6 +305,111 @@ mc_status mc_odp_threshold(const float* logits_host, int T, int E, double* mu, d
   return MC_OK;
 }
 
+// ------------------------------------------------------------------ PMQ --
+// Sec. 3.2.1: expert significance from calibration routing; each token's top-k
+// by (logit descending, expert index ascending), routing weights = softmax
+// over the selected k (fp64, summed in rank order).
+mc_status mc_pmq_significance(const float* logits_host, int T, int E, int k, double* phi, double* w) {
+  if (!logits_host || !phi || !w) return fail(MC_EINVAL, "NULL argument");
+  if (T < 1 || E < 1 || E > MC_MAX_EXPERTS || k < 1 || k > E || k > MC_MAX_TOPK)
+    return fail(MC_EINVAL, "bad shape T=%d E=%d k=%d", T, E, k);
+  std::vector<double> n(E, 0.0), s(E, 0.0);
+  std::vector<int> order(E);
+  for (int t = 0; t < T; ++t) {
+    const float* l = logits_host + (size_t)t * E;
+    for (int e = 0; e < E; ++e) {
+      if (!std::isfinite(l[e])) return fail(MC_EINVAL, "non-finite logit at token %d", t);
+      order[e] = e;
+    }
+    std::partial_sort(order.begin(), order.begin() + k, order.end(), [l](int a, int b) {
+      return l[a] > l[b] || (l[a] == l[b] && a < b);   // -0 == +0 as floats
+    });
+    double ex[MC_MAX_TOPK], sum = 0.0;
+    for (int r = 0; r < k; ++r) {
+      ex[r] = std::exp((double)l[order[r]] - (double)l[order[0]]);
+      sum += ex[r];
+    }
+    for (int r = 0; r < k; ++r) {
+      n[order[r]] += 1.0;
+      s[order[r]] += ex[r] / sum;
+    }
+  }
+  for (int e = 0; e < E; ++e) {
+    phi[e] = n[e] / T;
+    w[e] = s[e] / T;
+  }
+  return MC_OK;
+}
+
+// Sec. 3.2.2, Eq. 4: choose b_i in {1,2,3} minimising
+// sum_i phi_i^alpha w_i^beta eps_{i,b_i}^gamma subject to sum_i b_i =
+// total_bits, at least one expert at 3 bits and one at 2.  Exact: dynamic
+// programme over experts in index order with state (bits used, has a 2, has a
+// 3); the objective of an allocation is summed in expert order in fp64, and
+// among equal objectives the lexicographically smallest width vector wins.
+mc_status mc_pmq_allocate(const double* phi, const double* w, const double* eps, int E, double alpha,
+                          double beta, double gamma, int total_bits, int* bits, double* objective) {
+  if (!phi || !w || !eps || !bits) return fail(MC_EINVAL, "NULL argument");
+  if (E < 2 || E > MC_MAX_EXPERTS) return fail(MC_EINVAL, "E=%d outside [2, %d]", E, MC_MAX_EXPERTS);
+  if (!(alpha >= 0.0) || !(beta >= 0.0) || !(gamma > 0.0) || !std::isfinite(alpha + beta + gamma))
+    return fail(MC_EINVAL, "exponents alpha=%g beta=%g gamma=%g (need alpha, beta >= 0, gamma > 0)", alpha,
+                beta, gamma);
+  if (total_bits < E + 3 || total_bits > 3 * E - 1)
+    return fail(MC_EINVAL, "total_bits=%d not reachable with one 3-bit and one 2-bit expert among %d "
+                "(range [%d, %d])", total_bits, E, E + 3, 3 * E - 1);
+  std::vector<double> term((size_t)E * 3);
+  for (int i = 0; i < E; ++i) {
+    if (!(phi[i] >= 0.0) || !(w[i] >= 0.0) || !std::isfinite(phi[i]) || !std::isfinite(w[i]))
+      return fail(MC_EINVAL, "expert %d: phi=%g w=%g must be finite and >= 0", i, phi[i], w[i]);
+    for (int b = 0; b < 3; ++b) {
+      const double e = eps[(size_t)i * 3 + b];
+      if (!(e >= 0.0) || !std::isfinite(e)) return fail(MC_EINVAL, "expert %d: eps[%d]=%g", i, b + 1, e);
+      term[(size_t)i * 3 + b] = std::pow(phi[i], alpha) * std::pow(w[i], beta) * std::pow(e, gamma);
+    }
+  }
+  const int S = 3 * E + 1;
+  const double inf = INFINITY;
+  // state (s, f): f bit 0 = some expert at 2 bits, bit 1 = some expert at 3 bits
+  std::vector<double> cost(S * 4, inf), ncost(S * 4);
+  std::vector<uint8_t> pre((size_t)S * 4 * E, 0), npre((size_t)S * 4 * E);
+  cost[0] = 0.0;
+  for (int i = 0; i < E; ++i) {
+    std::fill(ncost.begin(), ncost.end(), inf);
+    for (int s = 0; s <= 3 * i; ++s) {
+      for (int f = 0; f < 4; ++f) {
+        const double c = cost[s * 4 + f];
+        if (c == inf) continue;
+        const uint8_t* pp = &pre[((size_t)s * 4 + f) * E];
+        for (int b = 1; b <= 3; ++b) {
+          const int s2 = s + b, f2 = f | (b == 2 ? 1 : 0) | (b == 3 ? 2 : 0);
+          const double c2 = c + term[(size_t)i * 3 + b - 1];
+          double& dst = ncost[s2 * 4 + f2];
+          uint8_t* dp = &npre[((size_t)s2 * 4 + f2) * E];
+          bool better = c2 < dst;
+          if (!better && c2 == dst) {        // equal objective: the lexicographically smaller vector
+            int j = 0;
+            while (j < i && pp[j] == dp[j]) ++j;
+            better = (j < i) ? pp[j] < dp[j] : b < dp[i];
+          }
+          if (better) {
+            dst = c2;
+            std::memcpy(dp, pp, (size_t)i);
+            dp[i] = (uint8_t)b;
+          }
+        }
+      }
+    }
+    cost.swap(ncost);
+    pre.swap(npre);
+  }
+  const double best = cost[total_bits * 4 + 3];
+  if (best == inf) return fail(MC_EINVAL, "no allocation reaches total_bits=%d", total_bits);
+  const uint8_t* bp = &pre[((size_t)total_bits * 4 + 3) * E];
+  for (int i = 0; i < E; ++i) bits[i] = bp[i];
+  if (objective) *objective = best;
+  return MC_OK;
+}
+
 mc_status mc_timing_enable(int on) {
   mc::timing_enable(on);
   return MC_OK;

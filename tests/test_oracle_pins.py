@@ -575,3 +575,85 @@ def test_median_ratio_brute_force():
             order = sorted(range(E), key=lambda e: (-float(lg[t, e]), e))
             ratios.append(math.exp(float(lg[t, order[1]]) - float(lg[t, order[0]])))
         assert oracle.median_ratio(lg) == pytest.approx(statistics.median(ratios), rel=1e-15)
+
+
+# -------------------------------------------------------------------- PMQ ---
+
+def _pmq_gold():
+    sig, alloc = [], []
+    for r in _lines("pmq_small.txt"):
+        if r[0] == "significance":
+            lg = np.array([[float(v) for v in row.split()] for row in r[1].split(";")], np.float32)
+            sig.append((lg, int(r[2]), [float(v) for v in r[3].split()], [float(v) for v in r[4].split()]))
+        else:
+            eps = [[float(v) for v in row.split()] for row in r[3].split(";")]
+            alloc.append(([float(v) for v in r[1].split()], [float(v) for v in r[2].split()], eps,
+                          int(r[4]), [int(v) for v in r[5].split()], float(r[6]),
+                          [float(v) for v in r[7].split()]))
+    return sig, alloc
+
+
+def test_pmq_significance_hand_example():
+    """Sec. 3.2.1 frequencies and mean routing weights on a hand-worked case
+    (including an exact tie between two logits, lower index first)."""
+    sig, _ = _pmq_gold()
+    for lg, k, phi, w in sig:
+        got_phi, got_w = oracle.pmq_significance(lg, k)
+        np.testing.assert_allclose(got_phi, phi, rtol=0, atol=0)
+        np.testing.assert_allclose(got_w, w, rtol=1e-7, atol=1e-12)
+
+
+def test_pmq_significance_sums():
+    """Every token selects k experts whose weights sum to one."""
+    for cid, T in ((2, 300), (4, 200)):
+        c = synthetic.config(cid)
+        phi, w = oracle.pmq_significance(synthetic.logits(cid, T), c["k"])
+        assert phi.sum() == pytest.approx(c["k"], rel=1e-12)
+        assert w.sum() == pytest.approx(1.0, rel=1e-12)
+        assert (w <= phi + 1e-15).all() and (phi <= 1).all()
+
+
+def test_pmq_allocate_hand_examples():
+    _, alloc = _pmq_gold()
+    for phi, w, eps, total, bits, obj, (a, b, gm) in alloc:
+        for solve in (oracle.pmq_allocate_bruteforce, oracle.pmq_allocate):
+            got = solve(phi, w, eps, total, alpha=a, beta=b, gamma=gm)
+            assert got[0] == bits and got[1] == obj
+
+
+def test_pmq_allocate_matches_enumeration():
+    """The dynamic programme against the enumeration of every width vector,
+    on random instances (including exactly tied objectives and infeasible
+    totals)."""
+    g = np.random.default_rng(11)
+    for trial in range(150):
+        E = int(g.integers(2, 8))
+        phi = g.uniform(0, 1, E)
+        w = g.uniform(0, 1, E) * phi
+        eps = np.sort(g.uniform(0, 4, (E, 3)), axis=1)[:, ::-1]
+        if trial % 5 == 0:
+            eps[:] = eps[0]                      # identical experts: many exact ties
+            phi[:] = phi[0]
+            w[:] = w[0]
+        total = int(g.integers(E, 3 * E + 1))
+        a, b, gm = [(1, 1, 2), (1.5, 1.5, 2), (2, 1, 2), (1, 2, 2)][trial % 4]
+        bf = oracle.pmq_allocate_bruteforce(phi, w, eps, total, a, b, gm)
+        dp = oracle.pmq_allocate(phi, w, eps, total, a, b, gm)
+        assert bf == dp, (trial, bf, dp)
+        if bf is not None:
+            assert sum(bf[0]) == total and 3 in bf[0] and 2 in bf[0]
+        else:
+            assert total < E + 3 or total > 3 * E - 1
+
+
+def test_pmq_allocate_favours_significant_experts():
+    """With equal errors, the more significant (frequent, heavily weighted)
+    expert never gets fewer bits than a less significant one."""
+    g = np.random.default_rng(3)
+    for _ in range(30):
+        E = 6
+        phi = np.sort(g.uniform(0.05, 1, E))
+        w = phi * 0.5
+        eps = np.tile([4.0, 1.5, 0.5], (E, 1))
+        bits, _ = oracle.pmq_allocate(phi, w, eps, 13)
+        assert all(bits[i] <= bits[i + 1] for i in range(E - 1)), bits
