@@ -13,7 +13,7 @@ __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ 
                                                       size_t part_stride,
                                                       const int32_t* __restrict__ pair_pos,
                                                       const float* __restrict__ topk_w, int k, int d,
-                                                      const uint16_t* __restrict__ res,
+                                                      int P, const uint16_t* __restrict__ res,
                                                       uint16_t* __restrict__ y) {
   const int t = blockIdx.y;
   const int i = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
@@ -28,7 +28,7 @@ __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ 
   }
   for (int r = 0; r < k; ++r) {
     const int pos = pair_pos[(size_t)t * k + r];
-    if (pos < 0) continue;
+    if (pos < 0 || pos >= P) continue;
     const float w = topk_w[(size_t)t * k + r];
     f32x4 v[NSPLIT];
 #pragma unroll
@@ -145,7 +145,7 @@ static hipError_t launch_combine(const float* partial, size_t part_stride, int n
   const dim3 cgrid((d / 4 + 255) / 256, r.T);
 #define MC_COMBINE(S)                                                                              \
   hipLaunchKernelGGL(combine_kernel<S>, cgrid, dim3(256), 0, stream, partial, part_stride,         \
-                     r.pair_pos, r.topk_w, r.k, d, res, y)
+                     r.pair_pos, r.topk_w, r.k, d, r.T * r.k, res, y)
   switch (nsplit) {
     case 1: MC_COMBINE(1); break;
     case 2: MC_COMBINE(2); break;
@@ -175,6 +175,7 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
   const size_t P = (size_t)T * k;
   Hidden hid;
   hid.P = (int)P;
+  hid.T = T;
   hid.h = static_cast<uint16_t*>(ws);
   char* p = static_cast<char*>(ws) + round256(P * L.ffn * sizeof(uint16_t));
   hid.ksplit = forward_ksplit(T, r.E, k, L.d, L.ffn);

@@ -397,6 +397,7 @@ struct Hidden {
   uint16_t* h;           // [P][ffn] fp16
   float* gu_part;        // [ksplit][2][P][ffn] when ksplit > 1
   int P;                 // T * k
+  int T;
   int ksplit;
 };
 

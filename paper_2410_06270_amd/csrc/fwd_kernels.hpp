@@ -59,11 +59,12 @@ __attribute__((amdgpu_waves_per_eu(4))) gateup_kernel(
   const int e = blockIdx.y;
   const int chunk = blockIdx.z / hid.ksplit, split = blockIdx.z - chunk * hid.ksplit;
   const int t0 = chunk * 16 * NTMAX;
-  const int ce = counts[e];
+  int ebase, ce;
+  expert_range(counts, offsets, e, hid.P, ebase, ce);
   if (t0 >= ce) return;
   const int nt = (ce - t0) < 16 * NTMAX ? (ce - t0) : 16 * NTMAX;
-  const int pbase = offsets[e] + t0;
-  for (int i = threadIdx.x; i < nt; i += blockDim.x) toks[i] = pair_token[pbase + i];
+  const int pbase = ebase + t0;
+  for (int i = threadIdx.x; i < nt; i += blockDim.x) toks[i] = clamp_token(pair_token[pbase + i], hid.T);
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int K = L.d, G = L.G, ntiles = K / kTileCols;
   const int per = (ntiles + hid.ksplit - 1) / hid.ksplit;
@@ -132,10 +133,11 @@ __attribute__((amdgpu_waves_per_eu(4))) down_kernel(
   const int e = blockIdx.y;
   const int chunk = blockIdx.z / nsplit, split = blockIdx.z - chunk * nsplit;
   const int t0 = chunk * 16 * NTMAX;
-  const int ce = counts[e];
+  int ebase, ce;
+  expert_range(counts, offsets, e, hid.P, ebase, ce);
   if (t0 >= ce) return;
   const int nt = (ce - t0) < 16 * NTMAX ? (ce - t0) : 16 * NTMAX;
-  const int pbase = offsets[e] + t0;
+  const int pbase = ebase + t0;
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int K = L.ffn, G = L.G, ntiles = K / kTileCols;
   const int b = L.cum_bits[e + 1] - L.cum_bits[e];

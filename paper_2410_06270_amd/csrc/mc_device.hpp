@@ -174,6 +174,29 @@ __device__ __forceinline__ size_t layer_sz_offset(const LayerArgs& L, int e, int
   return (3 * (size_t)e + m) * ((size_t)L.d * (size_t)L.ffn / L.G);
 }
 
+// Kept-pair range [begin, begin + count) of expert e from the routing counts
+// and offsets, or an empty range when they are inconsistent with P = T*k
+// kept-pair slots, so that no index derived from them leaves its buffer.
+__device__ __forceinline__ void expert_range(const int32_t* counts, const int32_t* offsets, int e, int P,
+                                             int& begin, int& count) {
+  int c = counts[e], b = offsets[e];
+  if (c < 0 || b < 0 || c > P || b > P - c) c = b = 0;
+  begin = b;
+  count = c;
+}
+
+// The same range from the offsets alone (count = offsets[e+1] - offsets[e]).
+__device__ __forceinline__ void expert_range_offsets(const int32_t* offsets, int e, int P, int& begin,
+                                                     int& count) {
+  int b = offsets[e], c = offsets[e + 1] - b;
+  if (c < 0 || b < 0 || c > P || b > P - c) c = b = 0;
+  begin = b;
+  count = c;
+}
+
+// A token index from the routing lists, clamped into [0, T).
+__device__ __forceinline__ int clamp_token(int t, int T) { return t < 0 ? 0 : (t >= T ? T - 1 : t); }
+
 struct RouteArgs {
   const int32_t* counts;
   const int32_t* offsets;

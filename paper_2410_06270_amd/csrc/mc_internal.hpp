@@ -5,7 +5,7 @@
 
 namespace mc {
 
-constexpr int kRouteFusedMaxT = 256;   // up to this many tokens routing runs in one launch
+constexpr int kRouteFusedMaxT = 64;    // up to this many tokens routing runs in one launch
 constexpr int kDecodeMaxT = 64;        // up to this many tokens one workgroup holds all of an expert's tokens
 
 enum TimingSite {

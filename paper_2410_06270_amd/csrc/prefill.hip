@@ -14,11 +14,15 @@ extern template hipError_t launch_prefill_gemm<4>(const LayerArgs&, const int32_
 
 // One workgroup: per expert e (thread e), fragment rows ceil(M_e/32) and
 // 256-token m-tiles ceil(M_e/256), exclusive scans, and the tables.
+// Counts outside [0, P] are taken as 0, and tables that would not fit their
+// capacity are left empty (no m-tiles), so inconsistent routing cannot make
+// any later access leave its buffer.
 __global__ void __launch_bounds__(256) prefill_setup_kernel(const int32_t* __restrict__ counts, int E,
                                                             PrefillTables tb) {
   __shared__ int snf[256], snm[256];
   const int t = threadIdx.x;
-  const int c = t < E ? counts[t] : 0;
+  int c = t < E ? counts[t] : 0;
+  if (c < 0 || c > tb.P) c = 0;
   const int nf = (c + kPfFragRows - 1) / kPfFragRows;
   const int nm = (c + PfCfg::kTokens - 1) / PfCfg::kTokens;
   snf[t] = nf;
@@ -33,6 +37,12 @@ __global__ void __launch_bounds__(256) prefill_setup_kernel(const int32_t* __res
     __syncthreads();
   }
   const int fb = snf[t] - nf, mb = snm[t] - nm;
+  const bool fits = snf[255] <= tb.f_max && snm[255] <= tb.mt_max;
+  if (!fits) {
+    for (int i = t; i <= E; i += blockDim.x) tb.ftile_base[i] = 0;
+    if (t == 255) *tb.mt_count = 0;
+    return;
+  }
   if (t < E) {
     tb.ftile_base[t] = fb;
     for (int i = 0; i < nf; ++i) tb.ftile_e[fb + i] = t;
@@ -58,15 +68,18 @@ __global__ void __launch_bounds__(256) prefill_gather_kernel(const uint16_t* __r
   const int f = blockIdx.x;
   if (f >= tb.ftile_base[E]) return;
   const int e = tb.ftile_e[f];
-  const int pos0 = offsets[e] + (f - tb.ftile_base[e]) * kPfFragRows;
-  const int pend = offsets[e + 1];
+  int ebase, ecount;
+  expert_range_offsets(offsets, e, tb.P, ebase, ecount);
+  const int pos0 = ebase + (f - tb.ftile_base[e]) * kPfFragRows;
+  const int pend = ebase + ecount;
   const int ng = d / G;
   unsigned char* out = reinterpret_cast<unsigned char*>(xt);
   for (int idx = threadIdx.x; idx < kPfFragRows * ng; idx += blockDim.x) {
     const int m = idx % kPfFragRows, gi = idx / kPfFragRows;
     const int pos = pos0 + m;
     const bool valid = pos < pend;
-    const u32x4* src = valid ? reinterpret_cast<const u32x4*>(x + (size_t)pair_token[pos] * d + G * gi) : nullptr;
+    const u32x4* src =
+        valid ? reinterpret_cast<const u32x4*>(x + (size_t)clamp_token(pair_token[pos], tb.T) * d + G * gi) : nullptr;
     float sum = 0.0f;
     for (int q = 0; q < G / 8; ++q) {
       u32x4 v = {0u, 0u, 0u, 0u};
@@ -123,6 +136,8 @@ hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routin
   tb.mt_count = tb.mt_j + pl.mt_max;
   tb.f_max = pl.f_max;
   tb.mt_max = pl.mt_max;
+  tb.T = r.T;
+  tb.P = r.T * r.k;
   uint16_t* xt = reinterpret_cast<uint16_t*>(base + pl.x);
   float* xsum = reinterpret_cast<float*>(base + pl.xsum);
   uint16_t* ht = reinterpret_cast<uint16_t*>(base + pl.h);

@@ -72,6 +72,7 @@ struct PrefillTables {
   int32_t* mt_j;         // [mt_max] m-tile index within its expert
   int32_t* mt_count;     // [1] m-tiles in use
   int f_max, mt_max;
+  int T, P;              // tokens and kept-pair slots (T*k) of the routing
 };
 
 struct PrefillGemm {
@@ -398,8 +399,10 @@ prefill_kernel(LayerArgs L, const int32_t* __restrict__ offsets, PrefillTables t
     }
   } else {
     if (!active) return;
-    const int pbase = offsets[e] + S::kTokens * j;
-    const int pend = offsets[e + 1];
+    int ebase, ecount;
+    expert_range_offsets(offsets, e, tb.P, ebase, ecount);
+    const int pbase = ebase + S::kTokens * j;
+    const int pend = ebase + ecount;
     float* out = g.partial + (size_t)split * g.part_stride;
 #pragma unroll
     for (int t = 0; t < kPfWaveTiles; ++t) {

@@ -57,27 +57,47 @@ __device__ void select_token(const float* __restrict__ logits, const uint8_t* __
   const float* l = logits + (size_t)t * E;
   const int nj = (E + 63) >> 6;                      // logits per lane (wave-uniform)
   float lv[4];
-  uint32_t khi[4], klo[4];
+  unsigned long long key[4];
   int rank[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + 64 * j;
     lv[j] = (e < E) ? l[e] : 0.0f;
-    khi[j] = (e < E) ? ordered_bits(lv[j]) : 0u;
-    klo[j] = (e < E) ? (uint32_t)(0xffff - e) : 0u;
+  }
+  // the protection flag is loaded beside the logits (one memory round trip)
+  const int prot_flag = important != nullptr ? (int)important[t] : 0;
+  asm volatile("" ::"v"(lv[0]), "v"(lv[1]), "v"(lv[2]), "v"(lv[3]), "v"(prot_flag));
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + 64 * j;
+    key[j] = (e < E) ? (((unsigned long long)ordered_bits(lv[j]) << 32) | (unsigned)(0xffff - e)) : 0ull;
     rank[j] = 0;
   }
   for (int sj = 0; sj < nj; ++sj) {
     const int n = (E - 64 * sj) < 64 ? (E - 64 * sj) : 64;
-    for (int src = 0; src < n; ++src) {
-      const uint32_t ohi = __builtin_amdgcn_readlane(khi[sj], src);
-      const uint32_t olo = __builtin_amdgcn_readlane(klo[sj], src);
+    const unsigned long long ks = sj == 0 ? key[0] : sj == 1 ? key[1] : sj == 2 ? key[2] : key[3];
+    const uint32_t khs = (uint32_t)(ks >> 32), kls = (uint32_t)ks;
+    int src = 0;
+    for (; src + 4 <= n; src += 4) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const unsigned long long o =
+            ((unsigned long long)__builtin_amdgcn_readlane(khs, src + u) << 32) |
+            __builtin_amdgcn_readlane(kls, src + u);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (j < nj) rank[j] += o > key[j] ? 1 : 0;
+      }
+    }
+    for (; src < n; ++src) {
+      const unsigned long long o =
+          ((unsigned long long)__builtin_amdgcn_readlane(khs, src) << 32) | __builtin_amdgcn_readlane(kls, src);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        if (j < nj) rank[j] += (ohi > khi[j] || (ohi == khi[j] && olo > klo[j])) ? 1 : 0;
+        if (j < nj) rank[j] += o > key[j] ? 1 : 0;
     }
   }
-  const bool prot = important != nullptr && important[t] != 0;
+  const bool prot = prot_flag != 0;
   int my_e = 0;
   float my_l = 0.0f;
   float l0 = 0.0f, l1 = 0.0f;
@@ -255,33 +275,80 @@ __global__ void __launch_bounds__(kCsrThreads) route_scatter_kernel(
               pair_w, pair_pos);
 }
 
-// Small batches (T <= kRouteFusedMaxT): selection and lists in one launch, the
-// selection kept in LDS; global outputs are only written.
+// Small batches (T <= kRouteFusedMaxT = 64): one launch.  The waves select
+// tokens in parallel (the selection kept in LDS); then wave 0, one lane per
+// token, forms each token's mask of kept experts, counts every expert's
+// tokens with one ballot per expert (the ballots kept in LDS), scans the
+// counts, and writes each kept pair at its expert's offset plus the number of
+// earlier tokens with that expert -- lists in token order, no atomics.
 __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
     const float* __restrict__ logits, const uint8_t* __restrict__ important, int T, int E, int k,
     float delta32, double tau, int32_t* topk_idx, float* topk_w, uint8_t* kept, int32_t* counts,
     int32_t* offsets, int32_t* pair_token, int32_t* pair_rank, float* pair_w, int32_t* pair_pos,
     int32_t* n_pruned) {
+  static_assert(kRouteFusedMaxT <= 64, "one lane per token");
   __shared__ uint16_t ent[kRouteFusedMaxT * MC_MAX_TOPK];
   __shared__ float wsel[kRouteFusedMaxT * MC_MAX_TOPK];
   __shared__ int cnt[MC_MAX_EXPERTS];
   __shared__ int base[MC_MAX_EXPERTS];
+  __shared__ unsigned long long bal[MC_MAX_EXPERTS];
   const int wave = wave_id(), nwaves = blockDim.x >> 6, lane = threadIdx.x & 63;
   for (int t = wave; t < T; t += nwaves)
     select_token(logits, important, t, E, k, delta32, tau, topk_idx, topk_w, kept, pair_pos, ent,
                  wsel);
   __syncthreads();
-  for (int e = wave; e < E; e += nwaves) {
-    const int n = list_pass(0, e, 0, 0, T, k, ent, wsel, true, topk_w, pair_token, pair_rank,
-                            pair_w, pair_pos);
-    if (lane == 0) cnt[e] = n;
+  if (wave != 0) return;
+  const bool act = lane < T;
+  int my_e[MC_MAX_TOPK];
+  unsigned long long m[MC_MAX_EXPERTS / 64] = {0ull, 0ull, 0ull, 0ull};
+#pragma unroll
+  for (int r = 0; r < MC_MAX_TOPK; ++r) {
+    my_e[r] = 0xffff;
+    if (act && r < k) {
+      const int e = ent[lane * k + r];
+      my_e[r] = e;
+      if (e != 0xffff) {
+        const unsigned long long bit = 1ull << (e & 63);
+#pragma unroll
+        for (int j = 0; j < MC_MAX_EXPERTS / 64; ++j) m[j] |= (e >> 6) == j ? bit : 0ull;
+      }
+    }
   }
-  __syncthreads();
-  if (wave == 0) scan_counts(T, E, k, cnt, base, counts, offsets, n_pruned);
-  __syncthreads();
-  for (int e = wave; e < E; e += nwaves)
-    list_pass(1, e, base[e], 0, T, k, ent, wsel, true, topk_w, pair_token, pair_rank, pair_w,
-              pair_pos);
+  for (int e = lane; e < E; e += 64) cnt[e] = 0;
+#pragma unroll
+  for (int j = 0; j < MC_MAX_EXPERTS / 64; ++j) {
+    if (64 * j >= E) break;
+    // experts of this 64-block that some token selected (OR over the lanes)
+    unsigned long long any = m[j];
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t lo = __shfl_xor((uint32_t)any, off), hi = __shfl_xor((uint32_t)(any >> 32), off);
+      any |= ((unsigned long long)hi << 32) | lo;
+    }
+    any = ((unsigned long long)__builtin_amdgcn_readfirstlane((uint32_t)(any >> 32)) << 32) |
+          __builtin_amdgcn_readfirstlane((uint32_t)any);
+    while (any) {
+      const int i = __ffsll((long long)any) - 1;
+      any &= any - 1ull;
+      const unsigned long long b = __ballot((m[j] >> i) & 1ull);
+      if (lane == 0) {
+        cnt[64 * j + i] = __popcll(b);
+        bal[64 * j + i] = b;
+      }
+    }
+  }
+  scan_counts(T, E, k, cnt, base, counts, offsets, n_pruned);
+  const unsigned long long below = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int r = 0; r < MC_MAX_TOPK; ++r) {
+    const int e = my_e[r];
+    if (e != 0xffff) {
+      const int pos = base[e] + __popcll(bal[e] & below);
+      pair_token[pos] = lane;
+      pair_rank[pos] = r;
+      pair_w[pos] = wsel[lane * k + r];
+      pair_pos[lane * k + r] = pos;
+    }
+  }
 }
 
 hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,
