@@ -102,6 +102,24 @@ mc_status mc_pack_sizes(int E, int d, int ffn, const int *bits_host, int group,
 mc_status mc_pack(const float *w_gate, const float *w_up, const float *w_down,
                   const mc_layer *L, void *stream);
 
+/* Quantization method per expert for mc_pack_methods. */
+#define MC_QUANT_RTN 0    /* the min-max round-to-nearest quantizer of mc_pack */
+#define MC_QUANT_SIGN 1   /* 1-bit sign binarization (appendix A.2, Eq. 7-9) */
+
+/* mc_pack with a method per expert (method_host: host [E], NULL = all RTN).
+ * MC_QUANT_SIGN (1-bit experts only): code = 1 where w >= 0, else 0 (sign(0)
+ * = +1), and every group of each of the expert's matrices stores
+ *   s = fp16(2 * ||W||_1 / (rows * cols)),  z = 1/2,
+ * so the dequantized weight s*(code - z) is +-||W||_1 / (rows * cols): the
+ * binarized matrix times its scale (Eq. 7-9), and the forward computes
+ * s * (sum of x where code = 1 - sum of x where code = 0), Eq. 10.  ||W||_1
+ * is summed in fp64 (fixed order) and rounded once; 2*mean|W| above 65504
+ * saturates.  The layout is that of mc_pack; every other call is unchanged.
+ * Errors: as mc_pack, plus MC_EINVAL for an unknown method or a sign method
+ * on an expert wider than 1 bit. */
+mc_status mc_pack_methods(const float *w_gate, const float *w_up, const float *w_down,
+                          const mc_layer *L, const int *method_host, void *stream);
+
 /* Test surface: write the dequantized matrix `mat` (0 gate, 1 up, 2 down) of
  * expert e as row-major fp16 [R][K]; each value is the round-to-nearest-even
  * fp16 of the exact product s*(q - z) (one rounding).  out must hold R*K

@@ -9,6 +9,8 @@ What it computes (Mixture Compressor for MoE LLMs, ICLR 2025):
 
 * ``quantize``      -- Sec. 3.1 uniform asymmetric group quantizer (fp16 scale
   and zero, codes in [0, 2^b - 1], nearest level decided exactly);
+* ``quantize_sign`` -- appendix A.2 sign binarization of 1-bit experts, in
+  the same group format (scale 2 mean|W|, zero 1/2);
 * ``layout_pack`` / ``layout_unpack`` / ``pack_sz`` / ``unpack_sz`` -- the
   packed storage format, element by element from its index function;
 * ``dequant_f16`` / ``dequant_exact`` -- the dequantized value s*(q - z);
@@ -48,6 +50,8 @@ _lib = None
 # (see tests/test_oracle_pins.py); none is "parity unpinned".
 PINS = {
     "quantize": "Fraction brute force over all codes; level bound; range endpoints",
+    "quantize_sign": "Eq. 7-9: 2 code - 1 = sign(W) with sign(0) = +1; dequantized = +-mean|W| "
+                     "to fp16 rounding; Eq. 10 add/subtract form of the product",
     "layout_pack": "round trip, word-count closed form, hand-built words",
     "dequant_f16": "Fraction value rounded by numpy float16 (library RNE)",
     "route": "naive stable sort; tau=0 and protected no-op; k=2 gap == ratio rule",
@@ -251,8 +255,26 @@ def layer_offsets(E: int, d: int, ffn: int, bits, G: int):
     return words, szs, wo, so
 
 
-def pack_layer(mats, bits, G: int):
-    """mats[e] = (gate [ffn][d], up [ffn][d], down [d][ffn]) fp32.
+def quantize_sign(W: np.ndarray, G: int):
+    """Appendix A.2 (Eq. 7-9) in the group format: B = sign(W) with sign(0) =
+    +1, stored as B~ = (B + 1)/2 (code 1 where w >= 0, -0 included); one scale
+    for the matrix, s = ||W||_1 / (rows * cols), kept in every group as
+    fp16(2 s) (saturating) with zero 1/2, so that s16 * (code - 1/2) =
+    +-s16 / 2.  ||W||_1 is summed exactly (math.fsum) and rounded once."""
+    W = np.asarray(W, dtype=np.float32)
+    R, K = W.shape
+    q = (W >= 0).astype(np.uint8)
+    l1 = math.fsum(float(v) for v in np.abs(W).ravel())
+    s2 = 2.0 * (l1 / (R * K))
+    s16 = f16_round(min(s2, 65504.0))
+    s = np.full((R, K // G), s16, np.uint16)
+    z = np.full((R, K // G), 0x3800, np.uint16)          # fp16 0.5
+    return q, s, z
+
+
+def pack_layer(mats, bits, G: int, methods=None):
+    """mats[e] = (gate [ffn][d], up [ffn][d], down [d][ffn]) fp32; methods[e]
+    = 0 (min-max RTN, ``quantize``) or 1 (sign binarization, 1-bit experts).
     Returns (words uint32, sz uint32, logical) with logical[e][m] = (q, s, z)."""
     E = len(mats)
     ffn, d = mats[0][0].shape
@@ -263,7 +285,11 @@ def pack_layer(mats, bits, G: int):
     for e in range(E):
         per = []
         for m in range(3):
-            q, s, z = quantize(mats[e][m], int(bits[e]), G)
+            if methods is not None and methods[e] == 1:
+                assert int(bits[e]) == 1
+                q, s, z = quantize_sign(mats[e][m], G)
+            else:
+                q, s, z = quantize(mats[e][m], int(bits[e]), G)
             w = layout_pack(q, int(bits[e]))
             words[wofs[(e, m)]: wofs[(e, m)] + w.size] = w
             p = pack_sz(s, z, G)

@@ -7,6 +7,8 @@ library is not built -- there is no fallback.
 """
 from ._binding import (  # noqa: F401
     MCError,
+    QUANT_RTN,
+    QUANT_SIGN,
     PackedLayer,
     Routing,
     codes_export,

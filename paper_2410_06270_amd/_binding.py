@@ -62,6 +62,8 @@ def load():
         lib.mc_pack_sizes.argtypes = [I, I, I, P, I, ctypes.POINTER(S), ctypes.POINTER(S)]
         lib.mc_pack.restype = st
         lib.mc_pack.argtypes = [P, P, P, ctypes.POINTER(_Layer), P]
+        lib.mc_pack_methods.restype = st
+        lib.mc_pack_methods.argtypes = [P, P, P, ctypes.POINTER(_Layer), P, P]
         lib.mc_dequant_export.restype = st
         lib.mc_dequant_export.argtypes = [ctypes.POINTER(_Layer), I, I, P, P]
         lib.mc_codes_export.restype = st
@@ -162,11 +164,21 @@ class Routing:
             self.pair_rank, self.pair_w, self.pair_pos, self.n_pruned)])
 
 
-def pack(w_gate, w_up, w_down, layer: PackedLayer, stream=None):
+QUANT_RTN, QUANT_SIGN = 0, 1
+
+
+def pack(w_gate, w_up, w_down, layer: PackedLayer, stream=None, methods=None):
+    """Quantize and pack; methods (per expert, QUANT_RTN or QUANT_SIGN for
+    1-bit sign binarization) defaults to RTN everywhere."""
     for t in (w_gate, w_up, w_down):
         assert t.dtype == torch.float32 and t.is_contiguous() and t.is_cuda
-    _check(load().mc_pack(_ptr(w_gate), _ptr(w_up), _ptr(w_down), ctypes.byref(layer.desc),
-                          _stream(stream)))
+    if methods is None:
+        _check(load().mc_pack(_ptr(w_gate), _ptr(w_up), _ptr(w_down), ctypes.byref(layer.desc),
+                              _stream(stream)))
+    else:
+        arr = (ctypes.c_int * layer.E)(*[int(m) for m in methods])
+        _check(load().mc_pack_methods(_ptr(w_gate), _ptr(w_up), _ptr(w_down), ctypes.byref(layer.desc),
+                                      arr, _stream(stream)))
 
 
 def dequant_export(layer: PackedLayer, e: int, mat: int, out, stream=None):

@@ -73,6 +73,7 @@ mc::LayerArgs layer_args(const mc_layer* L) {
   a.cum_bits[0] = 0;
   for (int e = 0; e < L->E; ++e) a.cum_bits[e + 1] = (uint16_t)(a.cum_bits[e] + L->bits_host[e]);
   for (int e = L->E; e < MC_MAX_EXPERTS; ++e) a.cum_bits[e + 1] = a.cum_bits[e];
+  for (int i = 0; i < MC_MAX_EXPERTS / 32; ++i) a.sign_mask[i] = 0u;
   return a;
 }
 
@@ -104,16 +105,34 @@ mc_status mc_pack_sizes(int E, int d, int ffn, const int* bits_host, int group, 
   return MC_OK;
 }
 
-mc_status mc_pack(const float* w_gate, const float* w_up, const float* w_down, const mc_layer* L,
-                  void* stream) {
+mc_status mc_pack_methods(const float* w_gate, const float* w_up, const float* w_down, const mc_layer* L,
+                          const int* method_host, void* stream) {
   mc_status s = check_layer(L, true);
   if (s != MC_OK) return s;
   if (!w_gate || !w_up || !w_down) return fail(MC_EINVAL, "weight pointer is NULL");
+  mc::LayerArgs a = layer_args(L);
+  bool any_sign = false;
+  if (method_host) {
+    for (int e = 0; e < L->E; ++e) {
+      if (method_host[e] == MC_QUANT_SIGN) {
+        if (L->bits_host[e] != 1)
+          return fail(MC_EINVAL, "expert %d: sign binarization needs 1 bit, has %d", e, L->bits_host[e]);
+        a.sign_mask[e >> 5] |= 1u << (e & 31);
+        any_sign = true;
+      } else if (method_host[e] != MC_QUANT_RTN) {
+        return fail(MC_EINVAL, "expert %d: unknown quantization method %d", e, method_host[e]);
+      }
+    }
+  }
   (void)hipGetLastError();
-  const mc::LayerArgs a = layer_args(L);
-  return hip_status(mc::launch_pack(w_gate, w_up, w_down, a, static_cast<uint32_t*>(L->words),
-                                    L->sz, static_cast<hipStream_t>(stream)),
+  return hip_status(mc::launch_pack(w_gate, w_up, w_down, a, static_cast<uint32_t*>(L->words), L->sz, any_sign,
+                                    static_cast<hipStream_t>(stream)),
                     "mc_pack launch");
+}
+
+mc_status mc_pack(const float* w_gate, const float* w_up, const float* w_down, const mc_layer* L,
+                  void* stream) {
+  return mc_pack_methods(w_gate, w_up, w_down, L, nullptr, stream);
 }
 
 static mc_status export_common(const mc_layer* L, int e, int mat, void* out, bool dequant,

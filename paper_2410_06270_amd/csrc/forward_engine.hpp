@@ -117,10 +117,10 @@ __device__ __forceinline__ float sum8(u32x4 v) {
   return s;
 }
 
-// Group epilogue: tot += s 2^b * (acc - (1 + z 2^-b) * sum_a); acc = 0
-// (both scalings by powers of two are exact).
+// Group epilogue: tot += s 2^b * (acc - (1 + z 2^-b) * sum_a) (both scalings
+// by powers of two are exact).  The next group's first MFMA starts from zero.
 template <int BITS>
-__device__ __forceinline__ void group_end(f32x4& acc, f32x4& tot, uint32_t szw, const float* sx4p) {
+__device__ __forceinline__ void group_end(const f32x4& acc, f32x4& tot, uint32_t szw, const float* sx4p) {
   const float s = half_bits_to_float(szw & 0xffffu) * (float)(1 << BITS);
   const float c = fmaf(half_bits_to_float(szw >> 16), 1.0f / (float)(1 << BITS), 1.0f);
   const f32x4 sx = *reinterpret_cast<const f32x4*>(sx4p);
@@ -128,7 +128,6 @@ __device__ __forceinline__ void group_end(f32x4& acc, f32x4& tot, uint32_t szw, 
   for (int i = 0; i < 4; ++i) {
     const float t = fmaf(-c, sx[i], acc[i]);
     tot[i] = fmaf(s, t, tot[i]);
-    acc[i] = 0.0f;
   }
 }
 
@@ -270,11 +269,13 @@ __device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
     const u32x4 b0 = b_operand<BITS, F16>(w[0], u, magic);
     const u32x4 b1 = b_operand<BITS, F16>(w[1], u, magic);
     const int kk = lc * kTileCols + 32 * u;
+    const bool first = u % SPG == 0;     // first MFMA step of a group
+    const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int tb = 0; tb < NT; ++tb) {
       const u32x4 a = *reinterpret_cast<const u32x4*>(arow[tb] + kk);
-      acc[0][tb] = mfma16<F16>(a, b0, acc[0][tb]);
-      acc[1][tb] = mfma16<F16>(a, b1, acc[1][tb]);
+      acc[0][tb] = mfma16<F16>(a, b0, first ? zero : acc[0][tb]);
+      acc[1][tb] = mfma16<F16>(a, b1, first ? zero : acc[1][tb]);
     }
     if ((u + 1) % SPG == 0) {
       const int q = (u + 1) / SPG - 1;

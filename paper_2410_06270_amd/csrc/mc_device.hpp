@@ -161,7 +161,12 @@ struct LayerArgs {
   const uint32_t* sz;
   int E, d, ffn, G;
   uint16_t cum_bits[MC_MAX_EXPERTS + 1];   // prefix sums of the expert widths
+  uint32_t sign_mask[MC_MAX_EXPERTS / 32]; // bit e: expert e is sign-binarized (1 bit)
 };
+
+__device__ __forceinline__ bool expert_is_sign(const LayerArgs& L, int e) {
+  return (L.sign_mask[e >> 5] >> (e & 31)) & 1u;
+}
 
 // Word offset of matrix m (0 gate, 1 up, 2 down) of expert e.
 __device__ __forceinline__ size_t layer_word_offset(const LayerArgs& L, int e, int m) {

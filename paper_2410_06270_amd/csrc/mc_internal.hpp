@@ -20,8 +20,9 @@ int timing_site(const char* name);
 hipError_t timing_read(int site, double* total_ms, int* launches);
 void timing_enable(int on);
 
+// any_sign: some expert of L.sign_mask is sign-binarized.
 hipError_t launch_pack(const float* wg, const float* wu, const float* wd, const LayerArgs& L,
-                       uint32_t* words, uint32_t* sz, hipStream_t stream);
+                       uint32_t* words, uint32_t* sz, bool any_sign, hipStream_t stream);
 hipError_t launch_export(const uint32_t* words, const uint32_t* sz, int bits, int R, int K, int G,
                          bool dequant, void* out, hipStream_t stream);
 hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,

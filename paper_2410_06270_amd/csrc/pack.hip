@@ -5,6 +5,11 @@
 // Per group of G inputs of one row, L = 2^b - 1:
 //   s = fp16(fp32(max - min) / L) (1.0 if it rounds to zero), z = fp16(-min / s),
 //   code = nearest level s*(j - z), ties to the even j, decided exactly in fp64.
+// Sign binarization (appendix A.2, Eq. 7-9; 1-bit experts that ask for it):
+// code = 1 where w >= 0, else 0, and every group of the matrix gets
+// s = fp16(2 * ||W||_1 / (rows * cols)), z = 1/2, so that s*(code - z) =
+// +-||W||_1 / (rows * cols) -- the binarized weight times its scale, in the same
+// packed format (the kernels' product is then Eq. 10's add/subtract form).
 #include "mc_internal.hpp"
 
 namespace mc {
@@ -97,6 +102,7 @@ __global__ void __launch_bounds__(256) pack_codes_kernel(const float* __restrict
   const int G = L.G, ng = K / G;
   const int b = L.cum_bits[e + 1] - L.cum_bits[e];
   const int Lc = (1 << b) - 1;
+  const bool sign = expert_is_sign(L, e);
   const float* W = (m == 0) ? wg : (m == 1) ? wu : wd;
   const float* row = W + (size_t)e * L.d * L.ffn + (size_t)n * K;
   const uint32_t* szm = sz + layer_sz_offset(L, e, m);
@@ -112,7 +118,7 @@ __global__ void __launch_bounds__(256) pack_codes_kernel(const float* __restrict
     const float4 c = reinterpret_cast<const float4*>(row + k0)[1];
     const float v[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
     for (int j = 0; j < 8; ++j) {
-      const uint32_t code = (uint32_t)nearest_code(v[j], s, z, Lc);
+      const uint32_t code = sign ? (v[j] >= 0.0f ? 1u : 0u) : (uint32_t)nearest_code(v[j], s, z, Lc);
       const int i = 4 * u + (j >> 1), h = j & 1;
       if (b == 1) {
         w[0] |= code << (16 * h + i);
@@ -127,6 +133,79 @@ __global__ void __launch_bounds__(256) pack_codes_kernel(const float* __restrict
   }
   uint32_t* dst = words_out + layer_word_offset(L, e, m) + ((size_t)tile * 64 + lane) * b;
   for (int p = 0; p < b; ++p) dst[p] = w[p];
+}
+
+// ------------------------------------------------------- sign binarization --
+// ||W||_1 of every sign-binarized matrix: kSignParts partial sums in fp64 per
+// matrix (each over a contiguous slice, fixed order inside the block), kept
+// in the matrix's own scale/zero words (overwritten by the finish kernel).
+constexpr int kSignThreads = 256;
+
+__host__ __device__ inline int sign_parts(long long groups_per_matrix) {
+  // partials (8 bytes = 2 words each) fit in the matrix's scale/zero words
+  const long long cap = groups_per_matrix / 2;
+  return (int)(cap < 1 ? 1 : (cap < 1024 ? cap : 1024));
+}
+
+__device__ __forceinline__ double block_sum_f64(double v, double* red) {
+  for (int off = 1; off < 64; off <<= 1) v += __shfl_xor(v, off);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double t = 0.0;
+  for (int w = 0; w < kSignThreads / 64; ++w) t += red[w];
+  return t;
+}
+
+// grid (parts, 3E matrices); matrices of other experts exit at once.
+__global__ void __launch_bounds__(kSignThreads) sign_l1_kernel(const float* __restrict__ wg,
+                                                               const float* __restrict__ wu,
+                                                               const float* __restrict__ wd, LayerArgs L,
+                                                               uint32_t* __restrict__ sz) {
+  __shared__ double red[kSignThreads / 64];
+  const int e = blockIdx.y / 3, m = blockIdx.y % 3;
+  if (!expert_is_sign(L, e)) return;
+  const long long n4 = (long long)L.d * L.ffn / 4;                    // float4 pieces
+  const long long gpm = (long long)L.d * L.ffn / L.G;
+  const int parts = sign_parts(gpm);
+  const int part = blockIdx.x;
+  if (part >= parts) return;
+  const long long per = (n4 + parts - 1) / parts;
+  const long long b0 = part * per, b1 = (b0 + per) < n4 ? (b0 + per) : n4;
+  const float* W = ((m == 0) ? wg : (m == 1) ? wu : wd) + (size_t)e * L.d * L.ffn;
+  double acc = 0.0;
+  for (long long i = b0 + threadIdx.x; i < b1; i += kSignThreads) {
+    const float4 v = reinterpret_cast<const float4*>(W)[i];
+    acc += (double)fabsf(v.x) + (double)fabsf(v.y) + (double)fabsf(v.z) + (double)fabsf(v.w);
+  }
+  const double t = block_sum_f64(acc, red);
+  if (threadIdx.x == 0) {             // two 32-bit words (the buffer is only 4-byte aligned)
+    const unsigned long long b = __double_as_longlong(t);
+    uint32_t* dst = sz + layer_sz_offset(L, e, m) + 2 * (size_t)part;
+    dst[0] = (uint32_t)b;
+    dst[1] = (uint32_t)(b >> 32);
+  }
+}
+
+// One workgroup per matrix of a binarized expert: adds the partials in order,
+// then writes the scale/zero word of every group.
+__global__ void __launch_bounds__(kSignThreads) sign_finish_kernel(LayerArgs L, uint32_t* __restrict__ sz) {
+  __shared__ double red[kSignThreads / 64];
+  const int e = blockIdx.x / 3, m = blockIdx.x % 3;
+  if (!expert_is_sign(L, e)) return;
+  const long long gpm = (long long)L.d * L.ffn / L.G;
+  const int parts = sign_parts(gpm);
+  uint32_t* dst = sz + layer_sz_offset(L, e, m);
+  double acc = 0.0;
+  const int per = (parts + kSignThreads - 1) / kSignThreads;
+  for (int i = threadIdx.x * per; i < (threadIdx.x + 1) * per && i < parts; ++i)
+    acc += __longlong_as_double((long long)(((unsigned long long)dst[2 * i + 1] << 32) | dst[2 * i]));
+  const double l1 = block_sum_f64(acc, red);             // every partial read before any write
+  double s2 = 2.0 * (l1 / ((double)L.d * (double)L.ffn));
+  if (s2 > 65504.0) s2 = 65504.0;
+  const uint32_t word = (uint32_t)double_to_half_rne(s2) | (0x3800u << 16);   // z = 1/2
+  __syncthreads();
+  for (long long i = threadIdx.x; i < gpm; i += kSignThreads) dst[i] = word;
 }
 
 // ------------------------------------------------------------------ export --
@@ -169,7 +248,7 @@ __global__ void __launch_bounds__(256) export_kernel(const uint32_t* __restrict_
 // ---------------------------------------------------------------- launchers --
 
 hipError_t launch_pack(const float* wg, const float* wu, const float* wd, const LayerArgs& L,
-                       uint32_t* words, uint32_t* sz, hipStream_t stream) {
+                       uint32_t* words, uint32_t* sz, bool any_sign, hipStream_t stream) {
   const long long groups = 3LL * L.E * L.d * L.ffn / L.G;
   const int lpg = L.G / 4 < 64 ? L.G / 4 : 64;
   const long long waves = (groups + (64 / lpg) - 1) / (64 / lpg);
@@ -177,6 +256,11 @@ hipError_t launch_pack(const float* wg, const float* wu, const float* wd, const 
   timing_begin(stream, kSitePackSz);
   hipLaunchKernelGGL(pack_sz_kernel, dim3((unsigned)blocks_sz), dim3(256), 0, stream, wg, wu, wd,
                      L, sz, groups);
+  if (any_sign) {
+    const int parts = sign_parts((long long)L.d * L.ffn / L.G);
+    hipLaunchKernelGGL(sign_l1_kernel, dim3(parts, 3 * L.E), dim3(kSignThreads), 0, stream, wg, wu, wd, L, sz);
+    hipLaunchKernelGGL(sign_finish_kernel, dim3(3 * L.E), dim3(kSignThreads), 0, stream, L, sz);
+  }
   timing_end(stream, kSitePackSz);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;

@@ -166,6 +166,19 @@ def test_pack_rejects(lib):
     assert lib.mc_codes_export(ctypes.byref(L), 0, 3, P(5), None) == 1
 
 
+def test_pack_methods_rejects(lib):
+    """Sign binarization is a 1-bit method; unknown method codes are refused
+    (both checks run before any launch)."""
+    P = ctypes.c_void_p
+    L, _keep = _fake_layer(bits=(1, 1, 2, 3, 2, 2, 2, 3))
+    m = (ctypes.c_int * 8)(0, 0, 1, 0, 0, 0, 0, 0)            # expert 2 has 2 bits
+    assert lib.mc_pack_methods(P(1), P(2), P(3), ctypes.byref(L), m, None) == 1
+    m = (ctypes.c_int * 8)(1, 7, 0, 0, 0, 0, 0, 0)            # 7 is no method
+    assert lib.mc_pack_methods(P(1), P(2), P(3), ctypes.byref(L), m, None) == 1
+    m = (ctypes.c_int * 8)(1, 1, 0, 0, 0, 0, 0, 0)
+    assert lib.mc_pack_methods(None, P(2), P(3), ctypes.byref(L), m, None) == 1
+
+
 def test_importance_rejects(lib):
     """Shape, rho, NULL and workspace checks of mc_token_importance (no launch)."""
     P = ctypes.c_void_p

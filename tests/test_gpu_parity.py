@@ -31,14 +31,14 @@ def u32(t):
     return t.cpu().numpy().view(np.uint32)
 
 
-def pack_gpu(mc, mats, bits, G):
+def pack_gpu(mc, mats, bits, G, methods=None):
     E = len(mats)
     ffn, d = mats[0][0].shape
     wg = to_dev(np.stack([m[0] for m in mats]))
     wu = to_dev(np.stack([m[1] for m in mats]))
     wd = to_dev(np.stack([m[2] for m in mats]))
     L = mc.PackedLayer(E, d, ffn, bits, G)
-    mc.pack(wg, wu, wd, L)
+    mc.pack(wg, wu, wd, L, methods=methods)
     torch.cuda.synchronize()
     return L
 
@@ -404,3 +404,65 @@ def test_importance_large(mc, H, L, d):
     I, m = importance_gpu(mc, A, xb, 0.02)
     np.testing.assert_allclose(I, I_ref, rtol=2e-5)
     np.testing.assert_array_equal(m, m_ref)
+
+
+# ------------------------------------------------------ sign binarization ---
+
+def _sign_layer(d, ffn):
+    mats = synthetic.layer_weights(1, E=4, d=d, ffn=ffn)
+    mats[0][0][0, :16] = 0.0
+    mats[0][0][1, :16] = -0.0
+    mats[0][2][3, :] = np.abs(mats[0][2][3, :])
+    return mats, [1, 1, 2, 3], [1, 0, 0, 0]
+
+
+@pytest.mark.parametrize("d,ffn,G", [(256, 512, 32), (512, 1024, 128)])
+def test_pack_sign_binarization_bit_exact(mc, d, ffn, G):
+    """Appendix A.2 sign binarization of a 1-bit expert beside RTN experts:
+    packed words and scale/zero words bit for bit, exported codes and fp16
+    dequantized values."""
+    mats, bits, methods = _sign_layer(d, ffn)
+    words, sz, logical = oracle.pack_layer(mats, bits, G, methods=methods)
+    L = pack_gpu(mc, mats, bits, G, methods)
+    assert (u32(L.words) == words).all()
+    assert (u32(L.sz) == sz).all()
+    for m in range(3):
+        q, s, z = logical[0][m]
+        R, K = q.shape
+        out = torch.empty((R, K), dtype=torch.int16, device="cuda")
+        mc.dequant_export(L, 0, m, out)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(out.cpu().numpy().view(np.uint16), oracle.dequant_f16(q, s, z, G).view(np.uint16))
+
+
+@pytest.mark.parametrize("T", [8, 130])
+def test_forward_sign_binarized(mc, T):
+    """Forward with a sign-binarized expert (decode and prefill paths)."""
+    d, ffn, G = 512, 1024, 128
+    mats, bits, methods = _sign_layer(d, ffn)
+    _, _, logical = oracle.pack_layer(mats, bits, G, methods=methods)
+    L = pack_gpu(mc, mats, bits, G, methods)
+    x = synthetic.activations(1, T, d=d)
+    lg = synthetic.logits(1, T)
+    lg[:, 0] += 1.0                                   # route plenty of tokens to the binarized expert
+    imp = synthetic.important_mask(1, T)
+    r = mc.Routing(T, 4, 2)
+    mc.route_and_prune(to_dev(lg), to_dev(imp), 0.3, r)
+    y = torch.empty((T, d), dtype=torch.int16, device="cuda")
+    ws = torch.empty(mc.forward_workspace(T, 4, 2, d, ffn), dtype=torch.uint8, device="cuda")
+    mc.moe_forward(to_dev(x.view(np.int16)), r, L, y, ws)
+    torch.cuda.synchronize()
+    ref = oracle.route(lg, imp, 2, 0.3)
+    assert ref["counts"][0] > 0
+    y_ref = oracle.moe_forward(x, ref, logical, G)
+    g = oracle.bf16_to_float64(y.cpu().numpy().view(np.uint16))
+    mae = float(np.abs(g - oracle.bf16_to_float64(oracle.bf16_round_array(y_ref))).mean())
+    rms = float(np.sqrt((y_ref ** 2).mean()))
+    maxrel = float((np.abs(g - y_ref) / np.maximum(np.abs(y_ref), rms)).max())
+    assert mae <= 1e-3 and maxrel <= 2e-2, (mae, maxrel)
+
+
+def test_pack_sign_rejects_wide_expert(mc):
+    mats, bits, _ = _sign_layer(256, 512)
+    with pytest.raises(mc.MCError):
+        pack_gpu(mc, mats, bits, 32, [0, 0, 1, 0])      # expert 2 has 2 bits

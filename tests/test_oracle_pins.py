@@ -657,3 +657,57 @@ def test_pmq_allocate_favours_significant_experts():
         eps = np.tile([4.0, 1.5, 0.5], (E, 1))
         bits, _ = oracle.pmq_allocate(phi, w, eps, 13)
         assert all(bits[i] <= bits[i + 1] for i in range(E - 1)), bits
+
+
+# ------------------------------------------------------ sign binarization ---
+
+def _sign_matrix(seed=4, R=32, K=256):
+    g = np.random.default_rng(seed)
+    W = (g.standard_normal((R, K)) * 0.02).astype(np.float32)
+    W[0, :8] = 0.0
+    W[1, :8] = -0.0
+    W[2, :] = np.abs(W[2, :])
+    return W
+
+
+def test_sign_binarization_eq7_to_9():
+    """B = sign(W) with sign(0) = +1 (Eq. 8); B~ = (B + 1)/2 (Eq. 9); the
+    dequantized weight is the sign times the scale mean|W| (up to the fp16
+    rounding of the stored 2 * mean|W|)."""
+    W = _sign_matrix()
+    q, s, z = oracle.quantize_sign(W, 32)
+    B = np.where(W >= 0, 1, -1)                    # numpy: -0 >= 0 is True
+    np.testing.assert_array_equal(2 * q.astype(int) - 1, B)
+    assert (q[1, :8] == 1).all() and (q[0, :8] == 1).all()
+    deq = oracle.dequant_exact(q, s, z, 32)
+    mean_abs = float(np.abs(W.astype(np.float64)).mean())
+    assert np.all(np.abs(np.abs(deq) - mean_abs) <= mean_abs * 2.0 ** -11)
+    assert len(np.unique(np.abs(deq))) == 1
+    np.testing.assert_array_equal(np.sign(deq), B)
+    # the dequantized fp16 value is exactly half the stored scale
+    np.testing.assert_array_equal(oracle.dequant_f16(q, s, z, 32).view(np.uint16) & 0x7fff,
+                                  (s.max() - 0x400) * np.ones_like(q, dtype=np.uint16))
+
+
+def test_sign_binarization_product_is_eq10():
+    """x . (s B) = s * (sum of x where B~ = 1 - sum of x where B~ = 0), Eq. 10."""
+    W = _sign_matrix(seed=9, R=16, K=128)
+    q, s, z = oracle.quantize_sign(W, 32)
+    deq = oracle.dequant_exact(q, s, z, 32)
+    x = np.random.default_rng(2).standard_normal((5, 128))
+    scale = abs(deq[0, 0])
+    want = np.stack([scale * (x @ (q[i] == 1) - x @ (q[i] == 0)) for i in range(16)], axis=1)
+    np.testing.assert_allclose(x @ deq.T, want, rtol=1e-12, atol=1e-14)
+
+
+def test_pack_layer_mixed_methods():
+    """A layer with a sign-binarized 1-bit expert beside RTN experts packs each
+    expert by its own method; the RTN experts are unchanged."""
+    mats = synthetic.layer_weights(1, E=3, d=256, ffn=512)
+    words0, sz0, lg0 = oracle.pack_layer(mats, [1, 1, 2], 32)
+    words1, sz1, lg1 = oracle.pack_layer(mats, [1, 1, 2], 32, methods=[1, 0, 0])
+    for m in range(3):
+        for a, b in zip(lg0[1][m], lg1[1][m]):
+            np.testing.assert_array_equal(a, b)
+        np.testing.assert_array_equal(lg1[0][m][2], 0x3800)
+        np.testing.assert_array_equal(lg1[0][m][0], (mats[0][m] >= 0).astype(np.uint8))
