@@ -10,8 +10,9 @@ line: decode at 1 and 8 tokens, prefill of 4096 tokens with the threshold
 swept over {0, 0.2, 0.4} (pruned fraction, tokens/s, MFMA fraction of the
 algorithmic 6*d*ffn FLOPs per kept pair), and the OLMoE-shaped layer (d=2048,
 ffn=1024, 64 experts, top-8, G=64, Zipf-skewed logits, threshold 0.05) in
-decode (16 tokens) and prefill (2048 tokens), and the token importance that
-marks the protected tokens (32 heads, 4096 tokens, rho = 0.02).
+decode (16 tokens) and prefill (2048 tokens), the token importance that
+marks the protected tokens (32 heads, 4096 tokens, rho = 0.02), the router
+logits ahead of routing, and the 32-layer residual stack.
 
 One step = route_and_prune + moe_forward over the batch for one layer.  The
 step rotates over packed copies of the layer (4 x 484 MB Mixtral, 3 x 131 MB
@@ -51,6 +52,7 @@ def parse():
     p.add_argument("--no-olmoe", action="store_true", help="skip the OLMoE-shaped layer")
     p.add_argument("--no-importance", action="store_true", help="skip the token-importance measurement")
     p.add_argument("--no-stack", action="store_true", help="skip the 32-layer stack")
+    p.add_argument("--no-router", action="store_true", help="skip the router-logits measurement")
     p.add_argument("--stack-steps", type=int, default=10)
     p.add_argument("--graph", action="store_true",
                    help="also time HIP-graph replays of the step (reported as ms_per_step_graph)")
@@ -328,6 +330,44 @@ def importance_entry(mc, torch, steps, warmup):
                 kernels_us={k: round(v, 2) for k, v in kus.items()})
 
 
+def router_entry(mc, torch, synthetic, steps, warmup):
+    """Router logits (x W_r^T in fp64 sums, one fp32 rounding) at the Mixtral
+    (d=4096, 8 experts) and OLMoE (d=2048, 64 experts) shapes, decode and
+    prefill token counts.  x rotates over copies totalling >= 512 MB when one
+    copy is large, so prefill-sized x comes from HBM.  Algorithmic bytes per
+    launch: x (2*T*d) + W_r (2*E*d) + logits (4*T*E); fp64 work T*E*d
+    multiply-adds (peak 78.6 TFLOP/s)."""
+    FP64_PEAK_TFLOPS = 78.6
+    runs = []
+    for cid, T in ((2, 32), (3, 4096), (4, 16), (4, 2048)):
+        c = synthetic.config(cid)
+        d, E = c["d"], c["E"]
+        w = torch.from_numpy(synthetic.router_weights(cid).view("int16")).cuda()
+        x0 = torch.from_numpy(synthetic.activations(cid, T).view("int16")).cuda()
+        n = max(1, min(64, -(-(512 << 20) // (2 * T * d)))) if 2 * T * d > (8 << 20) else 1
+        xs = [x0] + [x0.clone() for _ in range(n - 1)]
+        out = torch.empty((T, E), dtype=torch.float32, device="cuda")
+        for i in range(warmup):
+            mc.router_logits(xs[i % n], w, out)
+        torch.cuda.synchronize()
+        mc.timing_enable(True)
+        for i in range(steps):
+            mc.router_logits(xs[i % n], w, out)
+        torch.cuda.synchronize()
+        t, cnt = mc.timing_read("router")
+        mc.timing_enable(False)
+        us = 1e3 * t / max(cnt, 1)
+        alg = 2 * T * d + 2 * E * d + 4 * T * E
+        tflops = 2.0 * T * E * d / (us * 1e-6) / 1e12
+        runs.append(dict(workload=c["name"], tokens=T, d=d, experts=E, x_copies=n, kernel_us=round(us, 2),
+                         alg_bytes=alg, hbm_gbs=round(alg / (us * 1e3), 1),
+                         hbm_frac=round(alg / (us * 1e3) / HBM_PEAK_GBS, 4),
+                         fp64_tflops=round(tflops, 2), fp64_frac=round(tflops / FP64_PEAK_TFLOPS, 4)))
+        del xs, x0, w, out
+        torch.cuda.empty_cache()
+    return dict(kernel="router", runs=runs)
+
+
 def stack_entry(mc, torch, synthetic, steps, warmup):
     """The 32-layer Mixtral-shaped expert stack resident in HBM: 32 packed
     layers (widths [3,3,3,2,2,2,2,3] in a seeded order per layer, weights
@@ -511,6 +551,8 @@ def main():
                         "decode": dec, "prefill": prefill_entry(wo, ms_p, kus)}
     if not args.no_importance:
         out["importance"] = importance_entry(mc, torch, 20, 3)
+    if not args.no_router:
+        out["router"] = router_entry(mc, torch, synthetic, 50, 5)
     if not args.no_stack:
         out["stack"] = stack_entry(mc, torch, synthetic, args.stack_steps, 2)
     if not args.no_cpu:

@@ -9,6 +9,7 @@
  * inference path:
  *
  *   mc_pack            fp32 expert weights -> packed codes + fp16 scale/zero
+ *   mc_router_logits   the router's linear layer: x -> router logits
  *   mc_route_and_prune router logits -> top-k, Eq. 5 pruning, protection,
  *                      per-expert token lists (CSR)
  *   mc_moe_forward     Eq. 1 over the packed SwiGLU experts
@@ -150,6 +151,20 @@ typedef struct mc_routing {
   int32_t *n_pruned;     /* [1] number of pruned pairs */
 } mc_routing;
 
+/* Router logits, the scores whose top-k Eq. 1 takes:
+ *   logits[t][e] = sum_k x[t][k] * w_router[e][k]
+ * x: [T][d] bf16 (the MoE layer input), w_router: [E][d] bf16, both 16-byte
+ * aligned; logits: [T][E] fp32.  Every product is exact in fp64, the d
+ * products are summed in fp64 and the sum is rounded once to fp32, so each
+ * logit lies between the fp32 roundings of S - g and S + g, with S the exact
+ * sum and g = (d - 1) 2^-53 sum_k |x_k w_k|: the correctly rounded value
+ * except when S is that close to an fp32 rounding boundary.  Deterministic.
+ * Limits: 1 <= T <= MC_MAX_TOKENS, 1 <= E <= 256, d a positive multiple of 8.
+ * Errors: MC_EINVAL (shape, NULL or misaligned pointer), MC_EUNSUPPORTED
+ * (T above MC_MAX_TOKENS), MC_EHIP. */
+mc_status mc_router_logits(const uint16_t *x_bf16, const uint16_t *w_router_bf16, int T, int d, int E,
+                           float *logits, void *stream);
+
 /* Top-k routing with Online Dynamic Pruning (Eq. 1, Eq. 5, token protection).
  * logits: [T][E] fp32, finite.  important: [T] uint8, nonzero = protected
  * (may be NULL: no token protected).  threshold tau in [0, 1] acts on the
@@ -267,7 +282,7 @@ mc_status mc_pmq_allocate(const double *phi, const double *w, const double *eps,
  * events of one kernel and returns the summed duration in ms and the number
  * of launches.  Kernel names: pack_scale_zero, pack_codes, export,
  * route_fused, route_select, route_lists, prefill_prep, gateup, down, combine,
- * importance_colsum, importance_finish, importance_select, rmsnorm.
+ * importance_colsum, importance_finish, importance_select, rmsnorm, router.
  * Errors: MC_EINVAL (unknown name, NULL pointer), MC_EHIP. */
 mc_status mc_timing_enable(int on);
 mc_status mc_timing_read(const char *kernel, double *total_ms, int *launches);

@@ -14,6 +14,8 @@ What it computes (Mixture Compressor for MoE LLMs, ICLR 2025):
 * ``layout_pack`` / ``layout_unpack`` / ``pack_sz`` / ``unpack_sz`` -- the
   packed storage format, element by element from its index function;
 * ``dequant_f16`` / ``dequant_exact`` -- the dequantized value s*(q - z);
+* ``router_logits`` -- the router's linear layer x W_r^T whose top-k Eq. 1
+  takes, each logit the exact sum rounded once to fp32;
 * ``route``         -- Eq. 1 top-k, Eq. 5 pruning, Sec. 3.3.2 protection and
   the per-expert token lists;
 * ``moe_forward``   -- Eq. 1 over SwiGLU experts on exact dequantized weights;
@@ -54,6 +56,8 @@ PINS = {
                      "to fp16 rounding; Eq. 10 add/subtract form of the product",
     "layout_pack": "round trip, word-count closed form, hand-built words",
     "dequant_f16": "Fraction value rounded by numpy float16 (library RNE)",
+    "router_logits": "Fraction sums rounded to the nearest fp32 by exact distance; hand cases "
+                     "with cancellation, fp32 ties and double-rounding traps; fp64 matmul within 1 ulp",
     "route": "naive stable sort; tau=0 and protected no-op; k=2 gap == ratio rule",
     "moe_forward": "E=1,k=1 equals numpy SwiGLU; tau=0 all-protected dense top-k; linearity",
     "rms_norm": "torch.nn.functional.rms_norm in float64; scale invariance; unit mean square",
@@ -300,6 +304,41 @@ def pack_layer(mats, bits, G: int, methods=None):
 
 
 # ---------------------------------------------------------------- routing ---
+
+def _round_f32(terms) -> float:
+    """The fp32 nearest to the exact sum of the fp64 values ``terms`` (ties to
+    even); a zero sum is +0.  math.fsum gives s, the fp64 nearest to the sum,
+    and the fp64 nearest to the remainder (so its sign); the cast of s to fp32
+    is then correct except when s falls exactly halfway between two fp32
+    values, where the remainder's sign decides."""
+    s = math.fsum(terms)
+    if s == 0.0:
+        return 0.0
+    r = math.fsum(list(terms) + [-s])
+    f = np.float32(s)
+    if float(f) == s or r == 0.0:
+        return float(f)
+    lo = np.nextafter(f, np.float32(-np.inf)) if float(f) > s else f
+    hi = np.nextafter(lo, np.float32(np.inf))
+    if (float(lo) + float(hi)) / 2.0 != s:        # not a midpoint: the cast is right
+        return float(f)
+    return float(hi) if r > 0.0 else float(lo)
+
+
+def router_logits(x_bits: np.ndarray, w_bits: np.ndarray, tokens=None) -> np.ndarray:
+    """Router scores whose top-k Eq. 1 takes: logits[t][e] = sum_k x[t][k] *
+    W_r[e][k] for bf16 x [T][d] and W_r [E][d] (bit patterns), each the exact
+    sum rounded once to fp32 (bf16 products are exact in fp64).  ``tokens``
+    restricts the rows computed (others stay 0)."""
+    x = bf16_to_float64(x_bits)
+    w = bf16_to_float64(w_bits)
+    T, E = x.shape[0], w.shape[0]
+    out = np.zeros((T, E), dtype=np.float32)
+    for t in (range(T) if tokens is None else tokens):
+        for e in range(E):
+            out[t, e] = _round_f32((x[t] * w[e]).tolist())
+    return out
+
 
 def prune_delta(tau: float) -> float:
     """fp32 threshold on the logit gap l_0 - l_1 equivalent to p_1 < tau at k = 2:

@@ -24,6 +24,7 @@ from ._binding import (  # noqa: F401
     pmq_allocate,
     pmq_significance,
     route_and_prune,
+    router_logits,
     stack_forward,
     stack_workspace,
     timing_enable,

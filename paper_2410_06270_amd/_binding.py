@@ -68,6 +68,8 @@ def load():
         lib.mc_dequant_export.argtypes = [ctypes.POINTER(_Layer), I, I, P, P]
         lib.mc_codes_export.restype = st
         lib.mc_codes_export.argtypes = [ctypes.POINTER(_Layer), I, I, P, P]
+        lib.mc_router_logits.restype = st
+        lib.mc_router_logits.argtypes = [P, P, I, I, I, P, P]
         lib.mc_route_and_prune.restype = st
         lib.mc_route_and_prune.argtypes = [P, P, ctypes.c_float, ctypes.POINTER(_Routing), P]
         lib.mc_forward_workspace.restype = st
@@ -189,6 +191,16 @@ def dequant_export(layer: PackedLayer, e: int, mat: int, out, stream=None):
 def codes_export(layer: PackedLayer, e: int, mat: int, out, stream=None):
     assert out.dtype == torch.uint8 and out.is_contiguous()
     _check(load().mc_codes_export(ctypes.byref(layer.desc), e, mat, _ptr(out), _stream(stream)))
+
+
+def router_logits(x, w_router, logits, stream=None):
+    """x [T][d], w_router [E][d]: bf16 (or int16 bit patterns); logits [T][E] fp32."""
+    assert x.is_contiguous() and w_router.is_contiguous() and logits.is_contiguous()
+    assert x.element_size() == 2 and w_router.element_size() == 2 and logits.dtype == torch.float32
+    T, d = x.shape
+    E = w_router.shape[0]
+    assert w_router.shape[1] == d and tuple(logits.shape) == (T, E)
+    _check(load().mc_router_logits(_ptr(x), _ptr(w_router), T, d, E, _ptr(logits), _stream(stream)))
 
 
 def route_and_prune(logits, important, threshold: float, routing: Routing, stream=None):

@@ -169,6 +169,20 @@ static float prune_delta32(double tau) {
   return (float)std::log((1.0 - tau) / tau);
 }
 
+mc_status mc_router_logits(const uint16_t* x_bf16, const uint16_t* w_router_bf16, int T, int d, int E,
+                           float* logits, void* stream) {
+  if (T < 1 || E < 1 || E > MC_MAX_EXPERTS || d < 8 || d % 8 != 0)
+    return fail(MC_EINVAL, "bad shape T=%d d=%d E=%d (d a positive multiple of 8, E <= %d)", T, d, E,
+                MC_MAX_EXPERTS);
+  if (T > MC_MAX_TOKENS) return fail(MC_EUNSUPPORTED, "T=%d above %d", T, MC_MAX_TOKENS);
+  if (!x_bf16 || !w_router_bf16 || !logits) return fail(MC_EINVAL, "x, w_router or logits is NULL");
+  if ((reinterpret_cast<uintptr_t>(x_bf16) | reinterpret_cast<uintptr_t>(w_router_bf16)) & 15u)
+    return fail(MC_EINVAL, "x and w_router must be 16-byte aligned");
+  (void)hipGetLastError();
+  return hip_status(mc::launch_router(x_bf16, w_router_bf16, T, d, E, logits, static_cast<hipStream_t>(stream)),
+                    "mc_router_logits launch");
+}
+
 mc_status mc_route_and_prune(const float* logits, const uint8_t* important, float threshold,
                              const mc_routing* r, void* stream) {
   mc_status s = check_routing(r);

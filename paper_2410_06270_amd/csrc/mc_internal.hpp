@@ -11,7 +11,7 @@ constexpr int kDecodeMaxT = 64;        // up to this many tokens one workgroup h
 enum TimingSite {
   kSitePackSz, kSitePackCodes, kSiteExport, kSiteRouteFused, kSiteRouteSelect, kSiteRouteLists,
   kSiteGateUp, kSiteDown, kSiteCombine, kSitePrefillPrep, kSiteImpColsum, kSiteImpFinish, kSiteImpSelect,
-  kSiteRmsNorm,
+  kSiteRmsNorm, kSiteRouter,
   kNumSites
 };
 void timing_begin(hipStream_t stream, int site);
@@ -47,6 +47,9 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
 constexpr double kRmsNormEps = 1e-5;
 hipError_t launch_rmsnorm(const uint16_t* h, int T, int d, double eps, uint16_t* xn, hipStream_t stream);
 size_t stack_workspace_bytes(int T, int E, int k, int d, int ffn);   // xn [T][d] + forward workspace
+// logits [T][E] fp32 = x [T][d] . w [E][d]^T (bf16), fp64 sums rounded once.
+hipError_t launch_router(const uint16_t* x, const uint16_t* w, int T, int d, int E, float* logits,
+                         hipStream_t stream);
 size_t importance_workspace_bytes(int H, int L);
 hipError_t launch_importance(const uint16_t* attn, int H, int L, const uint16_t* x, int d, float rho,
                              float* importance, uint8_t* mask, void* ws, hipStream_t stream);

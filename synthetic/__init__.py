@@ -26,6 +26,8 @@ Workloads (the paper's Mixtral 8x7b and OLMoE shapes; no dataset is used):
                  prefill T=1024, tau=0.3.
 
 Weights are N(0, 0.02^2) fp32, activations N(0,1) rounded once to bfloat16,
+router weights [E][d] N(0, 1/d) rounded to bfloat16 (unit-variance logits on
+such activations),
 and round(0.1*T) tokens (a seeded permutation) are marked important.
 Attention maps (the input of token importance) are causal row softmaxes of
 scores N(0, 1.5^2) with +4 on the first key (an attention sink), rounded to
@@ -51,7 +53,7 @@ CONFIGS = {
 }
 
 # stream ids inside a config's seed
-_S_X, _S_BIAS, _S_LOGITS, _S_MASK, _S_BITS, _S_ATTN = 1, 2, 3, 4, 5, 6
+_S_X, _S_BIAS, _S_LOGITS, _S_MASK, _S_BITS, _S_ATTN, _S_ROUTER = 1, 2, 3, 4, 5, 6, 7
 _S_WEIGHT = 1000
 _S_LAYER = 100000       # stream offset per layer of a stack (config 5)
 
@@ -128,6 +130,15 @@ def logits(config_id: int, T: int, E=None) -> np.ndarray:
         offset = np.log(p[perm])
     g = rng(config_id, _S_LOGITS + 100 * T)
     return (g.standard_normal(size=(T, E)) + offset[None, :]).astype(np.float32)
+
+
+def router_weights(config_id: int, E=None, d=None) -> np.ndarray:
+    """Router weight W_r [E][d] ~ N(0, 1/d) rounded to bfloat16: uint16 bits."""
+    c = CONFIGS[config_id]
+    E = c["E"] if E is None else E
+    d = c["d"] if d is None else d
+    g = rng(config_id, _S_ROUTER)
+    return to_bf16_bits(g.standard_normal(size=(E, d), dtype=np.float32) / np.float32(np.sqrt(d)))
 
 
 def important_mask(config_id: int, T: int, frac: float = 0.1) -> np.ndarray:

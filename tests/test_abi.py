@@ -252,3 +252,17 @@ def test_pmq_allocate_matches_oracle(lib):
         pmq_allocate([1, 1, 1], [1, 1, 1], [[1, 1, 1]] * 3, 5)       # 5 < E + 3
     with pytest.raises(MCError):
         pmq_allocate([1, -1, 1], [1, 1, 1], [[1, 1, 1]] * 3, 7)
+
+
+def test_router_rejects(lib):
+    """Shape, NULL and alignment checks of mc_router_logits (no launch)."""
+    P = ctypes.c_void_p
+    f = lib.mc_router_logits
+    assert f(P(0x100), P(0x200), 0, 4096, 8, P(0x300), None) == 1          # T < 1
+    assert f(P(0x100), P(0x200), 4, 4100, 8, P(0x300), None) == 1          # d % 8
+    assert f(P(0x100), P(0x200), 4, 4096, 0, P(0x300), None) == 1          # E < 1
+    assert f(P(0x100), P(0x200), 4, 4096, 257, P(0x300), None) == 1        # E > 256
+    assert f(None, P(0x200), 4, 4096, 8, P(0x300), None) == 1
+    assert f(P(0x100), P(0x200), 4, 4096, 8, None, None) == 1
+    assert f(P(0x108), P(0x200), 4, 4096, 8, P(0x300), None) == 1          # x not 16-byte aligned
+    assert f(P(0x100), P(0x200), 65537, 4096, 8, P(0x300), None) == 4      # above MC_MAX_TOKENS

@@ -1,0 +1,137 @@
+"""GPU parity of the router's linear layer (logits = x W_r^T, the scores whose
+top-k Eq. 1 takes) through the C-ABI against the oracle.
+
+The kernel sums the exact fp64 products in fp64 and rounds once to fp32; the
+oracle rounds the exact sum.  The bar, derived from that arithmetic: with s
+the fp64 sum and g = (d - 1) 2^-53 sum |x_k w_k| the fp64 summation bound,
+a logit must equal the oracle's bit for bit wherever the exact sum lies
+farther than g from both fp32 rounding boundaries around the oracle's value,
+and be within one fp32 ulp of it everywhere.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synthetic
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def mc():
+    import paper_2410_06270_amd as m
+    m.load()
+    return m
+
+
+def to_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def router_gpu(mc, x_bits, w_bits):
+    T, E = x_bits.shape[0], w_bits.shape[0]
+    out = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    mc.router_logits(to_dev(x_bits.view(np.int16)), to_dev(w_bits.view(np.int16)), out)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def assert_faithful(got, x_bits, w_bits, tokens):
+    x = oracle.bf16_to_float64(x_bits)
+    w = oracle.bf16_to_float64(w_bits)
+    d = x.shape[1]
+    ref = oracle.router_logits(x_bits, w_bits, tokens=tokens)
+    exact = ambiguous = 0
+    for t in tokens:
+        for e in range(w.shape[0]):
+            p = (x[t] * w[e]).tolist()
+            s = math.fsum(p)
+            g = (d - 1) * 2.0 ** -53 * math.fsum(abs(v) for v in p) + 2.0 ** -1074
+            f = np.float32(ref[t, e])
+            lo = (float(np.nextafter(f, np.float32(-np.inf))) + float(f)) / 2
+            hi = (float(f) + float(np.nextafter(f, np.float32(np.inf)))) / 2
+            a, b = np.float32(got[t, e]), f
+            assert abs(float(a) - float(b)) <= float(np.spacing(np.abs(b))), (t, e, a, b)
+            if abs(s - lo) > 2 * g and abs(s - hi) > 2 * g:
+                assert a.view(np.uint32) == b.view(np.uint32) or (a == 0 and b == 0), (t, e, a, b)
+                exact += 1
+            else:
+                ambiguous += 1
+    return exact, ambiguous
+
+
+def sample_tokens(T, n=24, seed=0):
+    if T <= n:
+        return list(range(T))
+    g = np.random.default_rng(seed)
+    return sorted({0, T - 1, *g.choice(T, n - 2, replace=False).tolist()})
+
+
+@pytest.mark.parametrize("cid,T,d,E", [
+    (1, 5, 256, 4), (1, 64, 256, 4), (1, 1029, 256, 4),       # tiny shape, ragged token tails
+    (2, 1, 4096, 8), (2, 32, 4096, 8), (2, 257, 4096, 8),     # Mixtral decode / first 4-token path
+    (3, 4096, 4096, 8),                                       # Mixtral prefill (sampled)
+    (4, 16, 2048, 64), (4, 2048, 2048, 64),                   # OLMoE decode / prefill (sampled)
+    (1, 3, 8, 13),                                            # smallest d, experts not a multiple of 8
+])
+def test_router_logits_parity(mc, cid, T, d, E):
+    x = synthetic.activations(cid, T, d=d)
+    w = synthetic.router_weights(cid, E=E, d=d)
+    got = router_gpu(mc, x, w)
+    assert np.isfinite(got).all()
+    exact, ambiguous = assert_faithful(got, x, w, sample_tokens(T))
+    assert exact >= 0.9 * (exact + ambiguous)      # logits near 0 have a fine fp32 grid
+
+
+def _row(v, d=8):
+    a = np.zeros((1, d), np.float32)
+    a[0, :len(v)] = v
+    return (a.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def test_router_logits_hand_cases(mc):
+    """Cancellation that a running fp32 sum would lose is exact; a sum that sits
+    2^-80 above an fp32 midpoint (which fp64 accumulation cannot see) comes out
+    as one of its two fp32 neighbours, within the bar."""
+    x = np.concatenate([_row([1, 1, 1]), _row([1, 2 ** -12, 2 ** -40]), _row([0.0, -0.0])])
+    w = np.concatenate([_row([2.0 ** 30, 1, -(2.0 ** 30)]), _row([1, 2 ** -12, 2 ** -40]),
+                        _row([-3.0, 5.0])])
+    got = router_gpu(mc, x, w)
+    assert got[0, 0] == 1.0
+    assert got[1, 1] in (np.float32(1.0), np.float32(1.0 + 2.0 ** -23))
+    assert got[2, 2] == 0.0
+    assert_faithful(got, x, w, [0, 1, 2])
+
+
+def test_router_then_route_mixtral(mc):
+    """Router logits feed route_and_prune directly: the routing from the GPU
+    logits equals the oracle's routing from the oracle's logits."""
+    T, k, tau = 32, 2, 0.3
+    x = synthetic.activations(2, T)
+    w = synthetic.router_weights(2)
+    imp = synthetic.important_mask(2, T)
+    lg = torch.empty((T, 8), dtype=torch.float32, device="cuda")
+    mc.router_logits(to_dev(x.view(np.int16)), to_dev(w.view(np.int16)), lg)
+    r = mc.Routing(T, 8, k)
+    mc.route_and_prune(lg, to_dev(imp), tau, r)
+    torch.cuda.synchronize()
+    ref_logits = oracle.router_logits(x, w)
+    np.testing.assert_array_equal(lg.cpu().numpy(), ref_logits)
+    ref = oracle.route(ref_logits, imp, k, tau)
+    np.testing.assert_array_equal(r.topk_idx.cpu().numpy(), ref["topk_idx"])
+    np.testing.assert_array_equal(r.kept.cpu().numpy(), ref["kept"])
+    np.testing.assert_array_equal(r.counts.cpu().numpy(), ref["counts"])
+    n = int(ref["offsets"][-1])
+    np.testing.assert_array_equal(r.pair_token.cpu().numpy()[:n], ref["pair_token"][:n])
+
+
+def test_router_logits_rejects(mc):
+    x = torch.zeros((4, 12), dtype=torch.int16, device="cuda")        # d not a multiple of 8
+    w = torch.zeros((8, 12), dtype=torch.int16, device="cuda")
+    out = torch.empty((4, 8), dtype=torch.float32, device="cuda")
+    with pytest.raises(mc.MCError):
+        mc.router_logits(x, w, out)

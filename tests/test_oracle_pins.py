@@ -711,3 +711,85 @@ def test_pack_layer_mixed_methods():
             np.testing.assert_array_equal(a, b)
         np.testing.assert_array_equal(lg1[0][m][2], 0x3800)
         np.testing.assert_array_equal(lg1[0][m][0], (mats[0][m] >= 0).astype(np.uint8))
+
+
+# ----------------------------------------------------------- router GEMM ---
+
+def _bf(v):
+    """bf16 bit patterns of values that bfloat16 holds exactly."""
+    a = np.asarray(v, dtype=np.float32)
+    b = (a.view(np.uint32) >> 16).astype(np.uint16)
+    assert ((b.astype(np.uint32) << 16).view(np.float32) == a).all()
+    return b.reshape(1, -1)
+
+
+def _nearest_f32(S: Fraction) -> int:
+    """fp32 bits nearest to the rational S by exact distance, ties to an even
+    significand, a zero sum as +0 (brute force over the neighbours)."""
+    if S == 0:
+        return 0
+    f = np.float32(float(S))
+    cands = {f, np.nextafter(f, np.float32(np.inf)), np.nextafter(f, np.float32(-np.inf))}
+    best = None
+    for c in cands:
+        if not np.isfinite(c):
+            continue
+        dist = abs(Fraction(float(c)) - S)
+        key = (dist, int(np.array(c, np.float32).view(np.uint32)) & 1)
+        if best is None or key < best[0]:
+            best = (key, c)
+    return int(np.array(best[1], np.float32).view(np.uint32))
+
+
+def _logit_bits(xv, wv):
+    return int(oracle.router_logits(_bf(xv), _bf(wv)).view(np.uint32)[0, 0])
+
+
+@pytest.mark.parametrize("x,w,want", [
+    ([1, 1, 1], [2.0 ** 30, 1, -(2.0 ** 30)], 0x3F800000),        # cancellation: exactly 1
+    ([1, 2 ** -12, 2 ** -40], [1, 2 ** -12, 2 ** -40], 0x3F800001),  # just above a midpoint
+    ([1, 2 ** -12, 2 ** -40], [1, 2 ** -12, -(2 ** -40)], 0x3F800000),  # just below it
+    ([1, 2 ** -12], [1, 2 ** -12], 0x3F800000),                    # exact tie, even is 1.0
+    ([1, 2 ** -12, 2 ** -12], [1, 2 ** -11, 2 ** -12], 0x3F800002),   # 1 + 3 2^-24: tie, even is 1 + 2^-22
+    ([-1, 2 ** -12, 2 ** -40], [1, -(2 ** -12), 2 ** -40], 0xBF800000),  # -(1 + 2^-24) + 2^-80 -> -1
+    ([2 ** -75, 2 ** -125], [2 ** -75, 2 ** -125], 0x00000001),    # 2^-150 + 2^-250: subnormal rounds up
+    ([2 ** -75], [2 ** -75], 0x00000000),                          # 2^-150 alone: tie to +0
+    ([0.0, -0.0], [-3.0, 5.0], 0x00000000),                        # zero sum is +0
+])
+def test_router_logits_hand_cases(x, w, want):
+    """Each logit is the exact sum rounded once to fp32: cancellation that a
+    running fp32 sum loses, ties to even, and sums that fp64 rounds onto an
+    fp32 midpoint (where a fp64-then-fp32 cast rounds the wrong way)."""
+    assert _logit_bits(x, w) == want
+
+
+def test_router_logits_nearest_by_exact_distance():
+    """Random rows built to land near fp32 rounding boundaries, against the
+    nearest fp32 of the rational sum found by brute force."""
+    g = np.random.default_rng(5)
+    for _ in range(300):
+        n = int(g.integers(2, 24))
+        e = g.integers(-30, 10, n)
+        m = g.integers(128, 256, n) / 128.0
+        xv = (m * 2.0 ** e * g.choice([-1, 1], n)).astype(np.float32)
+        wv = (g.integers(128, 256, n) / 128.0 * 2.0 ** g.integers(-20, 5, n)).astype(np.float32)
+        if g.random() < 0.5:
+            xv *= np.float32(2.0 ** -45)       # the rest below fp64's resolution at 1
+        xv[0], wv[0] = 1.0, 1.0
+        if n > 2:
+            xv[1], wv[1] = 2.0 ** -12, float(g.choice([-1, 1])) * 2.0 ** -12   # half an ulp of 1
+        S = sum(Fraction(float(a)) * Fraction(float(b)) for a, b in zip(xv, wv))
+        assert _logit_bits(xv, wv) == _nearest_f32(S)
+
+
+def test_router_logits_matches_fp64_matmul():
+    """Mixtral-shaped rows: within one fp32 ulp of numpy's fp64 product cast to
+    fp32, and equal to it almost everywhere (a transposed operand fails)."""
+    x = synthetic.activations(2, 6)
+    w = synthetic.router_weights(2)
+    got = oracle.router_logits(x, w)
+    ref = (oracle.bf16_to_float64(x) @ oracle.bf16_to_float64(w).T).astype(np.float32)
+    ulp = np.spacing(np.abs(ref))
+    assert (np.abs(got - ref) <= ulp).all()
+    assert (got == ref).mean() > 0.95
+    assert 0.5 < float(got.std()) < 2.0                    # unit-variance logits by construction
