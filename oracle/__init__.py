@@ -14,6 +14,10 @@ What it computes (Mixture Compressor for MoE LLMs, ICLR 2025):
 * ``layout_pack`` / ``layout_unpack`` / ``pack_sz`` / ``unpack_sz`` -- the
   packed storage format, element by element from its index function;
 * ``dequant_f16`` / ``dequant_exact`` -- the dequantized value s*(q - z);
+* ``gptq_hessian`` / ``gptq_quantize`` -- the GPTQ quantizer the paper uses
+  (Sec. 3.1; H = 2 X^T X, columns quantized in order, each column's error
+  compensated on the columns after it through the upper Cholesky factor of
+  H^-1), with the group parameters of the Sec. 3.1 quantizer;
 * ``router_logits`` -- the router's linear layer x W_r^T whose top-k Eq. 1
   takes, each logit the exact sum rounded once to fp32;
 * ``route``         -- Eq. 1 top-k, Eq. 5 pruning, Sec. 3.3.2 protection and
@@ -56,6 +60,10 @@ PINS = {
                      "to fp16 rounding; Eq. 10 add/subtract form of the product",
     "layout_pack": "round trip, word-count closed form, hand-built words",
     "dequant_f16": "Fraction value rounded by numpy float16 (library RNE)",
+    "gptq_factor": "U^T U H = I; upper triangular with positive diagonal; dead inputs; damping scale",
+    "gptq_quantize": "H = c I reduces to RTN bit for bit; two-column closed form (w1 + rho (w0 - q0)); "
+                     "loss identity d H d^T = sum e^2; error below RTN's on correlated inputs; dead inputs",
+    "codes_for": "equals the quantizer's own codes when the parameters come from the same values",
     "router_logits": "Fraction sums rounded to the nearest fp32 by exact distance; hand cases "
                      "with cancellation, fp32 ties and double-rounding traps; fp64 matmul within 1 ulp",
     "route": "naive stable sort; tau=0 and protected no-op; k=2 gap == ratio rule",
@@ -304,6 +312,103 @@ def pack_layer(mats, bits, G: int, methods=None):
 
 
 # ---------------------------------------------------------------- routing ---
+
+def codes_for(w32: np.ndarray, s16: np.ndarray, z16: np.ndarray, bits: int) -> np.ndarray:
+    """Nearest level code of each fp32 value w under fp16 scale/zero bits
+    (one per value): the number of level midpoints s*(j + 1/2 - z) below w,
+    the even neighbour when w is exactly on a midpoint (midpoints are exact
+    in fp64)."""
+    L = (1 << bits) - 1
+    w = np.asarray(w32, dtype=np.float32).astype(np.float64)
+    s = np.asarray(s16, np.uint16).view(np.float16).astype(np.float64)
+    z = np.asarray(z16, np.uint16).view(np.float16).astype(np.float64)
+    below = np.zeros(w.shape, np.int64)
+    for j in range(L):
+        below += (s * ((j + 0.5) - z) < w)
+    on_mid = (below < L) & (below % 2 == 1) & (s * ((below + 0.5) - z) == w)
+    return (below + on_mid).astype(np.uint8)
+
+
+def gptq_hessian(x_bits: np.ndarray) -> np.ndarray:
+    """H = 2 X^T X (fp64) from calibration inputs X [N][K] (bf16 bits): the
+    Hessian in W of the layer-wise error ||W X^T - Q X^T||^2 (Sec. 3.1)."""
+    X = bf16_to_float64(x_bits)
+    return 2.0 * (X.T @ X)
+
+
+def _f32_margin(w64: np.ndarray) -> np.ndarray:
+    """Relative distance of each fp64 value to the nearest fp32 rounding
+    boundary (how far it is from rounding to another fp32)."""
+    f = w64.astype(np.float32)
+    up = np.nextafter(f, np.float32(np.inf)).astype(np.float64)
+    dn = np.nextafter(f, np.float32(-np.inf)).astype(np.float64)
+    fd = f.astype(np.float64)
+    dist = np.minimum(np.abs(w64 - (fd + up) / 2), np.abs(w64 - (fd + dn) / 2))
+    return dist / np.maximum(np.abs(w64), 1e-300)
+
+
+def gptq_factor(H: np.ndarray, damp: float = 0.01):
+    """The factor GPTQ quantizes with, from the Hessian H [K][K] (fp64):
+    inputs with H_kk = 0 are dead (H_kk := 1; their weights are zeroed);
+    H += damp * mean(diag H) * I; U = the upper-triangular Cholesky factor of
+    H^-1 (H^-1 = U^T U).  Returns (U [K][K] fp64, dead [K] uint8)."""
+    H = np.array(H, dtype=np.float64, copy=True)
+    K = H.shape[0]
+    dead = np.diag(H) == 0.0
+    H[dead, dead] = 1.0
+    H[np.diag_indices(K)] += damp * np.mean(np.diag(H))
+    U = np.linalg.cholesky(np.linalg.inv(H)).T
+    return np.triu(U), dead.astype(np.uint8)
+
+
+def gptq_quantize_u(W: np.ndarray, U: np.ndarray, dead: np.ndarray, bits: int, G: int):
+    """GPTQ on one matrix W [R][K] (rows = outputs, K = inputs) with the
+    factor U of ``gptq_factor``, in fp64.  Dead inputs get weight 0; then for
+    k = 0 .. K-1 (columns in order):
+      at a group start, s and z come from the Sec. 3.1 quantizer on the fp32
+      rounding of the group's current (already compensated) values;
+      q_k = nearest level of fp32(w_k);  e_k = (w_k - s (q_k - z)) / U_kk;
+      w_j -= e_k U_kj for every j > k.
+    Returns (q [R][K] uint8, s16 [R][K/G], z16 [R][K/G], loss [R] = sum e_k^2
+    / 2, margin [R]): margin is the smallest, over the row's decisions, of the
+    relative distance of w_k to an fp32 rounding boundary and of fp32(w_k) to a
+    level midpoint (in units of s); a row with a tiny margin can round the
+    other way under a different fp64 summation order."""
+    W = np.asarray(W, dtype=np.float32)
+    R, K = W.shape
+    Wk = W.astype(np.float64)
+    Wk[:, np.asarray(dead, bool)] = 0.0
+    L = (1 << bits) - 1
+    q = np.zeros((R, K), np.uint8)
+    s = np.zeros((R, K // G), np.uint16)
+    z = np.zeros((R, K // G), np.uint16)
+    loss = np.zeros(R)
+    margin = np.full(R, np.inf)
+    for k in range(K):
+        g = k // G
+        if k % G == 0:
+            _, sg, zg = quantize(Wk[:, k:k + G].astype(np.float32), bits, G)
+            s[:, g], z[:, g] = sg[:, 0], zg[:, 0]
+            sf = s[:, g].view(np.float16).astype(np.float64)
+            zf = z[:, g].view(np.float16).astype(np.float64)
+        w64 = Wk[:, k]
+        w32 = w64.astype(np.float32)
+        qk = codes_for(w32, s[:, g], z[:, g], bits)
+        q[:, k] = qk
+        mids = sf[:, None] * ((np.arange(L) + 0.5)[None, :] - zf[:, None])
+        dmid = np.abs(w32.astype(np.float64)[:, None] - mids).min(axis=1) / sf
+        margin = np.minimum(margin, np.minimum(_f32_margin(w64), dmid))
+        err = (w64 - sf * (qk.astype(np.float64) - zf)) / U[k, k]
+        Wk[:, k + 1:] -= np.outer(err, U[k, k + 1:])
+        loss += err * err / 2.0
+    return q, s, z, loss, margin
+
+
+def gptq_quantize(W: np.ndarray, H: np.ndarray, bits: int, G: int, damp: float = 0.01):
+    """GPTQ from the Hessian: ``gptq_quantize_u`` with ``gptq_factor(H, damp)``."""
+    U, dead = gptq_factor(H, damp)
+    return gptq_quantize_u(W, U, dead, bits, G)
+
 
 def _round_f32(terms) -> float:
     """The fp32 nearest to the exact sum of the fp64 values ``terms`` (ties to

@@ -27,7 +27,9 @@ Workloads (the paper's Mixtral 8x7b and OLMoE shapes; no dataset is used):
 
 Weights are N(0, 0.02^2) fp32, activations N(0,1) rounded once to bfloat16,
 router weights [E][d] N(0, 1/d) rounded to bfloat16 (unit-variance logits on
-such activations),
+such activations), calibration inputs for GPTQ [N][K] with correlated
+channels (rank-8 N(0,1) factors plus N(0, 0.5^2) noise) and per-channel
+scales exp(N(0, 0.5^2)), 1 % of channels x8 (outlier features), in bfloat16,
 and round(0.1*T) tokens (a seeded permutation) are marked important.
 Attention maps (the input of token importance) are causal row softmaxes of
 scores N(0, 1.5^2) with +4 on the first key (an attention sink), rounded to
@@ -54,6 +56,7 @@ CONFIGS = {
 
 # stream ids inside a config's seed
 _S_X, _S_BIAS, _S_LOGITS, _S_MASK, _S_BITS, _S_ATTN, _S_ROUTER = 1, 2, 3, 4, 5, 6, 7
+_S_CALIB = 500          # + tag: calibration inputs of one matrix
 _S_WEIGHT = 1000
 _S_LAYER = 100000       # stream offset per layer of a stack (config 5)
 
@@ -139,6 +142,19 @@ def router_weights(config_id: int, E=None, d=None) -> np.ndarray:
     d = c["d"] if d is None else d
     g = rng(config_id, _S_ROUTER)
     return to_bf16_bits(g.standard_normal(size=(E, d), dtype=np.float32) / np.float32(np.sqrt(d)))
+
+
+def calibration(config_id: int, N: int, K: int, tag: int = 0, rank: int = 8) -> np.ndarray:
+    """Calibration inputs X [N][K] of one linear layer (bf16 bits): rank-`rank`
+    correlated N(0,1) factors plus N(0, 0.5^2) noise, each channel scaled by
+    exp(N(0, 0.5^2)) and 1 % of the channels by a further 8 (outliers)."""
+    g = rng(config_id, _S_CALIB + tag)
+    V = g.standard_normal((rank, K))
+    c = g.standard_normal((N, rank))
+    x = c @ V / np.sqrt(rank) + 0.5 * g.standard_normal((N, K))
+    scale = np.exp(0.5 * g.standard_normal(K))
+    scale[g.choice(K, max(1, K // 100), replace=False)] *= 8.0
+    return to_bf16_bits((x * scale).astype(np.float32))
 
 
 def important_mask(config_id: int, T: int, frac: float = 0.1) -> np.ndarray:

@@ -793,3 +793,186 @@ def test_router_logits_matches_fp64_matmul():
     assert (np.abs(got - ref) <= ulp).all()
     assert (got == ref).mean() > 0.95
     assert 0.5 < float(got.std()) < 2.0                    # unit-variance logits by construction
+
+
+# ------------------------------------------------------------------ GPTQ ---
+
+def test_codes_for_matches_quantizer():
+    """With the parameters the quantizer picked for the same values, the
+    nearest-code helper gives the quantizer's own codes (tie-heavy groups)."""
+    g = np.random.default_rng(11)
+    for bits in (1, 2, 3):
+        W = (g.standard_normal((64, 128)) * 0.02).astype(np.float32)
+        W[:8] = np.round(W[:8] * 400) / 400                    # many values on level midpoints
+        q, s, z = oracle.quantize(W, bits, 32)
+        got = oracle.codes_for(W, np.repeat(s, 32, axis=1), np.repeat(z, 32, axis=1), bits)
+        np.testing.assert_array_equal(got, q)
+
+
+def _calib_h(N, K, tag=0):
+    return oracle.gptq_hessian(synthetic.calibration(1, N, K, tag=tag))
+
+
+def test_gptq_hessian_is_gram():
+    """H = 2 X^T X: symmetric, and x^T H x = 2 ||X x||^2 for a random x."""
+    X = synthetic.calibration(1, 300, 64)
+    H = oracle.gptq_hessian(X)
+    Xf = oracle.bf16_to_float64(X)
+    v = np.random.default_rng(3).standard_normal(64)
+    np.testing.assert_array_equal(H, H.T)
+    assert np.isclose(v @ H @ v, 2 * np.sum((Xf @ v) ** 2), rtol=1e-12)
+
+
+def test_gptq_factor_properties():
+    """U is upper triangular with a positive diagonal and U^T U is the inverse
+    of the damped H; scaling H by c scales U by 1/sqrt(c) (relative damping);
+    a zero input row/column is dead and gets H_kk = 1 before damping."""
+    H = _calib_h(200, 96)
+    H[5, :] = 0.0
+    H[:, 5] = 0.0
+    U, dead = oracle.gptq_factor(H, 0.01)
+    assert dead.tolist() == [1 if k == 5 else 0 for k in range(96)]
+    np.testing.assert_array_equal(U, np.triu(U))
+    assert (np.diag(U) > 0).all()
+    Hd = H.copy()
+    Hd[5, 5] = 1.0
+    Hd[np.diag_indices(96)] += 0.01 * np.mean(np.diag(Hd))
+    np.testing.assert_allclose(U.T @ U @ Hd, np.eye(96), atol=1e-9)
+    U4, _ = oracle.gptq_factor(H * 4.0, 0.01)
+    # dead H_kk is set to 1 regardless of scale, so compare without a dead input
+    H2 = _calib_h(200, 96, tag=1)
+    Ua, _ = oracle.gptq_factor(H2, 0.01)
+    Ub, _ = oracle.gptq_factor(H2 * 4.0, 0.01)
+    np.testing.assert_allclose(Ub, Ua / 2.0, rtol=1e-9, atol=1e-12)
+    assert U4.shape == U.shape
+
+
+def test_gptq_identity_hessian_is_rtn():
+    """With H a multiple of I no error is passed on: GPTQ = the Sec. 3.1
+    round-to-nearest quantizer bit for bit, loss = (h / 2) sum (w - deq)^2."""
+    K, R = 128, 48
+    c = 2.0 ** -3
+    X = np.zeros((K, K), np.uint16)
+    X[np.arange(K), np.arange(K)] = oracle.bf16_round(c)          # X = c I
+    H = oracle.gptq_hessian(X)
+    W = (np.random.default_rng(4).standard_normal((R, K)) * 0.02).astype(np.float32)
+    for bits, G in ((1, 32), (2, 64), (3, 128)):
+        q, s, z, loss, _ = oracle.gptq_quantize(W, H, bits, G)
+        qr, sr, zr = oracle.quantize(W, bits, G)
+        np.testing.assert_array_equal(q, qr)
+        np.testing.assert_array_equal(s, sr)
+        np.testing.assert_array_equal(z, zr)
+        h = 2 * c * c * 1.01
+        d = W.astype(np.float64) - oracle.dequant_exact(qr, sr, zr, G)
+        np.testing.assert_allclose(loss, h / 2 * (d * d).sum(axis=1), rtol=1e-12)
+
+
+def _nearest_exact(w32, s16, z16, bits):
+    """Brute force over all codes with exact rationals, ties to the even code."""
+    s, z = Fraction(f16val(s16)), Fraction(f16val(z16))
+    best = None
+    for j in range(1 << bits):
+        key = (abs(Fraction(float(w32)) - s * (j - z)), j & 1)
+        if best is None or key < best[0]:
+            best = (key, j)
+    return best[1]
+
+
+def test_gptq_two_columns_closed_form():
+    """K = 2, one group, H = [[1, rho], [rho, 1]], no damping: U = [[1/c, -rho/c],
+    [0, 1]] with c = sqrt(1 - rho^2), so column 1 is quantized at
+    w1 + rho (w0 - deq0) (optimal brain surgeon compensation), and the loss is
+    ((w0 - deq0)^2 c^2 + (w1' - deq1)^2) / 2."""
+    g = np.random.default_rng(8)
+    for rho in (0.9, -0.6, 0.3):
+        H = np.array([[1.0, rho], [rho, 1.0]])
+        W = (g.standard_normal((40, 2)) * 0.05).astype(np.float32)
+        for bits in (1, 2, 3):
+            q, s, z, loss, _ = oracle.gptq_quantize(W, H, bits, 2, damp=0.0)
+            for r in range(40):
+                _, s16, z16 = oracle.quantize(W[r:r + 1], bits, 2)
+                s16, z16 = int(s16[0, 0]), int(z16[0, 0])
+                assert (s[r, 0], z[r, 0]) == (s16, z16)
+                q0 = _nearest_exact(W[r, 0], s16, z16, bits)
+                deq0 = f16val(s16) * (q0 - f16val(z16))
+                w1 = float(W[r, 1]) + rho * (float(W[r, 0]) - deq0)
+                q1 = _nearest_exact(np.float32(w1), s16, z16, bits)
+                deq1 = f16val(s16) * (q1 - f16val(z16))
+                assert (q[r, 0], q[r, 1]) == (q0, q1), (rho, bits, r)
+                want = ((float(W[r, 0]) - deq0) ** 2 * (1 - rho * rho) + (w1 - deq1) ** 2) / 2
+                assert math.isclose(loss[r], want, rel_tol=1e-12, abs_tol=1e-18)
+
+
+def test_gptq_loss_identity():
+    """Whatever codes are chosen, the error terms satisfy d H d^T = sum_k e_k^2
+    per row (d = w - dequantized w, H the damped Hessian): a wrong sign, index
+    or factor in the compensation breaks it."""
+    K, R = 192, 32
+    X = synthetic.calibration(1, 256, K, tag=2)
+    H = oracle.gptq_hessian(X)
+    W = synthetic.weight(1, 0, 1, shape=(R, K))
+    for bits, G in ((1, 32), (3, 64)):
+        q, s, z, loss, _ = oracle.gptq_quantize(W, H, bits, G)
+        Hd = H + 0.01 * np.mean(np.diag(H)) * np.eye(K)
+        d = W.astype(np.float64) - oracle.dequant_exact(q, s, z, G)
+        np.testing.assert_allclose(np.einsum("rk,kj,rj->r", d, Hd, d), 2 * loss, rtol=1e-9)
+
+
+def test_gptq_beats_rtn_on_correlated_inputs():
+    """The layer-wise error ||(W - Q) X^T||^2 that GPTQ minimises greedily is
+    well below round-to-nearest's on correlated calibration inputs."""
+    K, R = 256, 64
+    X = synthetic.calibration(1, 512, K, tag=3)
+    Xf = oracle.bf16_to_float64(X)
+    H = oracle.gptq_hessian(X)
+    W = synthetic.weight(1, 1, 0, shape=(R, K))
+    for bits, G in ((2, 32), (3, 128)):
+        q, s, z, _, _ = oracle.gptq_quantize(W, H, bits, G)
+        qr, sr, zr = oracle.quantize(W, bits, G)
+        e_g = np.sum(((W - oracle.dequant_exact(q, s, z, G)) @ Xf.T) ** 2)
+        e_r = np.sum(((W - oracle.dequant_exact(qr, sr, zr, G)) @ Xf.T) ** 2)
+        assert e_g < 0.6 * e_r, (bits, e_g, e_r)
+
+
+def test_gptq_dead_inputs():
+    """Inputs the calibration never excites are zeroed: their weights do not
+    change the result, and their codes are the nearest level to 0."""
+    K, R, G = 128, 16, 32
+    X = synthetic.calibration(1, 256, K, tag=4)
+    X[:, [3, 70]] = 0
+    H = oracle.gptq_hessian(X)
+    W = synthetic.weight(1, 2, 0, shape=(R, K))
+    W2 = W.copy()
+    W2[:, [3, 70]] = 5.0
+    a = oracle.gptq_quantize(W, H, 2, G)
+    b = oracle.gptq_quantize(W2, H, 2, G)
+    for u, v in zip(a[:4], b[:4]):
+        np.testing.assert_array_equal(u, v)
+    q, s, z = a[:3]
+    for k in (3, 70):
+        want = oracle.codes_for(np.zeros(R, np.float32), s[:, k // G], z[:, k // G], 2)
+        np.testing.assert_array_equal(q[:, k], want)
+
+
+def test_gptq_group_params_follow_compensation():
+    """A factor whose only off-diagonal entry couples column 0 to column 2
+    (U = I + a e_0 e_2^T): column 2 is quantized at w2 - a (w0 - deq0), and the
+    second group's scale/zero come from that compensated value, not from w2."""
+    g = np.random.default_rng(12)
+    a = 0.75
+    U = np.eye(4)
+    U[0, 2] = a
+    W = (g.standard_normal((30, 4)) * 0.05).astype(np.float32)
+    q, s, z, loss, _ = oracle.gptq_quantize_u(W, U, np.zeros(4, np.uint8), 2, 2)
+    differs = 0
+    for r in range(30):
+        _, s0, z0 = oracle.quantize(W[r:r + 1, :2], 2, 2)
+        s0, z0 = int(s0[0, 0]), int(z0[0, 0])
+        q0 = _nearest_exact(W[r, 0], s0, z0, 2)
+        w2 = np.float32(float(W[r, 2]) - a * (float(W[r, 0]) - f16val(s0) * (q0 - f16val(z0))))
+        _, s1, z1 = oracle.quantize(np.array([[w2, W[r, 3]]], np.float32), 2, 2)
+        assert (s[r, 1], z[r, 1]) == (int(s1[0, 0]), int(z1[0, 0])), r
+        assert q[r, 2] == _nearest_exact(w2, int(s1[0, 0]), int(z1[0, 0]), 2)
+        _, s1o, _ = oracle.quantize(W[r:r + 1, 2:], 2, 2)
+        differs += int(s1o[0, 0]) != s[r, 1]
+    assert differs > 10          # the compensation does move the second group's range
