@@ -12,7 +12,8 @@ algorithmic 6*d*ffn FLOPs per kept pair), and the OLMoE-shaped layer (d=2048,
 ffn=1024, 64 experts, top-8, G=64, Zipf-skewed logits, threshold 0.05) in
 decode (16 tokens) and prefill (2048 tokens), the token importance that
 marks the protected tokens (32 heads, 4096 tokens, rho = 0.02), the router
-logits ahead of routing, and the 32-layer residual stack.
+logits ahead of routing, GPTQ of one expert's gate and down matrices, and
+the 32-layer residual stack.
 
 One step = route_and_prune + moe_forward over the batch for one layer.  The
 step rotates over packed copies of the layer (4 x 484 MB Mixtral, 3 x 131 MB
@@ -53,6 +54,7 @@ def parse():
     p.add_argument("--no-importance", action="store_true", help="skip the token-importance measurement")
     p.add_argument("--no-stack", action="store_true", help="skip the 32-layer stack")
     p.add_argument("--no-router", action="store_true", help="skip the router-logits measurement")
+    p.add_argument("--no-gptq", action="store_true", help="skip the GPTQ measurement")
     p.add_argument("--stack-steps", type=int, default=10)
     p.add_argument("--graph", action="store_true",
                    help="also time HIP-graph replays of the step (reported as ms_per_step_graph)")
@@ -368,6 +370,51 @@ def router_entry(mc, torch, synthetic, steps, warmup):
     return dict(kernel="router", runs=runs)
 
 
+def gptq_entry(mc, torch, synthetic):
+    """GPTQ (fp64) of one Mixtral expert's gate matrix (14336 x 4096, 3 bits)
+    and down matrix (4096 x 14336, 2 bits), G = 128, from 8192 calibration
+    rows each, timed per stage with the library's HIP events (one run after
+    a warm-up run).  Work per stage: Hessian 2*N*K^2 flops; factor (Cholesky
+    and triangular inverse) 4/3*K^3; quantize R*K^2 (one multiply and one
+    subtract per compensation term).  Peak: 78.6 fp64 TFLOP/s."""
+    FP64_PEAK_TFLOPS = 78.6
+    runs = []
+    for name, (R, K, bits, tag) in (("gate", (14336, 4096, 3, 1)), ("down", (4096, 14336, 2, 2))):
+        N = 8192
+        X = torch.from_numpy(synthetic.calibration(2, N, K, tag=tag).view("int16")).cuda()
+        W = torch.from_numpy(synthetic.weight(2, 0, 0 if name == "gate" else 2, shape=(R, K))).cuda()
+        d, ffn = (K, R) if name == "gate" else (R, K)
+        L = mc.PackedLayer(1, d, ffn, [bits], 128)
+        H = torch.empty((K, K), dtype=torch.float64, device="cuda")
+        U = torch.empty_like(H)
+        dead = torch.empty(K, dtype=torch.uint8, device="cuda")
+        ws = torch.empty(mc.gptq_workspace(R, K), dtype=torch.uint8, device="cuda")
+        mat = 0 if name == "gate" else 2
+        def run():
+            mc.gptq_hessian(X, H)
+            mc.gptq_factor(H, U, dead, ws)
+            mc.gptq_quantize(L, 0, mat, W, U, dead, ws)
+        run()
+        torch.cuda.synchronize()
+        mc.timing_enable(True)
+        run()
+        torch.cuda.synchronize()
+        ms = {}
+        for st in ("gptq_hessian", "gptq_factor", "gptq_quantize"):
+            t, _ = mc.timing_read(st)
+            ms[st] = t
+        mc.timing_enable(False)
+        flops = {"gptq_hessian": 2.0 * N * K * K, "gptq_factor": 4.0 / 3.0 * K ** 3, "gptq_quantize": 1.0 * R * K * K}
+        runs.append(dict(matrix=name, rows=R, inputs=K, bits=bits, calib_rows=N,
+                         ms={k: round(v, 2) for k, v in ms.items()},
+                         fp64_tflops={k: round(flops[k] / (ms[k] * 1e-3) / 1e12, 2) for k in ms},
+                         fp64_frac={k: round(flops[k] / (ms[k] * 1e-3) / 1e12 / FP64_PEAK_TFLOPS, 4) for k in ms},
+                         total_ms=round(sum(ms.values()), 1)))
+        del X, W, L, H, U, dead, ws
+        torch.cuda.empty_cache()
+    return dict(workload="mixtral_8x7b_expert_gptq", group=128, runs=runs)
+
+
 def stack_entry(mc, torch, synthetic, steps, warmup):
     """The 32-layer Mixtral-shaped expert stack resident in HBM: 32 packed
     layers (widths [3,3,3,2,2,2,2,3] in a seeded order per layer, weights
@@ -551,6 +598,8 @@ def main():
                         "decode": dec, "prefill": prefill_entry(wo, ms_p, kus)}
     if not args.no_importance:
         out["importance"] = importance_entry(mc, torch, 20, 3)
+    if not args.no_gptq:
+        out["gptq"] = gptq_entry(mc, torch, synthetic)
     if not args.no_router:
         out["router"] = router_entry(mc, torch, synthetic, 50, 5)
     if not args.no_stack:

@@ -9,6 +9,7 @@
  * inference path:
  *
  *   mc_pack            fp32 expert weights -> packed codes + fp16 scale/zero
+ *   mc_gptq_*          GPTQ quantization of one matrix into the packed layer
  *   mc_router_logits   the router's linear layer: x -> router logits
  *   mc_route_and_prune router logits -> top-k, Eq. 5 pruning, protection,
  *                      per-expert token lists (CSR)
@@ -151,6 +152,48 @@ typedef struct mc_routing {
   int32_t *n_pruned;     /* [1] number of pruned pairs */
 } mc_routing;
 
+/* GPTQ, the quantizer the paper applies to the experts (Sec. 3.1: Hessian
+ * H = 2 X^T X of the layer-wise squared error ||W X^T - Q X^T||^2, columns
+ * quantized in order, each column's error compensated on the columns after
+ * it), producing the same packed format as mc_pack.  Offline; all arithmetic
+ * fp64; deterministic.  For a matrix W [R][K] (R outputs, K inputs) with
+ * calibration inputs X [N][K]:
+ *
+ *   mc_gptq_hessian   H = 2 X^T X (accumulate = 0) or H += 2 X^T X
+ *                     (accumulate != 0, for calibration sets in pieces).
+ *                     x_bf16: [N][K] bf16; H: [K][K] fp64 (8-byte aligned).
+ *   mc_gptq_factor    inputs with H_kk = 0 are dead (dead[k] = 1; H_kk taken
+ *                     as 1), H += damp * mean(diag H) * I (GPTQ uses damp =
+ *                     0.01), and U [K][K] fp64 = the upper-triangular
+ *                     Cholesky factor of H^-1 (H^-1 = U^T U; zeros below the
+ *                     diagonal).  H is read only.  H must be symmetric
+ *                     positive semi-definite with damp > 0, or positive
+ *                     definite; otherwise U holds NaNs.
+ *   mc_gptq_quantize  quantizes matrix `mat` (0 gate [ffn][d], 1 up [ffn][d],
+ *                     2 down [d][ffn]) of expert e of L at the expert's width
+ *                     and L's group size, writing its codes and scale/zero
+ *                     words into L (the other matrices are untouched):
+ *                     dead inputs get weight 0; for k = 0 .. K-1, at a group
+ *                     start s and z are the Sec. 3.1 parameters (as mc_pack)
+ *                     of the fp32 rounding of the group's current values;
+ *                     q_k = nearest level of fp32(w_k); e_k = (w_k - s(q_k -
+ *                     z)) / U_kk; w_j -= e_k U_kj for j > k, applied one
+ *                     column after the other.  W: [R][K] fp32; loss (may be
+ *                     NULL): [R] fp64, sum_k e_k^2 / 2 per row.
+ *
+ * K (the input width) must be a multiple of 128, at most MC_GPTQ_MAX_K.
+ * Workspace: mc_gptq_workspace(R, K) bytes (2 K^2 + 64 K doubles for the
+ * factor, R K (8 + 1) + 1024 R bytes for the quantizer), 8-byte aligned.
+ * Errors: MC_EINVAL (shape, NULL or misaligned pointer, damp < 0 or not
+ * finite), MC_ENOSPACE (workspace or layer buffers), MC_EHIP. */
+#define MC_GPTQ_MAX_K 32768
+mc_status mc_gptq_workspace(int R, int K, size_t *bytes);
+mc_status mc_gptq_hessian(const uint16_t *x_bf16, int N, int K, double *H, int accumulate, void *stream);
+mc_status mc_gptq_factor(const double *H, int K, double damp, double *U, uint8_t *dead, void *workspace,
+                         size_t ws_bytes, void *stream);
+mc_status mc_gptq_quantize(const mc_layer *L, int e, int mat, const float *W, const double *U,
+                           const uint8_t *dead, double *loss, void *workspace, size_t ws_bytes, void *stream);
+
 /* Router logits, the scores whose top-k Eq. 1 takes:
  *   logits[t][e] = sum_k x[t][k] * w_router[e][k]
  * x: [T][d] bf16 (the MoE layer input), w_router: [E][d] bf16, both 16-byte
@@ -282,7 +325,8 @@ mc_status mc_pmq_allocate(const double *phi, const double *w, const double *eps,
  * events of one kernel and returns the summed duration in ms and the number
  * of launches.  Kernel names: pack_scale_zero, pack_codes, export,
  * route_fused, route_select, route_lists, prefill_prep, gateup, down, combine,
- * importance_colsum, importance_finish, importance_select, rmsnorm, router.
+ * importance_colsum, importance_finish, importance_select, rmsnorm, router,
+ * gptq_hessian, gptq_factor, gptq_quantize (each a whole call).
  * Errors: MC_EINVAL (unknown name, NULL pointer), MC_EHIP. */
 mc_status mc_timing_enable(int on);
 mc_status mc_timing_read(const char *kernel, double *total_ms, int *launches);

@@ -14,6 +14,10 @@ from ._binding import (  # noqa: F401
     codes_export,
     dequant_export,
     forward_workspace,
+    gptq_factor,
+    gptq_hessian,
+    gptq_quantize,
+    gptq_workspace,
     importance_workspace,
     lib_path,
     load,

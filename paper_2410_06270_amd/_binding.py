@@ -68,6 +68,14 @@ def load():
         lib.mc_dequant_export.argtypes = [ctypes.POINTER(_Layer), I, I, P, P]
         lib.mc_codes_export.restype = st
         lib.mc_codes_export.argtypes = [ctypes.POINTER(_Layer), I, I, P, P]
+        lib.mc_gptq_workspace.restype = st
+        lib.mc_gptq_workspace.argtypes = [I, I, ctypes.POINTER(S)]
+        lib.mc_gptq_hessian.restype = st
+        lib.mc_gptq_hessian.argtypes = [P, I, I, P, I, P]
+        lib.mc_gptq_factor.restype = st
+        lib.mc_gptq_factor.argtypes = [P, I, ctypes.c_double, P, P, P, S, P]
+        lib.mc_gptq_quantize.restype = st
+        lib.mc_gptq_quantize.argtypes = [ctypes.POINTER(_Layer), I, I, P, P, P, P, P, S, P]
         lib.mc_router_logits.restype = st
         lib.mc_router_logits.argtypes = [P, P, I, I, I, P, P]
         lib.mc_route_and_prune.restype = st
@@ -191,6 +199,37 @@ def dequant_export(layer: PackedLayer, e: int, mat: int, out, stream=None):
 def codes_export(layer: PackedLayer, e: int, mat: int, out, stream=None):
     assert out.dtype == torch.uint8 and out.is_contiguous()
     _check(load().mc_codes_export(ctypes.byref(layer.desc), e, mat, _ptr(out), _stream(stream)))
+
+
+def gptq_workspace(R: int, K: int) -> int:
+    b = ctypes.c_size_t()
+    _check(load().mc_gptq_workspace(R, K, ctypes.byref(b)))
+    return b.value
+
+
+def gptq_hessian(x, H, accumulate: bool = False, stream=None):
+    """x: [N][K] bf16 (or int16 bits); H: [K][K] float64."""
+    assert x.is_contiguous() and x.element_size() == 2 and H.is_contiguous() and H.dtype == torch.float64
+    N, K = x.shape
+    assert tuple(H.shape) == (K, K)
+    _check(load().mc_gptq_hessian(_ptr(x), N, K, _ptr(H), int(bool(accumulate)), _stream(stream)))
+
+
+def gptq_factor(H, U, dead, workspace, damp: float = 0.01, stream=None):
+    """H, U: [K][K] float64; dead: [K] uint8."""
+    K = H.shape[0]
+    assert H.is_contiguous() and U.is_contiguous() and H.dtype == torch.float64 and U.dtype == torch.float64
+    assert dead.dtype == torch.uint8 and dead.numel() == K
+    _check(load().mc_gptq_factor(_ptr(H), K, float(damp), _ptr(U), _ptr(dead), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def gptq_quantize(layer: PackedLayer, e: int, mat: int, W, U, dead, workspace, loss=None, stream=None):
+    """W: [R][K] float32 (the fp32 weights of matrix `mat` of expert e)."""
+    assert W.is_contiguous() and W.dtype == torch.float32 and U.dtype == torch.float64
+    _check(load().mc_gptq_quantize(ctypes.byref(layer.desc), e, mat, _ptr(W), _ptr(U), _ptr(dead), _ptr(loss),
+                                   _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                   _stream(stream)))
 
 
 def router_logits(x, w_router, logits, stream=None):

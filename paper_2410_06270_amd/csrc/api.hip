@@ -163,6 +163,76 @@ mc_status mc_codes_export(const mc_layer* L, int e, int mat, uint8_t* out, void*
   return export_common(L, e, mat, out, false, stream);
 }
 
+// ----------------------------------------------------------------- GPTQ --
+static mc_status check_gptq_k(int K) {
+  if (K < 128 || K % 128 != 0 || K > MC_GPTQ_MAX_K)
+    return fail(MC_EINVAL, "K=%d: need a multiple of 128 in [128, %d]", K, MC_GPTQ_MAX_K);
+  return MC_OK;
+}
+
+mc_status mc_gptq_workspace(int R, int K, size_t* bytes) {
+  mc_status s = check_gptq_k(K);
+  if (s != MC_OK) return s;
+  if (R < 16 || R % 16 != 0) return fail(MC_EINVAL, "R=%d: need a positive multiple of 16", R);
+  if (!bytes) return fail(MC_EINVAL, "bytes is NULL");
+  const size_t f = mc::gptq_factor_bytes(K), q = mc::gptq_quantize_bytes(R, K);
+  *bytes = f > q ? f : q;
+  return MC_OK;
+}
+
+mc_status mc_gptq_hessian(const uint16_t* x_bf16, int N, int K, double* H, int accumulate, void* stream) {
+  mc_status s = check_gptq_k(K);
+  if (s != MC_OK) return s;
+  if (N < 1) return fail(MC_EINVAL, "N=%d calibration rows", N);
+  if (!x_bf16 || !H) return fail(MC_EINVAL, "x or H is NULL");
+  if (reinterpret_cast<uintptr_t>(H) & 7u) return fail(MC_EINVAL, "H must be 8-byte aligned");
+  (void)hipGetLastError();
+  return hip_status(mc::launch_gptq_hessian(x_bf16, N, K, H, accumulate != 0, static_cast<hipStream_t>(stream)),
+                    "mc_gptq_hessian launch");
+}
+
+mc_status mc_gptq_factor(const double* H, int K, double damp, double* U, uint8_t* dead, void* workspace,
+                         size_t ws_bytes, void* stream) {
+  mc_status s = check_gptq_k(K);
+  if (s != MC_OK) return s;
+  if (!(damp >= 0.0) || !std::isfinite(damp)) return fail(MC_EINVAL, "damp %g: need a finite value >= 0", damp);
+  if (!H || !U || !dead || !workspace) return fail(MC_EINVAL, "H, U, dead or workspace is NULL");
+  if ((reinterpret_cast<uintptr_t>(H) | reinterpret_cast<uintptr_t>(U) | reinterpret_cast<uintptr_t>(workspace)) &
+      7u)
+    return fail(MC_EINVAL, "H, U and workspace must be 8-byte aligned");
+  const size_t need = mc::gptq_factor_bytes(K);
+  if (ws_bytes < need) return fail(MC_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+  (void)hipGetLastError();
+  return hip_status(mc::launch_gptq_factor(H, K, damp, U, dead, workspace, static_cast<hipStream_t>(stream)),
+                    "mc_gptq_factor launch");
+}
+
+mc_status mc_gptq_quantize(const mc_layer* L, int e, int mat, const float* W, const double* U, const uint8_t* dead,
+                           double* loss, void* workspace, size_t ws_bytes, void* stream) {
+  mc_status s = check_layer(L, true);
+  if (s != MC_OK) return s;
+  if (e < 0 || e >= L->E) return fail(MC_EINVAL, "expert %d outside [0, %d)", e, L->E);
+  if (mat < 0 || mat > 2) return fail(MC_EINVAL, "matrix %d not in {0,1,2}", mat);
+  const int R = mat < 2 ? L->ffn : L->d, K = mat < 2 ? L->d : L->ffn;
+  s = check_gptq_k(K);
+  if (s != MC_OK) return s;
+  if (!W || !U || !dead || !workspace) return fail(MC_EINVAL, "W, U, dead or workspace is NULL");
+  if ((reinterpret_cast<uintptr_t>(U) | reinterpret_cast<uintptr_t>(workspace) |
+       reinterpret_cast<uintptr_t>(loss)) & 7u)
+    return fail(MC_EINVAL, "U, loss and workspace must be 8-byte aligned");
+  const size_t need = mc::gptq_quantize_bytes(R, K);
+  if (ws_bytes < need) return fail(MC_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+  const mc::LayerArgs a = layer_args(L);
+  const int b = L->bits_host[e];
+  const size_t per_bit = (size_t)L->d * L->ffn / 32;
+  const size_t wofs = (3 * (size_t)a.cum_bits[e] + (size_t)mat * b) * per_bit;
+  const size_t sofs = (3 * (size_t)e + mat) * ((size_t)L->d * L->ffn / L->group);
+  (void)hipGetLastError();
+  return hip_status(mc::launch_gptq_quantize(W, U, dead, R, K, b, L->group, static_cast<uint32_t*>(L->words) + wofs,
+                                             L->sz + sofs, loss, workspace, static_cast<hipStream_t>(stream)),
+                    "mc_gptq_quantize launch");
+}
+
 static float prune_delta32(double tau) {
   if (tau == 0.0) return INFINITY;
   if (tau == 1.0) return -INFINITY;

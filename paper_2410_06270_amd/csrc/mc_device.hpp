@@ -156,6 +156,55 @@ __device__ __forceinline__ int extract_code(const uint32_t* w, int i, int h) {
 
 // --------------------------------------------------------------- arguments --
 
+// Lane `src`'s value of v, as a wave-uniform value (src must be uniform).
+__device__ __forceinline__ double readlane_f64(double v, int src) {
+  const unsigned long long b = __double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, src);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(b >> 32), src);
+  return __longlong_as_double(((long long)hi << 32) | lo);
+}
+
+// ------------------------------------------------------------- quantizer --
+// Sec. 3.1 group parameters from the group's fp32 min and max, as one
+// scale/zero word (s16 low, z16 high), L = 2^b - 1:
+//   s = fp16(fp32(max - min) / L) (1.0 if it rounds to zero), z = fp16(-min / s).
+__device__ __forceinline__ uint32_t group_sz_word(float mn, float mx, int b) {
+  const float Lf = (float)((1 << b) - 1);
+  const float s32 = (mx - mn) / Lf;                 // IEEE fp32 division
+  uint16_t s16 = float_to_half_sat(s32);
+  if ((s16 & 0x7fffu) == 0) s16 = 0x3c00;           // scale 0 -> 1.0
+  const float z32 = -mn / half_bits_to_float(s16);
+  uint16_t z16 = float_to_half_sat(z32);
+  if (z16 == 0x8000u) z16 = 0;                      // -0 -> +0
+  return (uint32_t)s16 | ((uint32_t)z16 << 16);
+}
+
+// Code of w under scale s and zero z (fp16 values widened): the number of
+// level midpoints s*(j + 1/2 - z) below w, moved to the even neighbour when w
+// sits exactly on a midpoint.  Each midpoint is exact in fp64 (j + 1/2 - z
+// needs <= 41 bits, times the 11-bit s <= 52).
+__device__ __forceinline__ int nearest_code(float w, double s, double z, int L) {
+  const double wd = (double)w;
+  int below = 0;
+  for (int j = 0; j < L; ++j) below += (s * (((double)j + 0.5) - z) < wd) ? 1 : 0;
+  if (below < L && (below & 1) && s * (((double)below + 0.5) - z) == wd) ++below;
+  return below;
+}
+
+// Places one code into a lane's b packed words: code pair i (0..15) of the
+// lane's 32 codes, half h (0: first, 1: second of the pair).
+__device__ __forceinline__ void place_code(uint32_t (&w)[3], uint32_t code, int i, int h, int b) {
+  if (b == 1) {
+    w[0] |= code << (16 * h + i);
+  } else if (b == 2) {
+    w[i >> 3] |= code << (16 * h + 2 * (i & 7));
+  } else if (i < 15) {
+    w[i / 5] |= code << (16 * h + 3 * (i % 5));
+  } else {
+    for (int p = 0; p < 3; ++p) w[p] |= ((code >> p) & 1u) << (16 * h + 15);
+  }
+}
+
 struct LayerArgs {
   const uint32_t* words;
   const uint32_t* sz;

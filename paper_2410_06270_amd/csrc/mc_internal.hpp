@@ -11,7 +11,7 @@ constexpr int kDecodeMaxT = 64;        // up to this many tokens one workgroup h
 enum TimingSite {
   kSitePackSz, kSitePackCodes, kSiteExport, kSiteRouteFused, kSiteRouteSelect, kSiteRouteLists,
   kSiteGateUp, kSiteDown, kSiteCombine, kSitePrefillPrep, kSiteImpColsum, kSiteImpFinish, kSiteImpSelect,
-  kSiteRmsNorm, kSiteRouter,
+  kSiteRmsNorm, kSiteRouter, kSiteGptqHessian, kSiteGptqFactor, kSiteGptqQuantize,
   kNumSites
 };
 void timing_begin(hipStream_t stream, int site);
@@ -50,6 +50,16 @@ size_t stack_workspace_bytes(int T, int E, int k, int d, int ffn);   // xn [T][d
 // logits [T][E] fp32 = x [T][d] . w [E][d]^T (bf16), fp64 sums rounded once.
 hipError_t launch_router(const uint16_t* x, const uint16_t* w, int T, int d, int E, float* logits,
                          hipStream_t stream);
+// GPTQ (fp64): H (+)= 2 X^T X; the factor U (upper Cholesky of the damped
+// H^-1) with the dead-input mask; in-order quantization into one matrix's
+// packed words and scale/zero words.
+size_t gptq_factor_bytes(int K);
+size_t gptq_quantize_bytes(int R, int K);
+hipError_t launch_gptq_hessian(const uint16_t* x, int N, int K, double* H, bool accumulate, hipStream_t st);
+hipError_t launch_gptq_factor(const double* H, int K, double damp, double* U, uint8_t* dead, void* ws,
+                              hipStream_t st);
+hipError_t launch_gptq_quantize(const float* W, const double* U, const uint8_t* dead, int R, int K, int bits, int G,
+                                uint32_t* words, uint32_t* sz, double* loss, void* ws, hipStream_t st);
 size_t importance_workspace_bytes(int H, int L);
 hipError_t launch_importance(const uint16_t* attn, int H, int L, const uint16_t* x, int d, float rho,
                              float* importance, uint8_t* mask, void* ws, hipStream_t stream);

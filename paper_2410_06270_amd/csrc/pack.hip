@@ -55,29 +55,12 @@ __global__ void __launch_bounds__(256) pack_sz_kernel(const float* __restrict__ 
   }
   if (!valid || sub != 0) return;
   const int b = L.cum_bits[e + 1] - L.cum_bits[e];
-  const float Lf = (float)((1 << b) - 1);
-  const float s32 = (mx - mn) / Lf;                 // IEEE fp32 division
-  uint16_t s16 = float_to_half_sat(s32);
-  if ((s16 & 0x7fffu) == 0) s16 = 0x3c00;           // scale 0 -> 1.0
-  const float z32 = -mn / half_bits_to_float(s16);
-  uint16_t z16 = float_to_half_sat(z32);
-  if (z16 == 0x8000u) z16 = 0;                      // -0 -> +0
   const size_t idx = layer_sz_offset(L, e, m) + ((size_t)(row / 16) * ng + g) * 16 + (row % 16);
-  sz_out[idx] = (uint32_t)s16 | ((uint32_t)z16 << 16);
+  sz_out[idx] = group_sz_word(mn, mx, b);
 }
 
 // ------------------------------------------------------------------- codes --
 // One thread per (matrix, tile, lane): 32 codes -> b words.
-// Code of w: the number of level midpoints s*(j + 1/2 - z) below w, moved to
-// the even neighbour when w sits exactly on a midpoint.  Each midpoint is
-// exact in fp64 (j + 1/2 - z needs <= 41 bits, times the 11-bit s <= 52).
-__device__ __forceinline__ int nearest_code(float w, double s, double z, int L) {
-  const double wd = (double)w;
-  int below = 0;
-  for (int j = 0; j < L; ++j) below += (s * (((double)j + 0.5) - z) < wd) ? 1 : 0;
-  if (below < L && (below & 1) && s * (((double)below + 0.5) - z) == wd) ++below;
-  return below;
-}
 
 __global__ void __launch_bounds__(256) pack_codes_kernel(const float* __restrict__ wg,
                                                          const float* __restrict__ wu,
@@ -119,16 +102,7 @@ __global__ void __launch_bounds__(256) pack_codes_kernel(const float* __restrict
     const float v[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
     for (int j = 0; j < 8; ++j) {
       const uint32_t code = sign ? (v[j] >= 0.0f ? 1u : 0u) : (uint32_t)nearest_code(v[j], s, z, Lc);
-      const int i = 4 * u + (j >> 1), h = j & 1;
-      if (b == 1) {
-        w[0] |= code << (16 * h + i);
-      } else if (b == 2) {
-        w[i >> 3] |= code << (16 * h + 2 * (i & 7));
-      } else if (i < 15) {
-        w[i / 5] |= code << (16 * h + 3 * (i % 5));
-      } else {
-        for (int p = 0; p < 3; ++p) w[p] |= ((code >> p) & 1u) << (16 * h + 15);
-      }
+      place_code(w, code, 4 * u + (j >> 1), j & 1, b);
     }
   }
   uint32_t* dst = words_out + layer_word_offset(L, e, m) + ((size_t)tile * 64 + lane) * b;

@@ -33,13 +33,6 @@ __device__ __forceinline__ uint32_t ordered_bits(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-__device__ __forceinline__ double readlane_f64(double v, int src) {
-  const unsigned long long b = __double_as_longlong(v);
-  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, src);
-  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(b >> 32), src);
-  return __longlong_as_double(((long long)hi << 32) | lo);
-}
-
 // Selects and prunes token t (one wavefront).  Lanes hold the logits (lane l
 // has experts l, l+64, ...) as distinct 64-bit keys (ordered logit bits, then
 // the complement of the expert index, so larger key = earlier rank); each

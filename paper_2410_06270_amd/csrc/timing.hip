@@ -14,7 +14,7 @@ namespace {
 const char* const kSiteNames[kNumSites] = {
     "pack_scale_zero", "pack_codes", "export", "route_fused", "route_select",
     "route_lists",     "gateup",     "down",   "combine", "prefill_prep",
-    "importance_colsum", "importance_finish", "importance_select", "rmsnorm", "router"};
+    "importance_colsum", "importance_finish", "importance_select", "rmsnorm", "router", "gptq_hessian", "gptq_factor", "gptq_quantize"};
 
 struct Pair {
   hipEvent_t start, stop;

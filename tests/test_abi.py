@@ -266,3 +266,29 @@ def test_router_rejects(lib):
     assert f(P(0x100), P(0x200), 4, 4096, 8, None, None) == 1
     assert f(P(0x108), P(0x200), 4, 4096, 8, P(0x300), None) == 1          # x not 16-byte aligned
     assert f(P(0x100), P(0x200), 65537, 4096, 8, P(0x300), None) == 4      # above MC_MAX_TOKENS
+
+
+def test_gptq_rejects(lib):
+    """Shape, damping, NULL, alignment and workspace checks of the GPTQ calls
+    (no launch)."""
+    P = ctypes.c_void_p
+    b = ctypes.c_size_t()
+    assert lib.mc_gptq_workspace(4096, 4096, ctypes.byref(b)) == 0
+    assert b.value >= 2 * 4096 * 4096 * 8
+    assert lib.mc_gptq_workspace(4096, 4100, ctypes.byref(b)) == 1         # K % 128
+    assert lib.mc_gptq_workspace(4096, 65536, ctypes.byref(b)) == 1        # K above the limit
+    assert lib.mc_gptq_workspace(10, 4096, ctypes.byref(b)) == 1           # R % 16
+    assert lib.mc_gptq_hessian(P(0x100), 0, 256, P(0x1000), 0, None) == 1  # N < 1
+    assert lib.mc_gptq_hessian(P(0x100), 8, 256, P(0x1004), 0, None) == 1  # H misaligned
+    D = ctypes.c_double
+    f = lib.mc_gptq_factor
+    assert f(P(0x1000), 256, D(-0.1), P(0x2000), P(0x3000), P(0x4000), 1 << 30, None) == 1
+    assert f(P(0x1000), 256, D(float("nan")), P(0x2000), P(0x3000), P(0x4000), 1 << 30, None) == 1
+    assert f(None, 256, D(0.01), P(0x2000), P(0x3000), P(0x4000), 1 << 30, None) == 1
+    assert f(P(0x1000), 256, D(0.01), P(0x2000), P(0x3000), P(0x4000), 1000, None) == 2
+    L, _keep = _fake_layer()
+    q = lib.mc_gptq_quantize
+    assert q(ctypes.byref(L), 8, 0, P(0x100), P(0x200), P(0x300), None, P(0x400), 1 << 40, None) == 1
+    assert q(ctypes.byref(L), 0, 3, P(0x100), P(0x200), P(0x300), None, P(0x400), 1 << 40, None) == 1
+    assert q(ctypes.byref(L), 0, 0, None, P(0x200), P(0x300), None, P(0x400), 1 << 40, None) == 1
+    assert q(ctypes.byref(L), 0, 0, P(0x100), P(0x200), P(0x300), None, P(0x400), 1000, None) == 2
