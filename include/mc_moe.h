@@ -14,6 +14,7 @@
  *   mc_route_and_prune router logits -> top-k, Eq. 5 pruning, protection,
  *                      per-expert token lists (CSR)
  *   mc_moe_forward     Eq. 1 over the packed SwiGLU experts
+ *   mc_moe_route_forward  routing and Eq. 1 in one call
  *   mc_moe_stack_forward  a stack of MoE layers with residual connections
  *
  * Conventions for every call
@@ -232,6 +233,15 @@ mc_status mc_forward_workspace(int T, int E, int k, int d, int ffn, size_t *byte
 mc_status mc_moe_forward(const uint16_t *x_bf16, const mc_routing *r,
                          const mc_layer *L, uint16_t *y_bf16, void *workspace,
                          size_t ws_bytes, void *stream);
+
+/* mc_route_and_prune followed by mc_moe_forward in one call (the routing
+ * kernels, then the expert kernels, on `stream`), with the same results:
+ * the routing buffers of r as mc_route_and_prune writes them, y as
+ * mc_moe_forward writes it.  Arguments and errors: those of the two calls
+ * (workspace: mc_forward_workspace). */
+mc_status mc_moe_route_forward(const uint16_t *x_bf16, const float *logits, const uint8_t *important,
+                               float threshold, const mc_routing *r, const mc_layer *L, uint16_t *y_bf16,
+                               void *workspace, size_t ws_bytes, void *stream);
 
 /* Workspace bytes mc_moe_stack_forward needs: the normalised layer input
  * (T*d bf16, rounded up to 256 bytes) + mc_forward_workspace.

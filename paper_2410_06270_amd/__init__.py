@@ -28,6 +28,7 @@ from ._binding import (  # noqa: F401
     pmq_allocate,
     pmq_significance,
     route_and_prune,
+    route_forward,
     router_logits,
     stack_forward,
     stack_workspace,

@@ -85,6 +85,9 @@ def load():
         lib.mc_moe_forward.restype = st
         lib.mc_moe_forward.argtypes = [P, ctypes.POINTER(_Routing), ctypes.POINTER(_Layer), P, P,
                                        S, P]
+        lib.mc_moe_route_forward.restype = st
+        lib.mc_moe_route_forward.argtypes = [P, P, P, ctypes.c_float, ctypes.POINTER(_Routing),
+                                             ctypes.POINTER(_Layer), P, P, S, P]
         lib.mc_stack_workspace.restype = st
         lib.mc_stack_workspace.argtypes = [I, I, I, I, I, ctypes.POINTER(S)]
         lib.mc_moe_stack_forward.restype = st
@@ -262,6 +265,19 @@ def moe_forward(x, routing: Routing, layer: PackedLayer, y, workspace, stream=No
     _check(load().mc_moe_forward(_ptr(x), ctypes.byref(routing.desc), ctypes.byref(layer.desc),
                                  _ptr(y), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                  _stream(stream)))
+
+
+def route_forward(x, logits, important, threshold: float, routing: Routing, layer: PackedLayer, y, workspace,
+                  stream=None):
+    """route_and_prune + moe_forward in one call (same results)."""
+    assert x.is_contiguous() and y.is_contiguous() and x.element_size() == 2
+    assert logits.dtype == torch.float32 and logits.is_contiguous()
+    if important is not None:
+        assert important.dtype == torch.uint8 and important.is_contiguous()
+    _check(load().mc_moe_route_forward(_ptr(x), _ptr(logits), _ptr(important), float(threshold),
+                                       ctypes.byref(routing.desc), ctypes.byref(layer.desc), _ptr(y),
+                                       _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                       _stream(stream)))
 
 
 def stack_workspace(T: int, E: int, k: int, d: int, ffn: int) -> int:

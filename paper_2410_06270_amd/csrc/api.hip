@@ -294,6 +294,28 @@ mc_status mc_moe_forward(const uint16_t* x_bf16, const mc_routing* r, const mc_l
                     "mc_moe_forward launch");
 }
 
+mc_status mc_moe_route_forward(const uint16_t* x_bf16, const float* logits, const uint8_t* important,
+                               float threshold, const mc_routing* r, const mc_layer* L, uint16_t* y_bf16,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  mc_status s = check_routing(r);
+  if (s != MC_OK) return s;
+  s = check_layer(L, true);
+  if (s != MC_OK) return s;
+  if (r->E != L->E) return fail(MC_EINVAL, "routing has E=%d, layer has E=%d", r->E, L->E);
+  if (!logits) return fail(MC_EINVAL, "logits pointer is NULL");
+  if (!(threshold >= 0.0f && threshold <= 1.0f))
+    return fail(MC_EINVAL, "threshold %g outside [0, 1]", (double)threshold);
+  if (!x_bf16 || !y_bf16 || !workspace) return fail(MC_EINVAL, "x, y or workspace is NULL");
+  const size_t need = mc::forward_workspace_bytes(r->T, r->E, r->k, L->d, L->ffn);
+  if (ws_bytes < need) return fail(MC_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+  const double tau = (double)threshold;
+  const mc::RouteArgs ra{logits, important, prune_delta32(tau), tau};
+  (void)hipGetLastError();
+  return hip_status(mc::launch_forward(x_bf16, layer_args(L), *r, y_bf16, workspace, nullptr,
+                                       static_cast<hipStream_t>(stream), &ra),
+                    "mc_moe_route_forward launch");
+}
+
 mc_status mc_stack_workspace(int T, int E, int k, int d, int ffn, size_t* bytes) {
   mc_status s = mc_forward_workspace(T, E, k, d, ffn, bytes);
   if (s != MC_OK) return s;
@@ -349,11 +371,8 @@ mc_status mc_moe_stack_forward(const uint16_t* x_bf16, int n_layers, const mc_la
     s = hip_status(mc::launch_rmsnorm(in, r->T, layers[0].d, mc::kRmsNormEps, xn, st),
                    "mc_moe_stack_forward rmsnorm launch");
     if (s != MC_OK) return s;
-    s = hip_status(mc::launch_route(logits + te * r->E, important ? important + te : nullptr, delta32,
-                                    tau, *r, st),
-                   "mc_moe_stack_forward routing launch");
-    if (s != MC_OK) return s;
-    s = hip_status(mc::launch_forward(xn, layer_args(&layers[l]), *r, out, fws, in, st),
+    const mc::RouteArgs ra{logits + te * r->E, important ? important + te : nullptr, delta32, tau};
+    s = hip_status(mc::launch_forward(xn, layer_args(&layers[l]), *r, out, fws, in, st, &ra),
                    "mc_moe_stack_forward forward launch");
     if (s != MC_OK) return s;
     in = out;

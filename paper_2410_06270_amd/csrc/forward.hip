@@ -162,8 +162,12 @@ static hipError_t launch_combine(const float* partial, size_t part_stride, int n
 }
 
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
-                          void* ws, const uint16_t* residual, hipStream_t stream) {
+                          void* ws, const uint16_t* residual, hipStream_t stream, const RouteArgs* route) {
   const int T = r.T, k = r.k;
+  if (route) {
+    const hipError_t err = launch_route(route->logits, route->important, route->delta32, route->tau, r, stream);
+    if (err != hipSuccess) return err;
+  }
   if (T > kDecodeMaxT) {
     float* partial = nullptr;
     size_t part_stride = 0;

@@ -251,13 +251,4 @@ __device__ __forceinline__ void expert_range_offsets(const int32_t* offsets, int
 // A token index from the routing lists, clamped into [0, T).
 __device__ __forceinline__ int clamp_token(int t, int T) { return t < 0 ? 0 : (t >= T ? T - 1 : t); }
 
-struct RouteArgs {
-  const int32_t* counts;
-  const int32_t* offsets;
-  const int32_t* pair_token;
-  const int32_t* pair_pos;
-  const float* topk_w;
-  int T, E, k;
-};
-
 }  // namespace mc

@@ -40,9 +40,19 @@ struct PrefillLayout {
 PrefillLayout prefill_layout(int T, int E, int k, int d, int ffn);
 hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routing& r, void* ws,
                           float** partial, size_t* part_stride, int* nsplit, hipStream_t stream);
+// Routing inputs of a forward call that routes its batch first (the outputs
+// go to the mc_routing buffers as mc_route_and_prune writes them).
+struct RouteArgs {
+  const float* logits;       // [T][E]
+  const uint8_t* important;  // [T] or null
+  float delta32;             // fp32 logit-gap threshold (k = 2)
+  double tau;                // normalised-weight threshold (k > 2)
+};
 // residual (may be null): y = bf16(residual + sum_r w_r E_{e_r}(x)).
+// route (may be null): route the batch first (the routing kernels).
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
-                          void* ws, const uint16_t* residual, hipStream_t stream);
+                          void* ws, const uint16_t* residual, hipStream_t stream,
+                          const RouteArgs* route = nullptr);
 // Stack of layers: xn = RMSNorm(h) (fp64, one bf16 rounding) before each layer.
 constexpr double kRmsNormEps = 1e-5;
 hipError_t launch_rmsnorm(const uint16_t* h, int T, int d, double eps, uint16_t* xn, hipStream_t stream);

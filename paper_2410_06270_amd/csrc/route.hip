@@ -17,7 +17,7 @@
 // everything kept in LDS; larger ones scatter by token blocks, each block
 // counting the selections of all tokens (expert totals) and of the tokens
 // before it (its start in each list).
-#include "mc_internal.hpp"
+#include "route_device.hpp"
 
 namespace mc {
 
@@ -25,162 +25,6 @@ constexpr int kCsrThreads = 1024;
 constexpr int kListBlocks = 64;     // at most this many token blocks scatter the lists
 constexpr int kListMaxBlockT = 1024;
 static_assert(kListBlocks * kListMaxBlockT >= MC_MAX_TOKENS, "list blocks cover every token");
-
-// Order-preserving integer image of a float, with -0 mapped onto +0.
-__device__ __forceinline__ uint32_t ordered_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) == 0) u = 0;
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-// Selects and prunes token t (one wavefront).  Lanes hold the logits (lane l
-// has experts l, l+64, ...) as distinct 64-bit keys (ordered logit bits, then
-// the complement of the expert index, so larger key = earlier rank); each
-// key's rank is the number of larger keys, counted against every key
-// broadcast in turn (no cross-lane reductions).  Lane r < k then takes rank r
-// and evaluates it; the softmax sums run over the ranks in order.  Lane r < k
-// writes rank r's outputs; when s_ent/s_w are given it also records them in
-// LDS (expert, or 0xffff if pruned).
-__device__ void select_token(const float* __restrict__ logits, const uint8_t* __restrict__ important,
-                             int t, int E, int k, float delta32, double tau,
-                             int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
-                             uint8_t* __restrict__ kept, int32_t* __restrict__ pair_pos,
-                             uint16_t* s_ent, float* s_w) {
-  const int lane = threadIdx.x & 63;
-  const float* l = logits + (size_t)t * E;
-  const int nj = (E + 63) >> 6;                      // logits per lane (wave-uniform)
-  float lv[4];
-  unsigned long long key[4];
-  int rank[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = lane + 64 * j;
-    lv[j] = (e < E) ? l[e] : 0.0f;
-  }
-  // the protection flag is loaded beside the logits (one memory round trip)
-  const int prot_flag = important != nullptr ? (int)important[t] : 0;
-  asm volatile("" ::"v"(lv[0]), "v"(lv[1]), "v"(lv[2]), "v"(lv[3]), "v"(prot_flag));
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = lane + 64 * j;
-    key[j] = (e < E) ? (((unsigned long long)ordered_bits(lv[j]) << 32) | (unsigned)(0xffff - e)) : 0ull;
-    rank[j] = 0;
-  }
-  for (int sj = 0; sj < nj; ++sj) {
-    const int n = (E - 64 * sj) < 64 ? (E - 64 * sj) : 64;
-    const unsigned long long ks = sj == 0 ? key[0] : sj == 1 ? key[1] : sj == 2 ? key[2] : key[3];
-    const uint32_t khs = (uint32_t)(ks >> 32), kls = (uint32_t)ks;
-    int src = 0;
-    for (; src + 4 <= n; src += 4) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const unsigned long long o =
-            ((unsigned long long)__builtin_amdgcn_readlane(khs, src + u) << 32) |
-            __builtin_amdgcn_readlane(kls, src + u);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (j < nj) rank[j] += o > key[j] ? 1 : 0;
-      }
-    }
-    for (; src < n; ++src) {
-      const unsigned long long o =
-          ((unsigned long long)__builtin_amdgcn_readlane(khs, src) << 32) | __builtin_amdgcn_readlane(kls, src);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (j < nj) rank[j] += o > key[j] ? 1 : 0;
-    }
-  }
-  const bool prot = prot_flag != 0;
-  int my_e = 0;
-  float my_l = 0.0f;
-  float l0 = 0.0f, l1 = 0.0f;
-  for (int r = 0; r < k; ++r) {
-    int e = 0;
-    float le = 0.0f;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (j < nj) {
-        const unsigned long long b = __ballot(rank[j] == r);
-        if (b) {
-          const int src = __ffsll((long long)b) - 1;
-          e = 64 * j + src;
-          le = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, lv[j]), src));
-        }
-      }
-    }
-    if (r == 0) l0 = le;
-    if (r == 1) l1 = le;
-    if (lane == r) {
-      my_e = e;
-      my_l = le;
-    }
-  }
-  if (k < 2) l1 = l0;
-  const bool mine = lane < k;
-  const double ex = mine ? exp((double)my_l - (double)l0) : 0.0;
-  double sum_all = 0.0;
-  for (int r = 0; r < k; ++r) sum_all += readlane_f64(ex, r);
-  bool keep = mine;
-  if (mine && lane > 0 && !prot) {
-    if (k == 2) {
-      const float gap = l0 - l1;
-      keep = !(gap > delta32);
-    } else {
-      keep = !(ex < tau * sum_all);
-    }
-  }
-  const unsigned long long kb = __ballot(keep);
-  double sum_kept = 0.0;
-  for (int r = 0; r < k; ++r)
-    if ((kb >> r) & 1ull) sum_kept += readlane_f64(ex, r);
-  if (mine) {
-    const size_t o = (size_t)t * k + lane;
-    const float w = keep ? (float)(ex / sum_kept) : 0.0f;
-    topk_idx[o] = my_e;
-    kept[o] = keep ? 1 : 0;
-    topk_w[o] = w;
-    if (!keep) pair_pos[o] = -1;
-    if (s_ent) {
-      s_ent[o] = keep ? (uint16_t)my_e : (uint16_t)0xffff;
-      s_w[o] = w;
-    }
-  }
-}
-
-// Exclusive scan of cnt[0..E) into base[] and offsets[0..E] (one wave: each
-// lane owns 4 consecutive experts); with `publish`, also the global counts
-// and the number of pruned pairs.
-__device__ void scan_counts(int T, int E, int k, const int* cnt, int* base, int32_t* counts, int32_t* offsets,
-                            int32_t* n_pruned, bool publish = true) {
-  const int lane = threadIdx.x & 63;
-  int c[4], local = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = 4 * lane + j;
-    c[j] = e < E ? cnt[e] : 0;
-    local += c[j];
-  }
-  int incl = local;
-  for (int off = 1; off < 64; off <<= 1) {
-    const int v = __shfl_up(incl, off);
-    if (lane >= off) incl += v;
-  }
-  int run = incl - local;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = 4 * lane + j;
-    if (e < E) {
-      base[e] = run;
-      offsets[e] = run;
-      if (publish) counts[e] = c[j];
-    }
-    run += c[j];
-  }
-  if (lane == 63) {
-    offsets[E] = incl;
-    if (publish) *n_pruned = T * k - incl;
-  }
-}
 
 // One pass over the tokens [c0, c0+nc) of expert e held in ent (LDS, indexed
 // from token c0): counts (pass 0) or writes the list entries from run (pass 1).
@@ -219,8 +63,8 @@ __global__ void __launch_bounds__(256) route_select_kernel(const float* __restri
                                                            int32_t* pair_pos) {
   const int t = blockIdx.x * (blockDim.x >> 6) + wave_id();
   if (t >= T) return;
-  select_token(logits, important, t, E, k, delta32, tau, topk_idx, topk_w, kept, pair_pos,
-               nullptr, nullptr);
+  select_token(logits + (size_t)t * E, important != nullptr ? important + t : nullptr, t, E, k, delta32, tau,
+               topk_idx, topk_w, kept, pair_pos, true, nullptr, nullptr);
 }
 
 // Tokens per list block: a multiple of 64, at most kListBlocks blocks.
@@ -239,7 +83,7 @@ __global__ void __launch_bounds__(kCsrThreads) route_scatter_kernel(
     const float* __restrict__ topk_w, int32_t* counts, int32_t* offsets, int32_t* pair_token,
     int32_t* pair_rank, float* pair_w, int32_t* pair_pos, int32_t* n_pruned) {
   __shared__ uint16_t ent[kListMaxBlockT * MC_MAX_TOPK];
-  __shared__ int tot[MC_MAX_EXPERTS], pre[MC_MAX_EXPERTS], base[MC_MAX_EXPERTS];
+  __shared__ int tot[MC_MAX_EXPERTS], pre[MC_MAX_EXPERTS], base[MC_MAX_EXPERTS + 1];
   __shared__ int32_t offs[MC_MAX_EXPERTS + 1];
   const int tid = threadIdx.x, wave = wave_id(), nwaves = blockDim.x >> 6;
   const int t0 = blockIdx.x * BT;
@@ -269,11 +113,8 @@ __global__ void __launch_bounds__(kCsrThreads) route_scatter_kernel(
 }
 
 // Small batches (T <= kRouteFusedMaxT = 64): one launch.  The waves select
-// tokens in parallel (the selection kept in LDS); then wave 0, one lane per
-// token, forms each token's mask of kept experts, counts every expert's
-// tokens with one ballot per expert (the ballots kept in LDS), scans the
-// counts, and writes each kept pair at its expert's offset plus the number of
-// earlier tokens with that expert -- lists in token order, no atomics.
+// tokens in parallel (the selections kept in LDS), then wave 0 builds the
+// lists (small_batch_lists).
 __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
     const float* __restrict__ logits, const uint8_t* __restrict__ important, int T, int E, int k,
     float delta32, double tau, int32_t* topk_idx, float* topk_w, uint8_t* kept, int32_t* counts,
@@ -283,65 +124,16 @@ __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
   __shared__ uint16_t ent[kRouteFusedMaxT * MC_MAX_TOPK];
   __shared__ float wsel[kRouteFusedMaxT * MC_MAX_TOPK];
   __shared__ int cnt[MC_MAX_EXPERTS];
-  __shared__ int base[MC_MAX_EXPERTS];
+  __shared__ int base[MC_MAX_EXPERTS + 1];
   __shared__ unsigned long long bal[MC_MAX_EXPERTS];
-  const int wave = wave_id(), nwaves = blockDim.x >> 6, lane = threadIdx.x & 63;
+  const int wave = wave_id(), nwaves = blockDim.x >> 6;
   for (int t = wave; t < T; t += nwaves)
-    select_token(logits, important, t, E, k, delta32, tau, topk_idx, topk_w, kept, pair_pos, ent,
-                 wsel);
+    select_token(logits + (size_t)t * E, important != nullptr ? important + t : nullptr, t, E, k, delta32, tau,
+                 topk_idx, topk_w, kept, pair_pos, true, ent, wsel);
   __syncthreads();
   if (wave != 0) return;
-  const bool act = lane < T;
-  int my_e[MC_MAX_TOPK];
-  unsigned long long m[MC_MAX_EXPERTS / 64] = {0ull, 0ull, 0ull, 0ull};
-#pragma unroll
-  for (int r = 0; r < MC_MAX_TOPK; ++r) {
-    my_e[r] = 0xffff;
-    if (act && r < k) {
-      const int e = ent[lane * k + r];
-      my_e[r] = e;
-      if (e != 0xffff) {
-        const unsigned long long bit = 1ull << (e & 63);
-#pragma unroll
-        for (int j = 0; j < MC_MAX_EXPERTS / 64; ++j) m[j] |= (e >> 6) == j ? bit : 0ull;
-      }
-    }
-  }
-  for (int e = lane; e < E; e += 64) cnt[e] = 0;
-#pragma unroll
-  for (int j = 0; j < MC_MAX_EXPERTS / 64; ++j) {
-    if (64 * j >= E) break;
-    // experts of this 64-block that some token selected (OR over the lanes)
-    unsigned long long any = m[j];
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint32_t lo = __shfl_xor((uint32_t)any, off), hi = __shfl_xor((uint32_t)(any >> 32), off);
-      any |= ((unsigned long long)hi << 32) | lo;
-    }
-    any = ((unsigned long long)__builtin_amdgcn_readfirstlane((uint32_t)(any >> 32)) << 32) |
-          __builtin_amdgcn_readfirstlane((uint32_t)any);
-    while (any) {
-      const int i = __ffsll((long long)any) - 1;
-      any &= any - 1ull;
-      const unsigned long long b = __ballot((m[j] >> i) & 1ull);
-      if (lane == 0) {
-        cnt[64 * j + i] = __popcll(b);
-        bal[64 * j + i] = b;
-      }
-    }
-  }
-  scan_counts(T, E, k, cnt, base, counts, offsets, n_pruned);
-  const unsigned long long below = (1ull << lane) - 1ull;
-#pragma unroll
-  for (int r = 0; r < MC_MAX_TOPK; ++r) {
-    const int e = my_e[r];
-    if (e != 0xffff) {
-      const int pos = base[e] + __popcll(bal[e] & below);
-      pair_token[pos] = lane;
-      pair_rank[pos] = r;
-      pair_w[pos] = wsel[lane * k + r];
-      pair_pos[lane * k + r] = pos;
-    }
-  }
+  const RouteLds s{ent, wsel, cnt, base, bal};
+  small_batch_lists(T, E, k, s, true, counts, offsets, pair_token, pair_rank, pair_w, pair_pos, n_pruned);
 }
 
 hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,
