@@ -61,10 +61,11 @@ __global__ void __launch_bounds__(256) route_select_kernel(const float* __restri
                                                            double tau, int32_t* topk_idx,
                                                            float* topk_w, uint8_t* kept,
                                                            int32_t* pair_pos) {
+  __shared__ __attribute__((aligned(16))) unsigned char scratch[4][kSelScratchBytes];
   const int t = blockIdx.x * (blockDim.x >> 6) + wave_id();
   if (t >= T) return;
   select_token(logits + (size_t)t * E, important != nullptr ? important + t : nullptr, t, E, k, delta32, tau,
-               topk_idx, topk_w, kept, pair_pos, true, nullptr, nullptr);
+               topk_idx, topk_w, kept, pair_pos, true, nullptr, nullptr, sel_scratch(scratch[wave_id()]));
 }
 
 // Tokens per list block: a multiple of 64, at most kListBlocks blocks.
@@ -126,10 +127,12 @@ __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
   __shared__ int cnt[MC_MAX_EXPERTS];
   __shared__ int base[MC_MAX_EXPERTS + 1];
   __shared__ unsigned long long bal[MC_MAX_EXPERTS];
+  __shared__ __attribute__((aligned(16))) unsigned char scratch[kCsrThreads / 64][kSelScratchBytes];
   const int wave = wave_id(), nwaves = blockDim.x >> 6;
+  const SelScratch sc = sel_scratch(scratch[wave]);
   for (int t = wave; t < T; t += nwaves)
     select_token(logits + (size_t)t * E, important != nullptr ? important + t : nullptr, t, E, k, delta32, tau,
-                 topk_idx, topk_w, kept, pair_pos, true, ent, wsel);
+                 topk_idx, topk_w, kept, pair_pos, true, ent, wsel, sc);
   __syncthreads();
   if (wave != 0) return;
   const RouteLds s{ent, wsel, cnt, base, bal};

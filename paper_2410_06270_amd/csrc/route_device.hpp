@@ -13,21 +13,39 @@ __device__ __forceinline__ uint32_t ordered_bits(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Per-wave LDS scratch of the selection: the token's E keys, the k selected
+// (expert, logit) pairs in rank order and their exp terms.
+struct SelScratch {
+  unsigned long long* key;   // [E]
+  int* sel_e;                // [k]
+  float* sel_l;              // [k]
+  double* ex;                // [k]
+};
+constexpr int kSelScratchBytes = MC_MAX_EXPERTS * 8 + MC_MAX_TOPK * (4 + 4 + 8);
+
+__device__ __forceinline__ SelScratch sel_scratch(unsigned char* base) {
+  SelScratch s;
+  s.key = reinterpret_cast<unsigned long long*>(base);
+  s.ex = reinterpret_cast<double*>(base + MC_MAX_EXPERTS * 8);
+  s.sel_e = reinterpret_cast<int*>(base + MC_MAX_EXPERTS * 8 + MC_MAX_TOPK * 8);
+  s.sel_l = reinterpret_cast<float*>(base + MC_MAX_EXPERTS * 8 + MC_MAX_TOPK * 12);
+  return s;
+}
+
 // Selects and prunes token t (one wavefront).  Lanes hold the logits (lane l
 // has experts l, l+64, ...) as distinct 64-bit keys (ordered logit bits, then
-// the complement of the expert index, so larger key = earlier rank); each
-// key's rank is the number of larger keys, counted against every key
-// broadcast in turn (no cross-lane reductions).  Lane r < k then takes rank r
-// and evaluates it; the softmax sums run over the ranks in order.  Lane r < k
+// the complement of the expert index, so larger key = earlier rank); the keys
+// go to the wave's LDS scratch and each key's rank is the number of larger
+// keys, read back as broadcasts.  The rank-r pair goes to slot r, lane r < k
+// takes it; the softmax sums run over the ranks in order (fp64).  Lane r < k
 // writes rank r's outputs (when `publish`); when s_ent/s_w are given it also
 // records them in LDS (expert, or 0xffff if pruned).  l: the token's E logits
 // and prot_src: its protection flag (NULL: unprotected), in memory or LDS.
 static __device__ void select_token(const float* l, const uint8_t* prot_src, int t, int E, int k, float delta32,
                                     double tau, int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
                                     uint8_t* __restrict__ kept, int32_t* __restrict__ pair_pos, bool publish,
-                                    uint16_t* s_ent, float* s_w) {
+                                    uint16_t* s_ent, float* s_w, const SelScratch& sc) {
   const int lane = threadIdx.x & 63;
-  const int nj = (E + 63) >> 6;                      // logits per lane (wave-uniform)
   float lv[4];
   unsigned long long key[4];
   int rank[4];
@@ -44,61 +62,46 @@ static __device__ void select_token(const float* l, const uint8_t* prot_src, int
     const int e = lane + 64 * j;
     key[j] = (e < E) ? (((unsigned long long)ordered_bits(lv[j]) << 32) | (unsigned)(0xffff - e)) : 0ull;
     rank[j] = 0;
+    if (e < E) sc.key[e] = key[j];
   }
-  for (int sj = 0; sj < nj; ++sj) {
-    const int n = (E - 64 * sj) < 64 ? (E - 64 * sj) : 64;
-    const unsigned long long ks = sj == 0 ? key[0] : sj == 1 ? key[1] : sj == 2 ? key[2] : key[3];
-    const uint32_t khs = (uint32_t)(ks >> 32), kls = (uint32_t)ks;
-    int src = 0;
-    for (; src + 4 <= n; src += 4) {
+  __builtin_amdgcn_wave_barrier();
+  const int nj = (E + 63) >> 6;                      // keys per lane (wave-uniform)
+  int e2 = 0;
+  for (; e2 + 4 <= E; e2 += 4) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const unsigned long long o =
-            ((unsigned long long)__builtin_amdgcn_readlane(khs, src + u) << 32) |
-            __builtin_amdgcn_readlane(kls, src + u);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (j < nj) rank[j] += o > key[j] ? 1 : 0;
-      }
-    }
-    for (; src < n; ++src) {
-      const unsigned long long o =
-          ((unsigned long long)__builtin_amdgcn_readlane(khs, src) << 32) | __builtin_amdgcn_readlane(kls, src);
+    for (int u = 0; u < 4; ++u) {
+      const unsigned long long o = sc.key[e2 + u];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (j < nj) rank[j] += o > key[j] ? 1 : 0;
     }
   }
-  const bool prot = prot_flag != 0;
-  int my_e = 0;
-  float my_l = 0.0f;
-  float l0 = 0.0f, l1 = 0.0f;
-  for (int r = 0; r < k; ++r) {
-    int e = 0;
-    float le = 0.0f;
+  for (; e2 < E; ++e2) {
+    const unsigned long long o = sc.key[e2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (j < nj) {
-        const unsigned long long b = __ballot(rank[j] == r);
-        if (b) {
-          const int src = __ffsll((long long)b) - 1;
-          e = 64 * j + src;
-          le = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, lv[j]), src));
-        }
-      }
-    }
-    if (r == 0) l0 = le;
-    if (r == 1) l1 = le;
-    if (lane == r) {
-      my_e = e;
-      my_l = le;
+    for (int j = 0; j < 4; ++j)
+      if (j < nj) rank[j] += o > key[j] ? 1 : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + 64 * j;
+    if (e < E && rank[j] < k) {
+      sc.sel_e[rank[j]] = e;
+      sc.sel_l[rank[j]] = lv[j];
     }
   }
-  if (k < 2) l1 = l0;
+  __builtin_amdgcn_wave_barrier();
   const bool mine = lane < k;
+  const int my_e = mine ? sc.sel_e[lane] : 0;
+  const float my_l = mine ? sc.sel_l[lane] : 0.0f;
+  const float l0 = sc.sel_l[0];
+  const float l1 = k < 2 ? l0 : sc.sel_l[1];
+  const bool prot = prot_flag != 0;
   const double ex = mine ? exp((double)my_l - (double)l0) : 0.0;
+  if (mine) sc.ex[lane] = ex;
+  __builtin_amdgcn_wave_barrier();
   double sum_all = 0.0;
-  for (int r = 0; r < k; ++r) sum_all += readlane_f64(ex, r);
+  for (int r = 0; r < k; ++r) sum_all += sc.ex[r];
   bool keep = mine;
   if (mine && lane > 0 && !prot) {
     if (k == 2) {
@@ -111,7 +114,7 @@ static __device__ void select_token(const float* l, const uint8_t* prot_src, int
   const unsigned long long kb = __ballot(keep);
   double sum_kept = 0.0;
   for (int r = 0; r < k; ++r)
-    if ((kb >> r) & 1ull) sum_kept += readlane_f64(ex, r);
+    if ((kb >> r) & 1ull) sum_kept += sc.ex[r];
   if (mine) {
     const size_t o = (size_t)t * k + lane;
     const float w = keep ? (float)(ex / sum_kept) : 0.0f;
@@ -126,6 +129,7 @@ static __device__ void select_token(const float* l, const uint8_t* prot_src, int
       s_w[o] = w;
     }
   }
+  __builtin_amdgcn_wave_barrier();   // the scratch is free for the wave's next token
 }
 
 // Exclusive scan of cnt[0..E) into base[] and offsets[0..E] (one wave: each
@@ -180,57 +184,30 @@ struct RouteLds {
 };
 
 // Lists of a small batch from the selections in LDS (one wavefront, lane t =
-// token t): every token's mask of kept experts, one ballot per selected expert
-// (the tokens that chose it), the counts' scan, then each kept pair at its
-// expert's offset plus the number of earlier tokens with that expert -- lists
-// in token order, no atomics.  With `publish` the routing outputs go to memory.
+// token t): every kept pair ORs its token's bit into its expert's mask (LDS
+// atomics; an OR does not depend on the order), the masks give the counts,
+// the counts' scan the list starts, and each kept pair goes to its expert's
+// start plus the number of earlier tokens with that expert -- lists in token
+// order.  With `publish` the routing outputs go to memory.
 static __device__ void small_batch_lists(int T, int E, int k, const RouteLds& s, bool publish, int32_t* counts,
                                          int32_t* offsets, int32_t* pair_token, int32_t* pair_rank, float* pair_w,
                                          int32_t* pair_pos, int32_t* n_pruned) {
   const int lane = threadIdx.x & 63;
   const bool act = lane < T;
   int my_e[MC_MAX_TOPK];
-  unsigned long long m[MC_MAX_EXPERTS / 64] = {0ull, 0ull, 0ull, 0ull};
 #pragma unroll
-  for (int r = 0; r < MC_MAX_TOPK; ++r) {
-    my_e[r] = 0xffff;
-    if (act && r < k) {
-      const int e = s.ent[lane * k + r];
-      my_e[r] = e;
-      if (e != 0xffff) {
-        const unsigned long long bit = 1ull << (e & 63);
+  for (int r = 0; r < MC_MAX_TOPK; ++r) my_e[r] = (act && r < k) ? s.ent[lane * k + r] : 0xffff;
+  for (int e = lane; e < E; e += 64) s.bal[e] = 0ull;
+  __builtin_amdgcn_wave_barrier();
 #pragma unroll
-        for (int j = 0; j < MC_MAX_EXPERTS / 64; ++j) m[j] |= (e >> 6) == j ? bit : 0ull;
-      }
-    }
-  }
-  for (int e = lane; e < E; e += 64) {
-    s.cnt[e] = 0;
-    s.bal[e] = 0ull;
-  }
-#pragma unroll
-  for (int j = 0; j < MC_MAX_EXPERTS / 64; ++j) {
-    if (64 * j >= E) break;
-    // experts of this 64-block that some token selected (OR over the lanes)
-    unsigned long long any = m[j];
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint32_t lo = __shfl_xor((uint32_t)any, off), hi = __shfl_xor((uint32_t)(any >> 32), off);
-      any |= ((unsigned long long)hi << 32) | lo;
-    }
-    any = ((unsigned long long)__builtin_amdgcn_readfirstlane((uint32_t)(any >> 32)) << 32) |
-          __builtin_amdgcn_readfirstlane((uint32_t)any);
-    while (any) {
-      const int i = __ffsll((long long)any) - 1;
-      any &= any - 1ull;
-      const unsigned long long b = __ballot((m[j] >> i) & 1ull);
-      if (lane == 0) {
-        s.cnt[64 * j + i] = __popcll(b);
-        s.bal[64 * j + i] = b;
-      }
-    }
-  }
+  for (int r = 0; r < MC_MAX_TOPK; ++r)
+    if (my_e[r] != 0xffff) atomicOr(&s.bal[my_e[r]], 1ull << lane);
+  __builtin_amdgcn_wave_barrier();
+  for (int e = lane; e < E; e += 64) s.cnt[e] = __popcll(s.bal[e]);
+  __builtin_amdgcn_wave_barrier();
   scan_counts(T, E, k, s.cnt, s.base, counts, offsets, n_pruned, publish);
   if (!publish) return;
+  __builtin_amdgcn_wave_barrier();
   const unsigned long long below = (1ull << lane) - 1ull;
 #pragma unroll
   for (int r = 0; r < MC_MAX_TOPK; ++r) {
