@@ -16,11 +16,11 @@
 // U without forming H^-1: with J the index reversal, J H J = L L^T (lower
 // Cholesky) gives H = V V^T with V = J L J upper triangular, so H^-1 =
 // V^-T V^-1 and U = V^-1 = J L^-1 J.  The factor step therefore runs one
-// blocked Cholesky and one blocked triangular inverse on the reversed matrix.
+// blocked Cholesky and one recursive triangular inverse on the reversed matrix.
 //
 // Kernels: a tiled fp64 GEMM with arbitrary (also negative) strides carries
 // the bulk of every step (Hessian, Cholesky trailing updates, the inverse's
-// off-diagonal blocks, GPTQ's deferred updates); the sequential parts run one
+// corner blocks, GPTQ's deferred updates); the sequential parts run one
 // wavefront per row (64 x 64 triangular solves with readlane broadcasts, and
 // the GPTQ column loop over 128-column blocks with the block of U in LDS).
 #include "mc_internal.hpp"
@@ -249,8 +249,37 @@ static unsigned grid_for(long long n) {
   return (unsigned)(b < 16384 ? b : 16384);
 }
 
+// Rows/columns of the first half of a recursive split of n (a multiple of 64).
+static int split_half(int n) { return ((n / kNb) / 2) * kNb; }
+
+// Workspace of the factor: the reversed matrix and its Cholesky factor (in
+// place), the inverse, the inverse's scratch product (at most the first split's
+// (n - n1) x n1 block) and one scalar.
 size_t gptq_factor_bytes(int K) {
-  return 2 * (size_t)K * K * sizeof(double) + (size_t)kNb * K * sizeof(double) + 256;
+  const int n1 = split_half(K);
+  return 2 * (size_t)K * K * sizeof(double) + (size_t)(K - n1) * (size_t)(n1 > 0 ? n1 : 1) * sizeof(double) + 256;
+}
+
+// Mi[off..off+n)^2 = inverse of the lower-triangular L[off..off+n)^2 (both
+// row-major with leading dimension K; Mi's strictly upper part in the range
+// is zero on entry and stays zero).  With L = [[A, 0], [B, C]]:
+// L^-1 = [[A^-1, 0], [-C^-1 B A^-1, C^-1]], the two halves recursively, the
+// corner by two GEMMs through the scratch X; 64 x 64 blocks by wavefront
+// substitution.
+static void tri_inverse(const double* L, double* Mi, double* X, int K, int off, int n, hipStream_t st) {
+  if (n == kNb) {
+    hipLaunchKernelGGL(tri_inv_diag_kernel, dim3(1), dim3(1024), 0, st, L, K, off / kNb, Mi);
+    return;
+  }
+  const int n1 = split_half(n), n2 = n - n1;
+  tri_inverse(L, Mi, X, K, off, n1, st);
+  tri_inverse(L, Mi, X, K, off + n1, n2, st);
+  const double* B = L + (size_t)(off + n1) * K + off;             // n2 x n1
+  const double* Ainv = Mi + (size_t)off * K + off;                // n1 x n1
+  const double* Cinv = Mi + (size_t)(off + n1) * K + off + n1;    // n2 x n2
+  zero2d(X, n2, n1, n1, st);
+  gemm<double, double>(n2, n1, n1, 1.0, B, K, 1, Ainv, K, 1, X, n1, false, st);          // X = B A^-1
+  gemm<double, double>(n2, n1, n2, -1.0, Cinv, K, 1, X, n1, 1, Mi + (size_t)(off + n1) * K + off, K, false, st);
 }
 
 hipError_t launch_gptq_hessian(const uint16_t* x, int N, int K, double* H, bool accumulate, hipStream_t st) {
@@ -266,8 +295,9 @@ hipError_t launch_gptq_factor(const double* H, int K, double damp, double* U, ui
                               hipStream_t st) {
   double* A = static_cast<double*>(ws);
   double* Mi = A + (size_t)K * K;
-  double* T = Mi + (size_t)K * K;
-  double* aux = T + (size_t)kNb * K;
+  double* X = Mi + (size_t)K * K;
+  const int n1 = split_half(K);
+  double* aux = X + (size_t)(K - n1) * (size_t)(n1 > 0 ? n1 : 1);
   const int nb = K / kNb;
   timing_begin(st, kSiteGptqFactor);
   hipLaunchKernelGGL(gptq_diag_kernel, dim3(1), dim3(1024), 0, st, H, K, damp, dead, aux);
@@ -283,16 +313,7 @@ hipError_t launch_gptq_factor(const double* H, int K, double damp, double* U, ui
                            A + (size_t)(kb + 1) * kNb * K + (size_t)(kb + 1) * kNb, K, true, st);
     }
   }
-  for (int ib = 0; ib < nb; ++ib) {
-    hipLaunchKernelGGL(tri_inv_diag_kernel, dim3(1), dim3(1024), 0, st, A, K, ib, Mi);
-    if (ib > 0) {
-      const int w = ib * kNb;
-      zero2d(T, kNb, w, K, st);
-      gemm<double, double>(kNb, w, w, 1.0, A + (size_t)w * K, K, 1, Mi, K, 1, T, K, false, st);
-      gemm<double, double>(kNb, w, kNb, -1.0, Mi + (size_t)w * K + w, K, 1, T, K, 1, Mi + (size_t)w * K, K, false,
-                           st);
-    }
-  }
+  tri_inverse(A, Mi, X, K, 0, K, st);
   hipLaunchKernelGGL(gptq_unreverse_kernel, dim3(grid_for((long long)K * K)), dim3(256), 0, st, Mi, K, U);
   timing_end(st, kSiteGptqFactor);
   return hipGetLastError();
