@@ -16,6 +16,10 @@
  *   mc_moe_forward     Eq. 1 over the packed SwiGLU experts
  *   mc_moe_route_forward  routing and Eq. 1 in one call
  *   mc_moe_stack_forward  a stack of MoE layers with residual connections
+ *   mc_token_importance   Eq. 6 token importance -> the protected set
+ *   mc_odp_threshold, mc_pmq_significance, mc_pmq_allocate
+ *                      host helpers: the pruning threshold, expert
+ *                      significance and the Eq. 4 width allocation
  *
  * Conventions for every call
  *   - Pointers are DEVICE pointers unless the comment says "host".
@@ -183,7 +187,7 @@ typedef struct mc_routing {
  *                     NULL): [R] fp64, sum_k e_k^2 / 2 per row.
  *
  * K (the input width) must be a multiple of 128, at most MC_GPTQ_MAX_K.
- * Workspace: mc_gptq_workspace(R, K) bytes (2 K^2 + 64 K doubles for the
+ * Workspace: mc_gptq_workspace(R, K) bytes (about 2.25 K^2 doubles for the
  * factor, R K (8 + 1) + 1024 R bytes for the quantizer), 8-byte aligned.
  * Errors: MC_EINVAL (shape, NULL or misaligned pointer, damp < 0 or not
  * finite), MC_ENOSPACE (workspace or layer buffers), MC_EHIP. */
