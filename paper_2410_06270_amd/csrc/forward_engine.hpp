@@ -287,6 +287,9 @@ __device__ __forceinline__ void compute_chunk(const uint32_t (&w)[2][BITS],
         group_end<BITS>(acc[1][tb], tot[1][tb], s[1][q], sxp);
       }
     }
+    // steps stay in order: hoisting the B operands of later steps ahead of
+    // their MFMAs runs the 32-token kernels out of registers (spills)
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -347,6 +350,10 @@ __device__ __forceinline__ void stream_pair(const Streams& sp, int c_begin, int 
       for (int j = 0; j < D; ++j) {
         compute_chunk<BITS, NT, GPC, F16>(wr[j], sr[j], acc, tot, arow, sxs, c + j - c0, lane, magic);
         load_chunk<BITS, GPC>(wr[j], sr[j], sp, c + j + D - c_begin, last);
+        // the refill issues here, not later: left to itself the scheduler
+        // sinks all refills of the unrolled ring to the end of the loop body,
+        // behind a wait for every load in flight, which drains the ring
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
 #pragma unroll
