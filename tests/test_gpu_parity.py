@@ -230,6 +230,26 @@ def test_forward_split_reduction(mc, d, T):
     assert mae < 2e-4, mae
 
 
+def test_forward_max_tokens_sampled(mc, tiny):
+    """The token limit of a call (65536) through the grouped GEMMs: every
+    kept pair of the batch is computed, sampled tokens (first, last, a pruned
+    one, a protected one, and a seeded spread) are checked against the oracle."""
+    L, logical, G = tiny
+    T = 65536
+    x = synthetic.activations(1, T)
+    lg = synthetic.logits(1, T)
+    imp = synthetic.important_mask(1, T)
+    y, r = forward_gpu(mc, L, x, lg, imp, 2, 0.3)
+    ref = oracle.route(lg, imp, 2, 0.3)
+    np.testing.assert_array_equal(r.counts.cpu().numpy(), ref["counts"])
+    toks = {0, T - 1, int(np.nonzero(ref["kept"][:, 1] == 0)[0][0]), int(np.nonzero(imp)[0][0])}
+    toks |= set(np.random.default_rng(65536).choice(T, 60, replace=False).tolist())
+    toks = sorted(toks)
+    y_ref = oracle.moe_forward(x, ref, logical, G, tokens=toks)
+    mae, _ = check_tol(y[toks], y_ref)
+    assert mae < 2e-4, mae
+
+
 @pytest.mark.parametrize("cid,E,d,ffn,T,hot", [
     (1, 4, 256, 512, 300, None),      # G = 32, ragged 32-row fragments
     (1, 4, 384, 256, 257, None),      # d not a multiple of the 256-row down tile
