@@ -42,6 +42,13 @@ constexpr int kMaxKsplit = 2;                 // largest split of the gate/up re
 constexpr int kXsBytes = 75 * 1024 + 512;
 constexpr int kLdsPerCu = 160 * 1024;
 static_assert(2 * (kXsBytes + 4 * 1024 + 32 * 4) <= kLdsPerCu, "two workgroups per CU");
+// The gate/up kernel of batches with up to 32 tokens per expert runs one
+// workgroup of 16 waves per CU instead (the same 16 waves): its slab then
+// takes all of d = 4096 for up to 16 tokens and half of it for 32, against
+// two and four slabs in 75.5 KB, and each slab change drains the weight ring.
+constexpr int kGuWaves32 = 16;
+constexpr int kGuXsBytes32 = 146 * 1024;
+static_assert(kGuXsBytes32 + 4 * 1024 + 32 * 4 + 512 <= kLdsPerCu, "one 16-wave gate/up workgroup per CU");
 // Chunks (16 rows x 128 columns of codes) kept in flight per stream.  The slab
 // is a multiple of this many chunks, so it is smaller where the slab rows are
 // many (token blocks) or the registers few (groups per chunk).
@@ -55,6 +62,7 @@ constexpr int slab_floor_bytes(int ntb) {
 }
 static_assert(slab_floor_bytes(1) <= kXsBytes, "LDS budget (<= 16 tokens)");
 static_assert(slab_floor_bytes(2) <= kXsBytes, "LDS budget (<= 32 tokens)");
+static_assert(slab_floor_bytes(2) <= kGuXsBytes32, "LDS budget (<= 32 tokens, 16 waves)");
 // Group sums: 16*ntb rows x (slab / G) groups x 4 bytes; the slab is capped by
 // kSxBytes, which must allow at least one ring of chunks at G = 32.
 static_assert((kSxBytes / (4 * 32)) * 32 >= 4 * kTileCols, "group-sum budget (32 tokens)");
