@@ -42,10 +42,11 @@ constexpr int kMaxKsplit = 2;                 // largest split of the gate/up re
 constexpr int kXsBytes = 75 * 1024 + 512;
 constexpr int kLdsPerCu = 160 * 1024;
 static_assert(2 * (kXsBytes + 4 * 1024 + 32 * 4) <= kLdsPerCu, "two workgroups per CU");
-// The gate/up kernel of batches with up to 32 tokens per expert runs one
-// workgroup of 16 waves per CU instead (the same 16 waves): its slab then
-// takes all of d = 4096 for up to 16 tokens and half of it for 32, against
-// two and four slabs in 75.5 KB, and each slab change drains the weight ring.
+// The kernels of 32-token blocks run one workgroup of 16 waves per CU
+// instead (the same 16 waves): the gate/up slab then takes all of d = 4096
+// for up to 16 tokens and half of it for 32, against two and four slabs in
+// 75.5 KB, the down slab a whole ffn split, and each slab change drains the
+// weight ring.
 constexpr int kGuWaves32 = 16;
 constexpr int kGuXsBytes32 = 146 * 1024;
 static_assert(kGuXsBytes32 + 4 * 1024 + 32 * 4 + 512 <= kLdsPerCu, "one 16-wave gate/up workgroup per CU");

@@ -116,13 +116,13 @@ __attribute__((amdgpu_waves_per_eu(4))) gateup_kernel(
 }
 
 // ------------------------------------------------------------------- down --
-// Workgroup: expert e, 32*kWavesPerWg output rows (two 16-row blocks per
+// Workgroup: expert e, 32*WAVES output rows (two 16-row blocks per
 // wave), one split of the ffn reduction, up to 16*NTMAX of the expert's pairs
 // -> fp32 partials.  When d is not a multiple of the workgroup's rows, the
 // surplus waves of the last workgroup repeat the last row blocks (identical
 // values written twice) so that every wave takes part in the staging barriers.
-template <int GPC, int NTMAX>
-__global__ void __launch_bounds__(64 * kWavesPerWg)
+template <int GPC, int NTMAX, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES)
 __attribute__((amdgpu_waves_per_eu(4))) down_kernel(
     Hidden hid, LayerArgs L, const int32_t* __restrict__ counts,
     const int32_t* __restrict__ offsets, int nsplit, float* __restrict__ partial,
@@ -145,7 +145,7 @@ __attribute__((amdgpu_waves_per_eu(4))) down_kernel(
   const int c_begin = split * per;
   const int c_end = (c_begin + per) < ntiles ? (c_begin + per) : ntiles;
   const int last_rb = L.d / kTileRows - 2;
-  const int rb_want = (blockIdx.x * kWavesPerWg + wave) * 2;
+  const int rb_want = (blockIdx.x * WAVES + wave) * 2;
   const int rb0 = rb_want < last_rb ? rb_want : last_rb;
   f32x4 tot[2][NTMAX];
   zero_tot(&tot[0][0], 2 * NTMAX);
@@ -231,29 +231,25 @@ static hipError_t launch_gateup_nt(const uint16_t* x, const LayerArgs& L, const 
   return hipGetLastError();
 }
 
-template <int GPC, int NTMAX>
+template <int GPC, int NTMAX, int WAVES>
 static hipError_t launch_down_nt(const Hidden& h, const LayerArgs& L, const mc_routing& r,
                                  int nsplit, float* partial, size_t part_stride, int xs_bytes,
                                  hipStream_t stream) {
   static bool attr = false;
   if (!attr) {
-    hipError_t e = allow_lds(&down_kernel<GPC, NTMAX>, kXsBytes + kSxBytes + 512);
+    hipError_t e = allow_lds(&down_kernel<GPC, NTMAX, WAVES>, xs_bytes + kSxBytes + 512);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int chunks = (r.T + 16 * NTMAX - 1) / (16 * NTMAX);
-  const int rows_per_wg = 32 * kWavesPerWg;
-  hipLaunchKernelGGL((down_kernel<GPC, NTMAX>),
+  const int rows_per_wg = 32 * WAVES;
+  hipLaunchKernelGGL((down_kernel<GPC, NTMAX, WAVES>),
                      dim3((L.d + rows_per_wg - 1) / rows_per_wg, L.E, chunks * nsplit),
-                     dim3(64 * kWavesPerWg), xs_bytes + kSxBytes, stream, h, L, r.counts,
+                     dim3(64 * WAVES), xs_bytes + kSxBytes, stream, h, L, r.counts,
                      r.offsets, nsplit, partial, part_stride, xs_bytes);
   return hipGetLastError();
 }
 
-// 16-token blocks: 8-wave workgroups, two per CU.  32-token blocks: one
-// 16-wave workgroup per CU with the larger slab, where ffn is a multiple of
-// its 256 rows (measured: gate/up 105 -> 96 us at T = 64, the step 3 % and
-// 5 % shorter at T = 32 and 64; with 16-token blocks it was slower).
 template <int GPC>
 hipError_t launch_gateup(const uint16_t* x, const LayerArgs& L, const mc_routing& r,
                          const Hidden& h, int ntmax, int xs_bytes, hipStream_t stream) {
@@ -263,12 +259,16 @@ hipError_t launch_gateup(const uint16_t* x, const LayerArgs& L, const mc_routing
   return launch_gateup_nt<GPC, 2, kWavesPerWg>(x, L, r, h, xs_bytes, stream);
 }
 
+// As for gate/up: 32-token blocks take one 16-wave workgroup per CU (512
+// output rows) with the larger h slab (measured: down 42.9 -> 39.7 us at
+// T = 32, 58.6 -> 52.7 us at T = 64; slower for 16-token blocks).
 template <int GPC>
 hipError_t launch_down(const Hidden& h, const LayerArgs& L, const mc_routing& r, int nsplit,
                        float* partial, size_t part_stride, int ntmax, int xs_bytes,
                        hipStream_t stream) {
-  if (ntmax == 1) return launch_down_nt<GPC, 1>(h, L, r, nsplit, partial, part_stride, xs_bytes, stream);
-  return launch_down_nt<GPC, 2>(h, L, r, nsplit, partial, part_stride, xs_bytes, stream);
+  if (ntmax == 1)
+    return launch_down_nt<GPC, 1, kWavesPerWg>(h, L, r, nsplit, partial, part_stride, xs_bytes, stream);
+  return launch_down_nt<GPC, 2, kGuWaves32>(h, L, r, nsplit, partial, part_stride, kGuXsBytes32, stream);
 }
 
 }  // namespace mc
