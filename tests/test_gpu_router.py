@@ -45,7 +45,7 @@ def assert_faithful(got, x_bits, w_bits, tokens):
     w = oracle.bf16_to_float64(w_bits)
     d = x.shape[1]
     ref = oracle.router_logits(x_bits, w_bits, tokens=tokens)
-    exact = ambiguous = 0
+    exact = ambiguous = ties = 0
     for t in tokens:
         for e in range(w.shape[0]):
             p = (x[t] * w[e]).tolist()
@@ -61,7 +61,8 @@ def assert_faithful(got, x_bits, w_bits, tokens):
                 exact += 1
             else:
                 ambiguous += 1
-    return exact, ambiguous
+                ties += s == lo or s == hi      # the exact sum on an fp32 midpoint
+    return exact, ambiguous, ties
 
 
 def sample_tokens(T, n=24, seed=0):
@@ -77,14 +78,19 @@ def sample_tokens(T, n=24, seed=0):
     (3, 4096, 4096, 8),                                       # Mixtral prefill (sampled)
     (4, 16, 2048, 64), (4, 2048, 2048, 64),                   # OLMoE decode / prefill (sampled)
     (1, 3, 8, 13),                                            # smallest d, experts not a multiple of 8
+    (1, 37, 40, 20), (1, 1, 8, 256), (1, 300, 264, 48),       # fma path: experts >= 16, small batches
+    (1, 600, 264, 48), (1, 1029, 40, 20), (1, 512, 8, 256),   # MFMA tiles: ragged tokens, experts and d
 ])
 def test_router_logits_parity(mc, cid, T, d, E):
     x = synthetic.activations(cid, T, d=d)
     w = synthetic.router_weights(cid, E=E, d=d)
     got = router_gpu(mc, x, w)
     assert np.isfinite(got).all()
-    exact, ambiguous = assert_faithful(got, x, w, sample_tokens(T))
-    assert exact >= 0.9 * (exact + ambiguous)      # logits near 0 have a fine fp32 grid
+    exact, ambiguous, ties = assert_faithful(got, x, w, sample_tokens(T))
+    # the bit-exact class must not be vacuous: short sums of bf16 products
+    # often land exactly on an fp32 midpoint (ties, ambiguous by the bar), the
+    # rest is ambiguous only within the fp64 error band
+    assert exact >= 0.9 * (exact + ambiguous - ties)
 
 
 def _row(v, d=8):
