@@ -217,12 +217,10 @@ static hipError_t allow_lds(K kernel, int bytes) {
 template <int GPC, int NTMAX, int WAVES>
 static hipError_t launch_gateup_nt(const uint16_t* x, const LayerArgs& L, const mc_routing& r,
                                    const Hidden& h, int xs_bytes, hipStream_t stream) {
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = allow_lds(&gateup_kernel<GPC, NTMAX, WAVES>, xs_bytes + kSxBytes + 512);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
+  // set once per instantiation (thread-safe static initialisation); the slab
+  // size of an instantiation is fixed
+  static const hipError_t attr = allow_lds(&gateup_kernel<GPC, NTMAX, WAVES>, xs_bytes + kSxBytes + 512);
+  if (attr != hipSuccess) return attr;
   const int chunks = (r.T + 16 * NTMAX - 1) / (16 * NTMAX);
   hipLaunchKernelGGL((gateup_kernel<GPC, NTMAX, WAVES>),
                      dim3(L.ffn / (16 * WAVES), L.E, chunks * h.ksplit),
@@ -235,12 +233,10 @@ template <int GPC, int NTMAX, int WAVES>
 static hipError_t launch_down_nt(const Hidden& h, const LayerArgs& L, const mc_routing& r,
                                  int nsplit, float* partial, size_t part_stride, int xs_bytes,
                                  hipStream_t stream) {
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = allow_lds(&down_kernel<GPC, NTMAX, WAVES>, xs_bytes + kSxBytes + 512);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
+  // set once per instantiation (thread-safe static initialisation); the slab
+  // size of an instantiation is fixed
+  static const hipError_t attr = allow_lds(&down_kernel<GPC, NTMAX, WAVES>, xs_bytes + kSxBytes + 512);
+  if (attr != hipSuccess) return attr;
   const int chunks = (r.T + 16 * NTMAX - 1) / (16 * NTMAX);
   const int rows_per_wg = 32 * WAVES;
   hipLaunchKernelGGL((down_kernel<GPC, NTMAX, WAVES>),

@@ -422,14 +422,13 @@ prefill_kernel(LayerArgs L, const int32_t* __restrict__ offsets, PrefillTables t
 template <int GPC>
 hipError_t launch_prefill_gemm(const LayerArgs& L, const int32_t* offsets, const PrefillTables& tb,
                                const PrefillGemm& g, bool gateup, hipStream_t stream) {
-  static bool attr[2] = {false, false};
-  const void* fn = gateup ? reinterpret_cast<const void*>(&prefill_kernel<GPC, true>)
-                          : reinterpret_cast<const void*>(&prefill_kernel<GPC, false>);
-  if (!attr[gateup]) {
-    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, PfCfg::kLdsBytes);
-    if (e != hipSuccess) return e;
-    attr[gateup] = true;
-  }
+  // set once per kernel (thread-safe static initialisation)
+  static const hipError_t attr_gu = hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_kernel<GPC, true>),
+                                                        hipFuncAttributeMaxDynamicSharedMemorySize, PfCfg::kLdsBytes);
+  static const hipError_t attr_dn = hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_kernel<GPC, false>),
+                                                        hipFuncAttributeMaxDynamicSharedMemorySize, PfCfg::kLdsBytes);
+  if (attr_gu != hipSuccess) return attr_gu;
+  if (attr_dn != hipSuccess) return attr_dn;
   const dim3 grid(tb.mt_max * g.n_tiles * g.nsplit);
   if (gateup)
     hipLaunchKernelGGL((prefill_kernel<GPC, true>), grid, dim3(64 * kPfWaves), PfCfg::kLdsBytes, stream, L,
