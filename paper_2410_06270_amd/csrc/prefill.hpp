@@ -41,7 +41,7 @@ constexpr int kPfFragRows = 32;                    // rows of a fragment (MFMA M
 constexpr int kPfFragBytes = 1024;                 // 32 rows x 16 16-bit values
 constexpr int kPfWaves = 8;
 constexpr int kPfWaveTiles = 2;                    // fragment rows per wave (64 tokens)
-constexpr int kPfWtok = 2;                         // token groups per workgroup
+constexpr int kPfWtok = 1;                         // token groups per workgroup (64-token m-tiles)
 constexpr int kPfSlots = 4;                        // LDS ring: chunks c-1 .. c+2
 
 template <int WTOK>
@@ -60,7 +60,7 @@ struct PfShape {
   static_assert(kTiles * 8 % kPfWaves == 0, "fragments spread evenly over the waves");
   static_assert(kTiles * 4 * 32 * 4 <= kSumBytes, "group sums of a chunk");
   static_assert(kLdsBytes <= kLdsPerCu, "prefill stages fit the LDS of a CU");
-  static_assert(kRowsGateUp == 128, "a gate/up workgroup covers whole groups of h columns");
+  static_assert(kRowsGateUp % 128 == 0, "a gate/up workgroup covers whole groups of h columns");
 };
 using PfCfg = PfShape<kPfWtok>;
 
