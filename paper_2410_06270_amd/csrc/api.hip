@@ -365,14 +365,17 @@ mc_status mc_moe_stack_forward(const uint16_t* x_bf16, int n_layers, const mc_la
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
   const uint16_t* in = x_bf16;
+  // layer 0's input is normalised here; every later layer's input is formed
+  // by the previous layer's combine (same bytes as a separate RMSNorm launch)
+  s = hip_status(mc::launch_rmsnorm(in, r->T, layers[0].d, mc::kRmsNormEps, xn, st),
+                 "mc_moe_stack_forward rmsnorm launch");
+  if (s != MC_OK) return s;
   for (int l = 0; l < n_layers; ++l) {
     uint16_t* out = ((n_layers - 1 - l) % 2 == 0) ? y_bf16 : tmp_bf16;
     const size_t te = (size_t)l * r->T;
-    s = hip_status(mc::launch_rmsnorm(in, r->T, layers[0].d, mc::kRmsNormEps, xn, st),
-                   "mc_moe_stack_forward rmsnorm launch");
-    if (s != MC_OK) return s;
     const mc::RouteArgs ra{logits + te * r->E, important ? important + te : nullptr, delta32, tau};
-    s = hip_status(mc::launch_forward(xn, layer_args(&layers[l]), *r, out, fws, in, st, &ra),
+    s = hip_status(mc::launch_forward(xn, layer_args(&layers[l]), *r, out, fws, in, st, &ra,
+                                      l + 1 < n_layers ? xn : nullptr),
                    "mc_moe_stack_forward forward launch");
     if (s != MC_OK) return s;
     in = out;

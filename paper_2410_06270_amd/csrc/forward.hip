@@ -9,15 +9,9 @@ namespace mc {
 // of w_r * sum over splits s, in order, of partial[s][pos(t, r)][i..i+3]);
 // res is the bf16 residual input (none when null).
 template <int NSPLIT>
-__global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ partial,
-                                                      size_t part_stride,
-                                                      const int32_t* __restrict__ pair_pos,
-                                                      const float* __restrict__ topk_w, int k, int d,
-                                                      int P, const uint16_t* __restrict__ res,
-                                                      uint16_t* __restrict__ y) {
-  const int t = blockIdx.y;
-  const int i = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
-  if (i >= d) return;
+__device__ __forceinline__ f32x4 combine4(const float* __restrict__ partial, size_t part_stride,
+                                          const int32_t* __restrict__ pair_pos, const float* __restrict__ topk_w,
+                                          int k, int d, int P, const uint16_t* __restrict__ res, int t, int i) {
   f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
   if (res) {
     const uint2 rv = *reinterpret_cast<const uint2*>(res + (size_t)t * d + i);
@@ -40,16 +34,33 @@ __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ 
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[c] = fmaf(w, sum[c], acc[c]);
   }
-  uint32_t lo = (uint32_t)float_to_bf16(acc[0]) | ((uint32_t)float_to_bf16(acc[1]) << 16);
-  uint32_t hi = (uint32_t)float_to_bf16(acc[2]) | ((uint32_t)float_to_bf16(acc[3]) << 16);
-  *reinterpret_cast<uint2*>(y + (size_t)t * d + i) = make_uint2(lo, hi);
+  return acc;
+}
+
+__device__ __forceinline__ uint2 bf16x4(const f32x4& a) {
+  return make_uint2((uint32_t)float_to_bf16(a[0]) | ((uint32_t)float_to_bf16(a[1]) << 16),
+                    (uint32_t)float_to_bf16(a[2]) | ((uint32_t)float_to_bf16(a[3]) << 16));
+}
+
+template <int NSPLIT>
+__global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ partial,
+                                                      size_t part_stride,
+                                                      const int32_t* __restrict__ pair_pos,
+                                                      const float* __restrict__ topk_w, int k, int d,
+                                                      int P, const uint16_t* __restrict__ res,
+                                                      uint16_t* __restrict__ y) {
+  const int t = blockIdx.y;
+  const int i = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
+  if (i >= d) return;
+  *reinterpret_cast<uint2*>(y + (size_t)t * d + i) =
+      bf16x4(combine4<NSPLIT>(partial, part_stride, pair_pos, topk_w, k, d, P, res, t, i));
 }
 
 // ---------------------------------------------------------------- rmsnorm --
 // xn[t][i] = bf16(h[t][i] / sqrt(mean_j h[t][j]^2 + eps)): the sum of squares
 // in fp64 in a fixed order (lane partials, wave butterfly, waves in order),
 // the quotient in fp64, rounded once.  One workgroup per token.
-constexpr int kNormThreads = 256;
+constexpr int kNormThreads = 1024;
 
 __global__ void __launch_bounds__(kNormThreads) rmsnorm_kernel(const uint16_t* __restrict__ h, int d,
                                                                double eps, uint16_t* __restrict__ xn) {
@@ -73,6 +84,46 @@ __global__ void __launch_bounds__(kNormThreads) rmsnorm_kernel(const uint16_t* _
   const double r = 1.0 / sqrt(tot / d + eps);
   for (int i = 4 * threadIdx.x; i < d; i += 4 * kNormThreads) {
     const uint2 v = *reinterpret_cast<const uint2*>(h + base + i);
+    const uint32_t lo = (uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.x & 0xffffu) * r) |
+                        ((uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.x >> 16) * r) << 16);
+    const uint32_t hi = (uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.y & 0xffffu) * r) |
+                        ((uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.y >> 16) * r) << 16);
+    *reinterpret_cast<uint2*>(xn + base + i) = make_uint2(lo, hi);
+  }
+}
+
+// The combine of a stack layer that also forms the next layer's input: one
+// workgroup per token writes y[t] as combine_kernel does and xn[t] =
+// RMSNorm(y[t]) as rmsnorm_kernel would from y -- each thread takes the same
+// columns in the same order as there, so the sum of squares, its reduction
+// and every rounding are those of the two separate launches.
+template <int NSPLIT>
+__global__ void __launch_bounds__(kNormThreads) combine_norm_kernel(
+    const float* __restrict__ partial, size_t part_stride, const int32_t* __restrict__ pair_pos,
+    const float* __restrict__ topk_w, int k, int d, int P, const uint16_t* __restrict__ res,
+    uint16_t* __restrict__ y, double eps, uint16_t* __restrict__ xn) {
+  __shared__ double part[kNormThreads / 64];
+  const int t = blockIdx.x;
+  const size_t base = (size_t)t * d;
+  double ss = 0.0;
+  for (int i = 4 * threadIdx.x; i < d; i += 4 * kNormThreads) {
+    const uint2 v = bf16x4(combine4<NSPLIT>(partial, part_stride, pair_pos, topk_w, k, d, P, res, t, i));
+    *reinterpret_cast<uint2*>(y + base + i) = v;
+    const double a = bf16_bits_to_float(v.x & 0xffffu), b = bf16_bits_to_float(v.x >> 16);
+    const double c = bf16_bits_to_float(v.y & 0xffffu), e = bf16_bits_to_float(v.y >> 16);
+    ss += a * a;
+    ss += b * b;
+    ss += c * c;
+    ss += e * e;
+  }
+  for (int off = 1; off < 64; off <<= 1) ss += __shfl_xor(ss, off);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  double tot = 0.0;
+  for (int w = 0; w < kNormThreads / 64; ++w) tot += part[w];
+  const double r = 1.0 / sqrt(tot / d + eps);
+  for (int i = 4 * threadIdx.x; i < d; i += 4 * kNormThreads) {
+    const uint2 v = *reinterpret_cast<const uint2*>(y + base + i);   // this thread's own stores
     const uint32_t lo = (uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.x & 0xffffu) * r) |
                         ((uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.x >> 16) * r) << 16);
     const uint32_t hi = (uint32_t)double_to_bf16_rne(bf16_bits_to_float(v.y & 0xffffu) * r) |
@@ -152,12 +203,17 @@ size_t stack_workspace_bytes(int T, int E, int k, int d, int ffn) {
 
 static hipError_t launch_combine(const float* partial, size_t part_stride, int nsplit,
                                  const mc_routing& r, int d, const uint16_t* res, uint16_t* y,
-                                 hipStream_t stream) {
+                                 uint16_t* xn_next, hipStream_t stream) {
   timing_begin(stream, kSiteCombine);
   const dim3 cgrid((d / 4 + 255) / 256, r.T);
 #define MC_COMBINE(S)                                                                              \
-  hipLaunchKernelGGL(combine_kernel<S>, cgrid, dim3(256), 0, stream, partial, part_stride,         \
-                     r.pair_pos, r.topk_w, r.k, d, r.T * r.k, res, y)
+  if (xn_next)                                                                                     \
+    hipLaunchKernelGGL(combine_norm_kernel<S>, dim3(r.T), dim3(kNormThreads), 0, stream, partial,  \
+                       part_stride, r.pair_pos, r.topk_w, r.k, d, r.T * r.k, res, y, kRmsNormEps,   \
+                       xn_next);                                                                   \
+  else                                                                                             \
+    hipLaunchKernelGGL(combine_kernel<S>, cgrid, dim3(256), 0, stream, partial, part_stride,       \
+                       r.pair_pos, r.topk_w, r.k, d, r.T * r.k, res, y)
   switch (nsplit) {
     case 1: MC_COMBINE(1); break;
     case 2: MC_COMBINE(2); break;
@@ -174,7 +230,8 @@ static hipError_t launch_combine(const float* partial, size_t part_stride, int n
 }
 
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
-                          void* ws, const uint16_t* residual, hipStream_t stream, const RouteArgs* route) {
+                          void* ws, const uint16_t* residual, hipStream_t stream, const RouteArgs* route,
+                          uint16_t* xn_next) {
   const int T = r.T, k = r.k;
   if (route) {
     const hipError_t err = launch_route(route->logits, route->important, route->delta32, route->tau, r, stream);
@@ -186,7 +243,7 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
     int nsplit = 1;
     const hipError_t err = launch_prefill(x, L, r, ws, &partial, &part_stride, &nsplit, stream);
     if (err != hipSuccess) return err;
-    return launch_combine(partial, part_stride, nsplit, r, L.d, residual, y, stream);
+    return launch_combine(partial, part_stride, nsplit, r, L.d, residual, y, xn_next, stream);
   }
   const size_t P = (size_t)T * k;
   Hidden hid;
@@ -218,7 +275,7 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
   else err = launch_down<4>(hid, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
   timing_end(stream, kSiteDown);
   if (err != hipSuccess) return err;
-  return launch_combine(partial, part_stride, nsplit, r, L.d, residual, y, stream);
+  return launch_combine(partial, part_stride, nsplit, r, L.d, residual, y, xn_next, stream);
 }
 
 }  // namespace mc

@@ -51,9 +51,12 @@ struct RouteArgs {
 };
 // residual (may be null): y = bf16(residual + sum_r w_r E_{e_r}(x)).
 // route (may be null): route the batch first (the routing kernels).
+// xn_next (may be null): also write RMSNorm(y) there, the next stack layer's
+// input (the combine forms it; the bytes of a separate rmsnorm launch).
 hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
                           void* ws, const uint16_t* residual, hipStream_t stream,
-                          const RouteArgs* route = nullptr);
+                          const RouteArgs* route = nullptr,
+                          uint16_t* xn_next = nullptr);
 // Stack of layers: xn = RMSNorm(h) (fp64, one bf16 rounding) before each layer.
 constexpr double kRmsNormEps = 1e-5;
 hipError_t launch_rmsnorm(const uint16_t* h, int T, int d, double eps, uint16_t* xn, hipStream_t stream);
