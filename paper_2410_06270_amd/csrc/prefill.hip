@@ -13,7 +13,7 @@ extern template hipError_t launch_prefill_gemm<4>(const LayerArgs&, const int32_
                                                   const PrefillGemm&, bool, hipStream_t);
 
 // One workgroup: per expert e (thread e), fragment rows ceil(M_e/32) and
-// 256-token m-tiles ceil(M_e/256), exclusive scans, and the tables.
+// m-tiles of PfCfg::kTokens tokens, exclusive scans, and the tables.
 // Counts outside [0, P] are taken as 0, and tables that would not fit their
 // capacity are left empty (no m-tiles), so inconsistent routing cannot make
 // any later access leave its buffer.
