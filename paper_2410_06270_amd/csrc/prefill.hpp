@@ -331,8 +331,16 @@ prefill_kernel(LayerArgs L, const int32_t* __restrict__ offsets, PrefillTables t
 
   int row[2];
   PfStream sp[2];
+  // gate/up: the last row tile may cover only the first 128 of its 256 ffn
+  // rows (ffn is a multiple of 128); its surplus waves read the tile's first
+  // rows again (in bounds) and write nothing.
+  bool rows_valid = true;
   if (GATEUP) {
     row[0] = row[1] = nt * S::kRowsGateUp + 32 * rg;
+    if (row[0] + 32 > L.ffn) {
+      rows_valid = false;
+      row[0] = row[1] = nt * S::kRowsGateUp + 32 * (rg & 3);
+    }
     sp[0] = pf_stream(L, e, 0, row[0], g.K, bits, lane);
     sp[1] = pf_stream(L, e, 1, row[1], g.K, bits, lane);
   } else {
@@ -373,7 +381,7 @@ prefill_kernel(LayerArgs L, const int32_t* __restrict__ offsets, PrefillTables t
 #pragma unroll
     for (int t = 0; t < kPfWaveTiles; ++t) {
       const int f = f0 + 2 * tg + t;
-      if (active && 2 * tg + t < nmt) {
+      if (active && rows_valid && 2 * tg + t < nmt) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int m = 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
@@ -389,9 +397,10 @@ prefill_kernel(LayerArgs L, const int32_t* __restrict__ offsets, PrefillTables t
     __syncthreads();
     const int gpw = L.G / 32;                       // row groups (32 columns each) per group
     const int ngw = S::kRowsGateUp / L.G;           // groups in this workgroup
+    const int ng_valid = (L.ffn - nt * S::kRowsGateUp) / L.G;   // groups inside ffn
     for (int idx = threadIdx.x; idx < kPfWtok * 64 * ngw; idx += blockDim.x) {
       const int q = idx % ngw, r = (idx / ngw) % 64, tg2 = idx / (ngw * 64);
-      if (2 * tg2 + r / 32 >= nmt) continue;
+      if (2 * tg2 + r / 32 >= nmt || q >= ng_valid) continue;
       float v = 0.0f;
       for (int k = 0; k < gpw; ++k) v += part[(tg2 * S::kWrow + q * gpw + k) * 64 + r];
       const int f = f0 + 2 * tg2 + r / 32;

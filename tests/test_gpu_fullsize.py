@@ -2,7 +2,9 @@
 ffn=14336, E=8, widths [3,3,3,2,2,2,2,3], G=128) in the launch configuration
 the benchmark times.  Packed words are compared in full for one expert; the
 layer output is compared on sampled tokens x rows, which the oracle computes
-one by one from its own quantization of the same fp32 weights."""
+one by one from its own quantization of the same fp32 weights: every token
+and row for decode batches, and for prefill one token from every 64-token
+m-tile of every expert over rows covering every 512-row tile."""
 import numpy as np
 import pytest
 
@@ -80,16 +82,34 @@ def test_mixtral_decode_sampled(mc, mixtral, T):
     ref = oracle.route(lg, imp, k, tau)
     np.testing.assert_array_equal(r.topk_idx.cpu().numpy(), ref["topk_idx"])
     np.testing.assert_array_equal(r.kept.cpu().numpy(), ref["kept"])
-    # sample: a pruned token, a protected token and the first/last tokens
-    toks = {0, T - 1}
-    pr = np.nonzero(ref["kept"][:, 1] == 0)[0]
-    if len(pr):
-        toks.add(int(pr[0]))
-    pt = np.nonzero(imp)[0]
-    if len(pt):
-        toks.add(int(pt[0]))
-    toks = sorted(toks)
-    rows = sorted(set(np.random.default_rng(T).choice(d, 48, replace=False).tolist()) | {0, d - 1})
+    if T <= 64:
+        # decode: every token, every row
+        toks, rows = list(range(T)), None
+    else:
+        # prefill: the first and last tokens, a pruned and a protected token,
+        # and one token from every 64-token m-tile of every expert (at a
+        # position that moves through the tile), over rows that cover every
+        # 512-row tile of the down GEMM (its first and last rows included)
+        toks = {0, T - 1}
+        pr = np.nonzero(ref["kept"][:, 1] == 0)[0]
+        if len(pr):
+            toks.add(int(pr[0]))
+        pt = np.nonzero(imp)[0]
+        if len(pt):
+            toks.add(int(pt[0]))
+        offs, pts = ref["offsets"], ref["pair_token"]
+        for e in range(E):
+            n = int(offs[e + 1] - offs[e])
+            for j in range((n + 63) // 64):
+                width = min(64, n - 64 * j)
+                toks.add(int(pts[offs[e] + 64 * j + (37 * j + 5 * e) % width]))
+        toks = sorted(toks)
+        g = np.random.default_rng(T)
+        rows = {0, d - 1}
+        for t0 in range(0, d, 512):
+            rows |= {t0, t0 + 511}
+            rows |= set((t0 + g.choice(512, 24, replace=False)).tolist())
+        rows = sorted(rows)
     need = sorted({int(ref["topk_idx"][t, rr]) for t in toks for rr in range(k) if ref["kept"][t, rr]})
     logical = [None] * E
     for e in need:
@@ -97,12 +117,14 @@ def test_mixtral_decode_sampled(mc, mixtral, T):
             _LOGICAL[e] = [oracle.quantize(mats[e][m], bits[e], G) for m in range(3)]
         logical[e] = _LOGICAL[e]
     y_ref = oracle.moe_forward(x, ref, logical, G, rows=rows, tokens=toks)
-    g = oracle.bf16_to_float64(y.cpu().numpy().view(np.uint16)[np.ix_(toks, rows)])
+    yb = y.cpu().numpy().view(np.uint16)[toks]
+    g = oracle.bf16_to_float64(yb if rows is None else yb[:, rows])
     rb = oracle.bf16_to_float64(oracle.bf16_round_array(y_ref))
     mae = np.abs(g - rb).mean()
     rms = np.sqrt((y_ref ** 2).mean())
     maxrel = (np.abs(g - y_ref) / np.maximum(np.abs(y_ref), rms)).max()
-    print("T=%d tokens %s MAE %.3e MaxRel %.3e rms %.3f" % (T, toks, mae, maxrel, rms))
+    print("T=%d: %d tokens x %s rows, MAE %.3e MaxRel %.3e rms %.3f"
+          % (T, len(toks), d if rows is None else len(rows), mae, maxrel, rms))
     assert mae <= 1e-3 and maxrel <= 2e-2, (mae, maxrel)
     # the whole output is finite and has the reference's scale
     yall = oracle.bf16_to_float64(y.cpu().numpy().view(np.uint16))

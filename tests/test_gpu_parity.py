@@ -255,6 +255,8 @@ def test_forward_max_tokens_sampled(mc, tiny):
     (1, 4, 384, 256, 257, None),      # d not a multiple of the 256-row down tile
     (1, 4, 256, 512, 600, 1),         # one expert takes every token: 600 + ~rest, 3 m-tiles
     (4, 16, 2048, 1024, 300, None),   # G = 64, 16 experts, top-8, ragged experts
+    (1, 4, 256, 384, 300, None),      # ffn % 256 = 128: the last gate/up row tile is half full
+    (1, 4, 256, 128, 300, None),      # ffn = 128: one half-full gate/up row tile
 ])
 def test_forward_prefill_shapes(mc, cid, E, d, ffn, T, hot):
     """Batches above 64 tokens go through the grouped GEMMs: partial 256-token
@@ -276,6 +278,22 @@ def test_forward_prefill_shapes(mc, cid, E, d, ffn, T, hot):
     y_ref = oracle.moe_forward(x, ref, logical, G)
     mae, maxrel = check_tol(y, y_ref)
     print("prefill cid=%d E=%d d=%d ffn=%d T=%d MAE %.3e MaxRel %.3e" % (cid, E, d, ffn, T, mae, maxrel))
+
+
+@pytest.mark.parametrize("ffn", [128, 384])
+@pytest.mark.parametrize("T", [5, 33])
+def test_forward_narrow_ffn_decode(mc, ffn, T):
+    """Decode batches with ffn not a multiple of 256 (one or three 128-row
+    gate/up blocks)."""
+    mats, bits, G, logical = layer_case(1, ffn=ffn)
+    L = pack_gpu(mc, mats, bits, G)
+    x = synthetic.activations(1, T)
+    lg = synthetic.logits(1, T)
+    imp = synthetic.important_mask(1, T)
+    y, _ = forward_gpu(mc, L, x, lg, imp, 2, 0.3)
+    y_ref = oracle.moe_forward(x, oracle.route(lg, imp, 2, 0.3), logical, G)
+    mae, _ = check_tol(y, y_ref)
+    assert mae < 2e-4, mae
 
 
 def test_forward_skewed_and_dense(mc, tiny):
