@@ -66,8 +66,8 @@ def parse():
 
 # Sources of the decode gate/up and down kernels: the stored HBM counter
 # figures are reported only while these files are unchanged.
-DECODE_SOURCES = ("forward_engine.hpp", "fwd_kernels.hpp", "mc_device.hpp", "gateup_g32.hip", "gateup_g64.hip",
-                  "gateup_g128.hip", "down_g32.hip", "down_g64.hip", "down_g128.hip")
+DECODE_SOURCES = ("forward_engine.hpp", "decode.hpp", "mc_device.hpp", "decode_g32.hip", "decode_g64.hip",
+                  "decode_g128.hip")
 
 
 def source_hash() -> str:

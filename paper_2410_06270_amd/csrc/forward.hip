@@ -1,17 +1,20 @@
 // forward.hip -- routing-weighted combination and the forward launcher
-// (gate/up and down kernels: fwd_kernels.hpp, one file per group size).
-#include "forward_engine.hpp"
+// (decode GEMVs: decode.hpp, prefill GEMMs: prefill.hpp, one file per group
+// size each).
+#include "decode.hpp"
 
 namespace mc {
 
 // ---------------------------------------------------------------- combine --
 // y[t][i..i+3] = bf16(res[t][i..i+3] + sum over kept ranks r, in rank order,
 // of w_r * sum over splits s, in order, of partial[s][pos(t, r)][i..i+3]);
-// res is the bf16 residual input (none when null).
+// res is the bf16 residual input (none when null).  NSPLIT = 0: the number
+// of splits is the run-time `nsplit` (more than 8).
 template <int NSPLIT>
 __device__ __forceinline__ f32x4 combine4(const float* __restrict__ partial, size_t part_stride,
                                           const int32_t* __restrict__ pair_pos, const float* __restrict__ topk_w,
-                                          int k, int d, int P, const uint16_t* __restrict__ res, int t, int i) {
+                                          int k, int d, int P, const uint16_t* __restrict__ res, int t, int i,
+                                          int nsplit = NSPLIT) {
   f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
   if (res) {
     const uint2 rv = *reinterpret_cast<const uint2*>(res + (size_t)t * d + i);
@@ -24,13 +27,20 @@ __device__ __forceinline__ f32x4 combine4(const float* __restrict__ partial, siz
     const int pos = pair_pos[(size_t)t * k + r];
     if (pos < 0 || pos >= P) continue;
     const float w = topk_w[(size_t)t * k + r];
-    f32x4 v[NSPLIT];
+    f32x4 sum;
+    if constexpr (NSPLIT == 0) {
+      sum = *reinterpret_cast<const f32x4*>(partial + (size_t)pos * d + i);
+      for (int s = 1; s < nsplit; ++s)
+        sum += *reinterpret_cast<const f32x4*>(partial + s * part_stride + (size_t)pos * d + i);
+    } else {
+      f32x4 v[NSPLIT];
 #pragma unroll
-    for (int s = 0; s < NSPLIT; ++s)
-      v[s] = *reinterpret_cast<const f32x4*>(partial + s * part_stride + (size_t)pos * d + i);
-    f32x4 sum = v[0];
+      for (int s = 0; s < NSPLIT; ++s)
+        v[s] = *reinterpret_cast<const f32x4*>(partial + s * part_stride + (size_t)pos * d + i);
+      sum = v[0];
 #pragma unroll
-    for (int s = 1; s < NSPLIT; ++s) sum += v[s];
+      for (int s = 1; s < NSPLIT; ++s) sum += v[s];
+    }
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[c] = fmaf(w, sum[c], acc[c]);
   }
@@ -48,12 +58,12 @@ __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ 
                                                       const int32_t* __restrict__ pair_pos,
                                                       const float* __restrict__ topk_w, int k, int d,
                                                       int P, const uint16_t* __restrict__ res,
-                                                      uint16_t* __restrict__ y) {
+                                                      uint16_t* __restrict__ y, int nsplit) {
   const int t = blockIdx.y;
   const int i = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
   if (i >= d) return;
   *reinterpret_cast<uint2*>(y + (size_t)t * d + i) =
-      bf16x4(combine4<NSPLIT>(partial, part_stride, pair_pos, topk_w, k, d, P, res, t, i));
+      bf16x4(combine4<NSPLIT>(partial, part_stride, pair_pos, topk_w, k, d, P, res, t, i, nsplit));
 }
 
 // ---------------------------------------------------------------- rmsnorm --
@@ -101,13 +111,13 @@ template <int NSPLIT>
 __global__ void __launch_bounds__(kNormThreads) combine_norm_kernel(
     const float* __restrict__ partial, size_t part_stride, const int32_t* __restrict__ pair_pos,
     const float* __restrict__ topk_w, int k, int d, int P, const uint16_t* __restrict__ res,
-    uint16_t* __restrict__ y, double eps, uint16_t* __restrict__ xn) {
+    uint16_t* __restrict__ y, double eps, uint16_t* __restrict__ xn, int nsplit) {
   __shared__ double part[kNormThreads / 64];
   const int t = blockIdx.x;
   const size_t base = (size_t)t * d;
   double ss = 0.0;
   for (int i = 4 * threadIdx.x; i < d; i += 4 * kNormThreads) {
-    const uint2 v = bf16x4(combine4<NSPLIT>(partial, part_stride, pair_pos, topk_w, k, d, P, res, t, i));
+    const uint2 v = bf16x4(combine4<NSPLIT>(partial, part_stride, pair_pos, topk_w, k, d, P, res, t, i, nsplit));
     *reinterpret_cast<uint2*>(y + base + i) = v;
     const double a = bf16_bits_to_float(v.x & 0xffffu), b = bf16_bits_to_float(v.x >> 16);
     const double c = bf16_bits_to_float(v.y & 0xffffu), e = bf16_bits_to_float(v.y >> 16);
@@ -142,45 +152,41 @@ hipError_t launch_rmsnorm(const uint16_t* h, int T, int d, double eps, uint16_t*
 
 // --------------------------------------------------------------- launchers --
 
-// Split of the down projection's reduction so that small batches still give
-// enough workgroups: about 1024 while the batch has fewer than 24 kept-pair
-// slots, 512 beyond, where the fp32 partials (splits x T*k x d x 4 bytes,
-// written here and read by the combine) cost more than the parallelism gains
-// (8-expert layer: down 47.9 -> 45.1 us at T = 32, 2.6 to 3.7 us less from
-// T = 12 to 64, 1.6 us more at T = 8).  Active experts are estimated as for
-// the gate/up split.  The prefill GEMMs choose their own split.
-int forward_nsplit(int T, int E, int k, int d, int ffn) {
-  if (T > kDecodeMaxT) return prefill_layout(T, E, k, d, ffn).nsplit;
-  const int tiles = (d + 255) / 256;
-  int active = (T * k) < E ? (T * k) : E;
-  if (E > 8) active = (active + 1) / 2;
-  const int target = T * k >= 24 ? 512 : 1024;
-  int s = (target + tiles * active - 1) / (tiles * active);
-  const int maxs = (ffn / kTileCols) / 4;
-  if (s > maxs) s = maxs;
-  if (s > kMaxNsplit) s = kMaxNsplit;
-  if (s < 1) s = 1;
-  return s;
+// Splits of the decode GEMVs' reductions: as few as let one item's
+// activations (16 rows of 128-column chunks) fit the LDS slab -- one for the
+// gate/up reduction over d up to 4352, four for Mixtral's ffn = 14336 (28
+// chunks each).  The slab capacity does not depend on the group size.
+static_assert(decode_slab_chunks(1) == decode_slab_chunks(4), "slab capacity independent of G");
+static int decode_splits(int K, int* c_per) {
+  const int nt = K / kTileCols, cap = decode_slab_chunks(1);
+  const int S = (nt + cap - 1) / cap;
+  if (c_per) *c_per = (nt + S - 1) / S;
+  return S;
 }
 
-// Split of the gate/up reduction (over d) when the active experts give fewer
-// than two workgroups per CU (batches of a few tokens); each split covers at
-// least two 128-column chunks.  With many experts the estimate of the active
-// ones is half of min(T*k, E): routers are skewed (on the OLMoE-shaped layer
-// 16 tokens x top-8 touch about 23 of 64 experts), and sizing for all of them
-// left the gate/up launch at under one workgroup per CU (measured there: gate/up
-// 25.9 -> 17.7 us, step 53.0 -> 49.0 us at T = 16).
+// Splits of the down reduction: the decode GEMV's, or the prefill GEMM's.
+int forward_nsplit(int T, int E, int k, int d, int ffn) {
+  if (T > kDecodeMaxT) return prefill_layout(T, E, k, d, ffn).nsplit;
+  return decode_splits(ffn, nullptr);
+}
+
+// Splits of the decode gate/up reduction over d (1 up to d = 4352).
 int forward_ksplit(int T, int E, int k, int d, int ffn) {
-  if (T > 16) return 1;
-  int active = (T * k) < E ? (T * k) : E;
-  if (E > 8) active = (active + 1) / 2;
-  const int wgs = (ffn / (16 * kWavesPerWg)) * active;
-  int s = (512 + wgs - 1) / wgs;
-  const int maxs = (d / kTileCols) / 2;
-  if (s > maxs) s = maxs;
-  if (s > kMaxKsplit) s = kMaxKsplit;
-  if (s < 1) s = 1;
-  return s;
+  (void)T; (void)E; (void)k; (void)ffn;
+  return decode_splits(d, nullptr);
+}
+
+// Compute units of the current device (one decode workgroup each).
+static int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
 }
 
 // Workspace: h (fp16) | gate/up partials (when split) | down partials, each
@@ -210,10 +216,10 @@ static hipError_t launch_combine(const float* partial, size_t part_stride, int n
   if (xn_next)                                                                                     \
     hipLaunchKernelGGL(combine_norm_kernel<S>, dim3(r.T), dim3(kNormThreads), 0, stream, partial,  \
                        part_stride, r.pair_pos, r.topk_w, r.k, d, r.T * r.k, res, y, kRmsNormEps,   \
-                       xn_next);                                                                   \
+                       xn_next, nsplit);                                                           \
   else                                                                                             \
     hipLaunchKernelGGL(combine_kernel<S>, cgrid, dim3(256), 0, stream, partial, part_stride,       \
-                       r.pair_pos, r.topk_w, r.k, d, r.T * r.k, res, y)
+                       r.pair_pos, r.topk_w, r.k, d, r.T * r.k, res, y, nsplit)
   switch (nsplit) {
     case 1: MC_COMBINE(1); break;
     case 2: MC_COMBINE(2); break;
@@ -222,7 +228,8 @@ static hipError_t launch_combine(const float* partial, size_t part_stride, int n
     case 5: MC_COMBINE(5); break;
     case 6: MC_COMBINE(6); break;
     case 7: MC_COMBINE(7); break;
-    default: MC_COMBINE(8); break;
+    case 8: MC_COMBINE(8); break;
+    default: MC_COMBINE(0); break;
   }
 #undef MC_COMBINE
   timing_end(stream, kSiteCombine);
@@ -246,33 +253,54 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
     return launch_combine(partial, part_stride, nsplit, r, L.d, residual, y, xn_next, stream);
   }
   const size_t P = (size_t)T * k;
-  Hidden hid;
-  hid.P = (int)P;
-  hid.T = T;
-  hid.h = static_cast<uint16_t*>(ws);
+  DecodeArgs a;
+  a.x = x;
+  a.counts = r.counts;
+  a.offsets = r.offsets;
+  a.pair_token = r.pair_token;
+  a.T = T;
+  a.P = (int)P;
+  a.nwg = device_cus();
+  int c_gu = 0, c_dn = 0;
+  const int s_gu = decode_splits(L.d, &c_gu);
+  const int nsplit = decode_splits(L.ffn, &c_dn);
+  uint16_t* h = static_cast<uint16_t*>(ws);
   char* p = static_cast<char*>(ws) + round256(P * L.ffn * sizeof(uint16_t));
-  hid.ksplit = forward_ksplit(T, r.E, k, L.d, L.ffn);
-  hid.gu_part = reinterpret_cast<float*>(p);
-  if (hid.ksplit > 1) p += round256((size_t)hid.ksplit * 2 * P * L.ffn * sizeof(float));
+  float* gu_part = reinterpret_cast<float*>(p);
+  if (s_gu > 1) p += round256((size_t)s_gu * 2 * P * L.ffn * sizeof(float));
   float* partial = reinterpret_cast<float*>(p);
   const size_t part_stride = P * L.d;
-  const int nsplit = forward_nsplit(T, r.E, k, L.d, L.ffn);
-  // A workgroup holds at most min(T, 16*ntmax) of an expert's tokens; an
-  // expert with more gets a workgroup per 32 of them (measured faster at 48
-  // and 64 tokens than one workgroup of up to 64 at half the occupancy).
-  const int ntmax = T <= 16 ? 1 : 2;
-  const int xs_bytes = kXsBytes;
+
+  a.h = nullptr;
+  a.gu_in = nullptr;
+  a.h_out = h;
+  a.gu_out = gu_part;
+  a.partial = nullptr;
+  a.part_stride = 0;
+  a.S = s_gu;
+  a.c_per = c_gu;
+  a.gu_split = 1;
   hipError_t err;
   timing_begin(stream, kSiteGateUp);
-  if (L.G == 128) err = launch_gateup<1>(x, L, r, hid, ntmax, xs_bytes, stream);
-  else if (L.G == 64) err = launch_gateup<2>(x, L, r, hid, ntmax, xs_bytes, stream);
-  else err = launch_gateup<4>(x, L, r, hid, ntmax, xs_bytes, stream);
+  if (L.G == 128) err = launch_decode<1, true>(L, a, stream);
+  else if (L.G == 64) err = launch_decode<2, true>(L, a, stream);
+  else err = launch_decode<4, true>(L, a, stream);
   timing_end(stream, kSiteGateUp);
   if (err != hipSuccess) return err;
+
+  a.h = h;
+  a.gu_in = gu_part;
+  a.h_out = nullptr;
+  a.gu_out = nullptr;
+  a.partial = partial;
+  a.part_stride = part_stride;
+  a.S = nsplit;
+  a.c_per = c_dn;
+  a.gu_split = s_gu;
   timing_begin(stream, kSiteDown);
-  if (L.G == 128) err = launch_down<1>(hid, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
-  else if (L.G == 64) err = launch_down<2>(hid, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
-  else err = launch_down<4>(hid, L, r, nsplit, partial, part_stride, ntmax, xs_bytes, stream);
+  if (L.G == 128) err = launch_decode<1, false>(L, a, stream);
+  else if (L.G == 64) err = launch_decode<2, false>(L, a, stream);
+  else err = launch_decode<4, false>(L, a, stream);
   timing_end(stream, kSiteDown);
   if (err != hipSuccess) return err;
   return launch_combine(partial, part_stride, nsplit, r, L.d, residual, y, xn_next, stream);
