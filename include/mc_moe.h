@@ -238,6 +238,21 @@ mc_status mc_moe_forward(const uint16_t *x_bf16, const mc_routing *r,
                          const mc_layer *L, uint16_t *y_bf16, void *workspace,
                          size_t ws_bytes, void *stream);
 
+/* mc_moe_forward for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same kernels and results, with the workspace taken from a device
+ * array the library holds on every GPU it runs on (MC_NOALLOC_SCRATCH_BYTES,
+ * kept until the process ends).  Nothing is allocated by the call.  The
+ * array is shared by all such calls on a GPU and keeps the last call's
+ * contents (the forward writes every workspace byte it reads, nothing needs
+ * clearing): calls that overlap on one GPU (other streams, other threads)
+ * race and must be serialised by the caller.  Errors: as mc_moe_forward;
+ * MC_ENOSPACE when mc_forward_workspace(T, ...) exceeds the array (decode
+ * batches of up to 64 tokens of the Mixtral-shaped layer fit). */
+#define MC_NOALLOC_SCRATCH_BYTES (32u << 20)
+mc_status mc_moe_forward_noalloc(const uint16_t *x_bf16, const mc_routing *r,
+                                 const mc_layer *L, uint16_t *y_bf16, void *stream);
+
 /* mc_route_and_prune followed by mc_moe_forward in one call (the routing
  * kernels, then the expert kernels, on `stream`), with the same results:
  * the routing buffers of r as mc_route_and_prune writes them, y as

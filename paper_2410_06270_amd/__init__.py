@@ -22,6 +22,7 @@ from ._binding import (  # noqa: F401
     lib_path,
     load,
     moe_forward,
+    moe_forward_noalloc,
     odp_threshold,
     pack,
     pack_sizes,

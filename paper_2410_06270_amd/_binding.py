@@ -85,6 +85,8 @@ def load():
         lib.mc_moe_forward.restype = st
         lib.mc_moe_forward.argtypes = [P, ctypes.POINTER(_Routing), ctypes.POINTER(_Layer), P, P,
                                        S, P]
+        lib.mc_moe_forward_noalloc.restype = st
+        lib.mc_moe_forward_noalloc.argtypes = [P, ctypes.POINTER(_Routing), ctypes.POINTER(_Layer), P, P]
         lib.mc_moe_route_forward.restype = st
         lib.mc_moe_route_forward.argtypes = [P, P, P, ctypes.c_float, ctypes.POINTER(_Routing),
                                              ctypes.POINTER(_Layer), P, P, S, P]
@@ -265,6 +267,13 @@ def moe_forward(x, routing: Routing, layer: PackedLayer, y, workspace, stream=No
     _check(load().mc_moe_forward(_ptr(x), ctypes.byref(routing.desc), ctypes.byref(layer.desc),
                                  _ptr(y), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                  _stream(stream)))
+
+
+def moe_forward_noalloc(x, routing: Routing, layer: PackedLayer, y, stream=None):
+    """moe_forward with the library's own device workspace (no allocation)."""
+    assert x.is_contiguous() and y.is_contiguous() and x.element_size() == 2
+    _check(load().mc_moe_forward_noalloc(_ptr(x), ctypes.byref(routing.desc), ctypes.byref(layer.desc),
+                                         _ptr(y), _stream(stream)))
 
 
 def route_forward(x, logits, important, threshold: float, routing: Routing, layer: PackedLayer, y, workspace,

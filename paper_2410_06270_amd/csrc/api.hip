@@ -5,9 +5,16 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "mc_internal.hpp"
+
+// Workspace of mc_moe_forward_noalloc: a file-scope device array, one copy
+// on every GPU the library runs on, held until the process ends.  Host code
+// never uses the name itself as an address (it is a host-side stand-in): the
+// device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[MC_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -75,6 +82,29 @@ mc::LayerArgs layer_args(const mc_layer* L) {
   for (int e = L->E; e < MC_MAX_EXPERTS; ++e) a.cum_bits[e + 1] = a.cum_bits[e];
   for (int i = 0; i < MC_MAX_EXPERTS / 32; ++i) a.sign_mask[i] = 0u;
   return a;
+}
+
+// This device's address of `scratch`, looked up on the first call made with
+// the device current and kept per device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+mc_status scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(MC_EUNSUPPORTED, "device %d above %d", dev, kMaxDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(MC_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MC_OK;
 }
 
 mc_status check_routing(const mc_routing* r) {
@@ -292,6 +322,29 @@ mc_status mc_moe_forward(const uint16_t* x_bf16, const mc_routing* r, const mc_l
   return hip_status(mc::launch_forward(x_bf16, a, *r, y_bf16, workspace, nullptr,
                                        static_cast<hipStream_t>(stream)),
                     "mc_moe_forward launch");
+}
+
+mc_status mc_moe_forward_noalloc(const uint16_t* x_bf16, const mc_routing* r, const mc_layer* L,
+                                 uint16_t* y_bf16, void* stream) {
+  mc_status s = check_routing(r);
+  if (s != MC_OK) return s;
+  s = check_layer(L, true);
+  if (s != MC_OK) return s;
+  if (r->E != L->E) return fail(MC_EINVAL, "routing has E=%d, layer has E=%d", r->E, L->E);
+  if (!x_bf16 || !y_bf16) return fail(MC_EINVAL, "x or y is NULL");
+  const size_t need = mc::forward_workspace_bytes(r->T, r->E, r->k, L->d, L->ffn);
+  if (need > (size_t)MC_NOALLOC_SCRATCH_BYTES)
+    return fail(MC_ENOSPACE,
+                "T=%d needs %zu bytes of workspace; mc_moe_forward_noalloc holds %zu (use mc_moe_forward "
+                "with a caller workspace)",
+                r->T, need, (size_t)MC_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  s = scratch_address(&ws);
+  if (s != MC_OK) return s;
+  (void)hipGetLastError();
+  return hip_status(mc::launch_forward(x_bf16, layer_args(L), *r, y_bf16, ws, nullptr,
+                                       static_cast<hipStream_t>(stream)),
+                    "mc_moe_forward_noalloc launch");
 }
 
 mc_status mc_moe_route_forward(const uint16_t* x_bf16, const float* logits, const uint8_t* important,
