@@ -150,8 +150,7 @@ __device__ __forceinline__ bool piece_in(const DecodeArgs& a, const DecLane& x, 
   p.u1 = u1 < R ? u1 : R;
   p.s = s;
   p.C = C;
-  p.pbase = eb + kDecTok * j;
-  p.nt = (ec - kDecTok * j) < kDecTok ? (ec - kDecTok * j) : kDecTok;
+  pair_block(eb, ec, j, kDecTok, p.pbase, p.nt);
   p.next = ib + (uint32_t)C * R;
   return true;
 }

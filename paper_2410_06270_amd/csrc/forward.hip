@@ -24,8 +24,8 @@ __device__ __forceinline__ f32x4 combine4(const float* __restrict__ partial, siz
     acc[3] = bf16_bits_to_float(rv.y >> 16);
   }
   for (int r = 0; r < k; ++r) {
-    const int pos = pair_pos[(size_t)t * k + r];
-    if (pos < 0 || pos >= P) continue;
+    const int pos = checked_pos(pair_pos[(size_t)t * k + r], P);
+    if (pos < 0) continue;
     const float w = topk_w[(size_t)t * k + r];
     f32x4 sum;
     if constexpr (NSPLIT == 0) {

@@ -228,11 +228,18 @@ __device__ __forceinline__ size_t layer_sz_offset(const LayerArgs& L, int e, int
   return (3 * (size_t)e + m) * ((size_t)L.d * (size_t)L.ffn / L.G);
 }
 
+// ------------------------------------------------ routing-derived indices --
+// Every index the forward kernels derive from the routing buffers goes
+// through these helpers, so that inconsistent routing (a caller's garbage,
+// or buffers a routing call never filled) gives wrong values but never an
+// access outside a buffer.  They are host-callable too: a CPU audit feeds
+// them garbage and checks every derived index against its buffer.
+
 // Kept-pair range [begin, begin + count) of expert e from the routing counts
 // and offsets, or an empty range when they are inconsistent with P = T*k
 // kept-pair slots, so that no index derived from them leaves its buffer.
-__device__ __forceinline__ void expert_range(const int32_t* counts, const int32_t* offsets, int e, int P,
-                                             int& begin, int& count) {
+__host__ __device__ __forceinline__ void expert_range(const int32_t* counts, const int32_t* offsets, int e, int P,
+                                                      int& begin, int& count) {
   int c = counts[e], b = offsets[e];
   if (c < 0 || b < 0 || c > P || b > P - c) c = b = 0;
   begin = b;
@@ -240,8 +247,8 @@ __device__ __forceinline__ void expert_range(const int32_t* counts, const int32_
 }
 
 // The same range from the offsets alone (count = offsets[e+1] - offsets[e]).
-__device__ __forceinline__ void expert_range_offsets(const int32_t* offsets, int e, int P, int& begin,
-                                                     int& count) {
+__host__ __device__ __forceinline__ void expert_range_offsets(const int32_t* offsets, int e, int P, int& begin,
+                                                              int& count) {
   int b = offsets[e], c = offsets[e + 1] - b;
   if (c < 0 || b < 0 || c > P || b > P - c) c = b = 0;
   begin = b;
@@ -249,6 +256,20 @@ __device__ __forceinline__ void expert_range_offsets(const int32_t* offsets, int
 }
 
 // A token index from the routing lists, clamped into [0, T).
-__device__ __forceinline__ int clamp_token(int t, int T) { return t < 0 ? 0 : (t >= T ? T - 1 : t); }
+__host__ __device__ __forceinline__ int clamp_token(int t, int T) { return t < 0 ? 0 : (t >= T ? T - 1 : t); }
+
+// Pairs [pbase, pbase + nt) of block j (blocks of `block` pairs) of an expert
+// whose kept pairs are [begin, begin + count): nt <= 0 when the block is empty.
+__host__ __device__ __forceinline__ void pair_block(int begin, int count, int j, int block, int& pbase, int& nt) {
+  pbase = begin + block * j;
+  nt = (count - block * j) < block ? (count - block * j) : block;
+}
+
+// A kept-pair position of the per-token table (pair_pos), or -1 when it is
+// outside [0, P) (the combine then skips that rank).
+__host__ __device__ __forceinline__ int checked_pos(int pos, int P) { return (pos < 0 || pos >= P) ? -1 : pos; }
+
+// An expert's count as the prefill set-up takes it: counts outside [0, P] are 0.
+__host__ __device__ __forceinline__ int checked_count(int c, int P) { return (c < 0 || c > P) ? 0 : c; }
 
 }  // namespace mc

@@ -21,8 +21,7 @@ __global__ void __launch_bounds__(256) prefill_setup_kernel(const int32_t* __res
                                                             PrefillTables tb) {
   __shared__ int snf[256], snm[256];
   const int t = threadIdx.x;
-  int c = t < E ? counts[t] : 0;
-  if (c < 0 || c > tb.P) c = 0;
+  const int c = t < E ? checked_count(counts[t], tb.P) : 0;
   const int nf = (c + kPfFragRows - 1) / kPfFragRows;
   const int nm = (c + PfCfg::kTokens - 1) / PfCfg::kTokens;
   snf[t] = nf;
