@@ -28,7 +28,13 @@ __host__ __device__ constexpr int prefetch_depth(int ntb, int gpc) {
   return (ntb >= 3 || gpc >= 4) ? 2 : 4;
 }
 
-__device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
+// silu(a) = a / (1 + e^-a) from the hardware base-2 exponential and
+// reciprocal (each within about 1 ulp): a few ulp of fp32, far below the fp16
+// rounding that follows it.  Large |a| saturate correctly (e^-a = inf gives
+// -0, e^-a = 0 gives a).
+__device__ __forceinline__ float silu(float a) {
+  return a * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-a * 1.4426950408889634f));
+}
 
 // Operand format of the activations: bf16 (x) or fp16 (h).  Codes of b bits
 // sit in the top b bits of the mantissa of 1.0 (bit kPos<b> upwards).

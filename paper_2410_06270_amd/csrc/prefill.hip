@@ -157,7 +157,7 @@ hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routin
   gu.a = xt;
   gu.asum = xsum;
   gu.K = L.d;
-  gu.n_tiles = (L.ffn + PfCfg::kRowsGateUp - 1) / PfCfg::kRowsGateUp;   // ffn % 256 may be 128
+  gu.n_tiles = L.ffn / PfCfg::kRowsGateUp;
   gu.c_per_split = L.d / kTileCols;
   gu.nsplit = 1;
   gu.h = ht;

@@ -23,11 +23,13 @@
 // formed while staging.  Rows of each expert start at a fragment boundary;
 // padding rows are zero.
 //
-// Workgroup: 8 waves (two per SIMD), WTOK token groups x (8/WTOK) row groups;
-// a wave computes 64 tokens x 2 streams of 32 weight rows (gate/up: the same
-// 32 ffn rows of gate and of up; down: 64 consecutive d rows), keeping the
-// group accumulators and the running fp32 totals in registers.  The
-// reduction runs in 128-column chunks, double-buffered in LDS.
+// Workgroup: 8 waves (two per SIMD) on one m-tile of 128 tokens (four
+// fragment rows); each wave computes all 128 tokens against one stream of 32
+// weight rows (gate/up: waves 2r and 2r+1 take the same 32 ffn rows of gate
+// and of up; down: 32 consecutive d rows), so that the codes a wave unpacks
+// for one MFMA step feed four MFMAs.  The group accumulators and the running
+// fp32 totals stay in registers; the reduction runs in 128-column chunks,
+// staged through a ring of four LDS slots.
 #pragma once
 
 #include "forward_engine.hpp"
@@ -40,29 +42,26 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kPfFragRows = 32;                    // rows of a fragment (MFMA M)
 constexpr int kPfFragBytes = 1024;                 // 32 rows x 16 16-bit values
 constexpr int kPfWaves = 8;
-constexpr int kPfWaveTiles = 2;                    // fragment rows per wave (64 tokens)
-constexpr int kPfWtok = 1;                         // token groups per workgroup (64-token m-tiles)
 constexpr int kPfSlots = 4;                        // LDS ring: chunks c-1 .. c+2
 
-template <int WTOK>
-struct PfShape {
-  static constexpr int kWrow = kPfWaves / WTOK;                  // row groups
-  static constexpr int kTiles = WTOK * kPfWaveTiles;             // fragment rows per workgroup
+struct PfCfg {
+  static constexpr int kTiles = 4;                               // fragment rows per m-tile
   static constexpr int kTokens = kTiles * kPfFragRows;           // tokens per m-tile
   static constexpr int kFragBytes = kTiles * 8 * kPfFragBytes;   // A fragments of one chunk
   static constexpr int kSumBytes = 2048;                         // group sums: kTiles x <= 4 groups x 32 rows
   static constexpr int kStageBytes = kFragBytes + kSumBytes;
   static constexpr int kLdsBytes = kPfSlots * kStageBytes;
-  static constexpr int kRowsGateUp = kWrow * 32;                 // ffn rows per gate/up workgroup
-  static constexpr int kRowsDown = kWrow * 64;                   // d rows per down workgroup
+  static constexpr int kRowsGateUp = kPfWaves / 2 * 32;          // ffn rows per gate/up workgroup
+  static constexpr int kRowsDown = kPfWaves * 32;                // d rows per down workgroup
   // every wave issues the same number of staging loads per chunk (counted waits)
   static constexpr int kFragLoadsPerWave = kTiles * 8 / kPfWaves;
   static_assert(kTiles * 8 % kPfWaves == 0, "fragments spread evenly over the waves");
   static_assert(kTiles * 4 * 32 * 4 <= kSumBytes, "group sums of a chunk");
   static_assert(kLdsBytes <= kLdsPerCu, "prefill stages fit the LDS of a CU");
   static_assert(kRowsGateUp % 128 == 0, "a gate/up workgroup covers whole groups of h columns");
+  static_assert(kPfWaves / 2 * kTiles * 16 * 64 * 4 + kTiles * 8 * kPfFragBytes <= kLdsBytes,
+                "the up totals and the h tile fit the ring");
 };
-using PfCfg = PfShape<kPfWtok>;
 
 // Expert-to-tile tables written by the set-up kernel into the workspace.
 struct PrefillTables {
@@ -149,15 +148,15 @@ __device__ __forceinline__ f32x16 pf_mfma(u32x4 a, u32x4 b, f32x16 c) {
                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
-// Stage chunk c straight into LDS: the A fragments of all kTiles fragment rows
+// Stage chunk c straight into LDS: the A fragments of the kTiles fragment rows
 // (rows past the m-tile's end read the padding rows of the buffer; their sums
 // are dropped) and the group sums [tile][GPC][32].  Each wave issues
 // kFragLoadsPerWave + 1 loads; the sums are split in two 1 KB halves, and
 // waves loading the same half write identical bytes.
-template <int GPC, int WTOK>
-__device__ __forceinline__ void pf_stage(unsigned char* stage, const PrefillGemm& g, int f0, int c,
-                                         int wave, int lane) {
-  using S = PfShape<WTOK>;
+template <int GPC>
+__device__ __forceinline__ void pf_stage(unsigned char* stage, const PrefillGemm& g, int f0, int c, int wave,
+                                         int lane) {
+  using S = PfCfg;
   const int ksteps = g.K / 16, ng = g.K * GPC / kTileCols;
 #pragma unroll
   for (int i = 0; i < S::kFragLoadsPerWave; ++i) {
@@ -177,55 +176,68 @@ __device__ __forceinline__ void pf_stage(unsigned char* stage, const PrefillGemm
 }
 
 // Group epilogue: tot += s 2^b * (acc - (1 + z 2^-b) * S_g); per lane its
-// row's s and z (word sw of each stream), S_g of the tile rows from the stage.
-template <int BITS, int GPC, bool BF16, int WTOK>
-__device__ __forceinline__ void pf_epilogue(const f32x16 (&acc)[kPfWaveTiles][2], const uint32_t (&sw)[2],
-                                            const unsigned char* stage, int q, int tg, int lane,
-                                            f32x16 (&tot)[kPfWaveTiles][2]) {
-  using S = PfShape<WTOK>;
-  const float* ssum = reinterpret_cast<const float*>(stage + S::kFragBytes);
-  float sj[2], cj[2];
+// row's s and z (word sw), S_g of the tile rows from the stage.
+template <int BITS, int GPC>
+__device__ __forceinline__ void pf_epilogue(const f32x16 (&acc)[PfCfg::kTiles], uint32_t sw,
+                                            const unsigned char* stage, int q, int lane,
+                                            f32x16 (&tot)[PfCfg::kTiles]) {
+  const float* ssum = reinterpret_cast<const float*>(stage + PfCfg::kFragBytes);
+  const float sj = half_bits_to_float(sw & 0xffffu) * (float)(1 << BITS);
+  const float cj = fmaf(half_bits_to_float(sw >> 16), 1.0f / (float)(1 << BITS), 1.0f);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    sj[j] = half_bits_to_float(sw[j] & 0xffffu) * (float)(1 << BITS);
-    cj[j] = fmaf(half_bits_to_float(sw[j] >> 16), 1.0f / (float)(1 << BITS), 1.0f);
-  }
-#pragma unroll
-  for (int t = 0; t < kPfWaveTiles; ++t) {
-    const float* sr = ssum + ((2 * tg + t) * GPC + q) * 32 + 4 * (lane >> 5);
+  for (int t = 0; t < PfCfg::kTiles; ++t) {
+    const float* sr = ssum + (t * GPC + q) * 32 + 4 * (lane >> 5);
     f32x4 sx[4];
 #pragma unroll
     for (int k4 = 0; k4 < 4; ++k4) sx[k4] = *reinterpret_cast<const f32x4*>(sr + 8 * k4);
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float u = fmaf(-cj[j], sx[i >> 2][i & 3], acc[t][j][i]);
-        tot[t][j][i] = fmaf(sj[j], u, tot[t][j][i]);
-      }
+    for (int i = 0; i < 16; ++i) {
+      const float u = fmaf(-cj, sx[i >> 2][i & 3], acc[t][i]);
+      tot[t][i] = fmaf(sj, u, tot[t][i]);
+    }
   }
 }
 
-// MFMAs of group q of the chunk in `stage` with the words `w`.
+// MFMAs of group q of the chunk in `stage` with the words `w`: per step the
+// eight codes of this lane's row feed the MFMAs of all kTiles fragment rows.
 template <int BITS, int GPC, bool BF16>
-__device__ __forceinline__ void pf_group(const unsigned char* stage, const uint32_t (&w)[2][2][BITS], int q,
-                                         int tg, int lane, uint32_t magic, f32x16 (&acc)[kPfWaveTiles][2]) {
+__device__ __forceinline__ void pf_group(const unsigned char* stage, const uint32_t (&w)[2][BITS], int q, int lane,
+                                         uint32_t magic, f32x16 (&acc)[PfCfg::kTiles]) {
   constexpr int KV = 8 / GPC;   // MFMA steps per group
-  const unsigned char* arow = stage + (2 * tg * 8) * kPfFragBytes + lane * 16;
+  const unsigned char* arow = stage + lane * 16;
 #pragma unroll
   for (int vv = 0; vv < KV; ++vv) {
     const int v = q * KV + vv;
-    u32x4 a[kPfWaveTiles];
+    u32x4 a[PfCfg::kTiles];
 #pragma unroll
-    for (int t = 0; t < kPfWaveTiles; ++t) a[t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + v) * kPfFragBytes);
-    const u32x4 b0 = pf_codes<BITS, BF16>(w[0][v & 1], v >> 1, magic);
-    const u32x4 b1 = pf_codes<BITS, BF16>(w[1][v & 1], v >> 1, magic);
+    for (int t = 0; t < PfCfg::kTiles; ++t) a[t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + v) * kPfFragBytes);
+    const u32x4 b = pf_codes<BITS, BF16>(w[v & 1], v >> 1, magic);
 #pragma unroll
-    for (int t = 0; t < kPfWaveTiles; ++t) {
+    for (int t = 0; t < PfCfg::kTiles; ++t) {
       const f32x16 z = {};
-      acc[t][0] = pf_mfma<BF16>(a[t], b0, vv == 0 ? z : acc[t][0]);
-      acc[t][1] = pf_mfma<BF16>(a[t], b1, vv == 0 ? z : acc[t][1]);
+      acc[t] = pf_mfma<BF16>(a[t], b, vv == 0 ? z : acc[t]);
     }
+  }
+}
+
+template <int BITS, int GPC, bool BF16>
+__device__ __forceinline__ void pf_chunk_body(const unsigned char* __restrict__ cur,
+                                              const unsigned char* __restrict__ prev,
+                                              unsigned char* __restrict__ next, const PfStream& sp,
+                                              const PrefillGemm& g, int f0, bool late, bool first, int c, int last,
+                                              int wave, int lane, const uint32_t (&w)[2][BITS],
+                                              const uint32_t (&s)[GPC], uint32_t (&nw)[2][BITS],
+                                              uint32_t (&ns)[GPC], uint32_t& ps, uint32_t magic,
+                                              f32x16 (&acc)[PfCfg::kTiles], f32x16 (&tot)[PfCfg::kTiles]) {
+  if (late && !first) pf_epilogue<BITS, GPC>(acc, ps, prev, GPC - 1, lane, tot);
+  pf_load<BITS, GPC>(nw, ns, sp, c + 1 < last ? c + 1 : last);
+  __builtin_amdgcn_sched_barrier(0);   // the words go out before the stage (counted waits)
+  pf_stage<GPC>(next, g, f0, c + 2 < last ? c + 2 : last, wave, lane);
+#pragma unroll
+  for (int q = 0; q < GPC; ++q) {
+    pf_group<BITS, GPC, BF16>(cur, w, q, lane, magic, acc);
+    if (q < GPC - 1 || !late) pf_epilogue<BITS, GPC>(acc, s[q], cur, q, lane, tot);
+    else ps = s[q];
   }
 }
 
@@ -235,18 +247,16 @@ __device__ __forceinline__ void pf_group(const unsigned char* stage, const uint3
 // may still be outstanding behind the words of c), then the MFMAs and group
 // epilogues.  The two waves of a SIMD run half a phase apart: a "late" wave
 // does the epilogue of the previous chunk's last group first (its acc, its
-// scale words `ps` and its stage, kept by the fourth LDS slot) and defers its
+// scale word `ps` and its stage, kept by the fourth LDS slot) and defers its
 // own last group's epilogue, so that one wave's epilogue overlaps the other's
 // MFMAs.
-template <int BITS, int GPC, bool BF16, int WTOK>
-__device__ __forceinline__ void pf_chunk(const PfStream (&sp)[2], const PrefillGemm& g, int f0, int tg,
-                                         bool active, bool late, bool first, int c, int last, int slot,
-                                         unsigned char* smem, int wave, int lane,
-                                         const uint32_t (&w)[2][2][BITS], const uint32_t (&s)[2][GPC],
-                                         uint32_t (&nw)[2][2][BITS], uint32_t (&ns)[2][GPC],
-                                         uint32_t (&ps)[2], uint32_t magic, f32x16 (&acc)[kPfWaveTiles][2],
-                                         f32x16 (&tot)[kPfWaveTiles][2]) {
-  using S = PfShape<WTOK>;
+template <int BITS, int GPC, bool BF16>
+__device__ __forceinline__ void pf_chunk(const PfStream& sp, const PrefillGemm& g, int f0, bool late, bool first,
+                                         int c, int last, int slot, unsigned char* smem, int wave, int lane,
+                                         const uint32_t (&w)[2][BITS], const uint32_t (&s)[GPC],
+                                         uint32_t (&nw)[2][BITS], uint32_t (&ns)[GPC], uint32_t& ps, uint32_t magic,
+                                         f32x16 (&acc)[PfCfg::kTiles], f32x16 (&tot)[PfCfg::kTiles]) {
+  using S = PfCfg;
   // Stage c has landed in LDS once at most the loads issued after it (stage
   // c+1) are outstanding; the plain barrier then publishes it (a fenced
   // __syncthreads would also wait for stage c+1, which is still in flight).
@@ -256,51 +266,40 @@ __device__ __forceinline__ void pf_chunk(const PfStream (&sp)[2], const PrefillG
   asm volatile("" ::: "memory");
   const int slotp = slot == 0 ? kPfSlots - 1 : slot - 1;
   const int slot2 = slot + 2 >= kPfSlots ? slot + 2 - kPfSlots : slot + 2;
-  const unsigned char* cur = smem + slot * S::kStageBytes;
-  if (active && late && !first) pf_epilogue<BITS, GPC, BF16, WTOK>(acc, ps, smem + slotp * S::kStageBytes, GPC - 1, tg, lane, tot);
-#pragma unroll
-  for (int j = 0; j < 2; ++j) pf_load<BITS, GPC>(nw[j], ns[j], sp[j], c + 1 < last ? c + 1 : last);
-  pf_stage<GPC, WTOK>(smem + slot2 * S::kStageBytes, g, f0, c + 2 < last ? c + 2 : last, wave, lane);
-  if (!active) return;
-#pragma unroll
-  for (int q = 0; q < GPC; ++q) {
-    pf_group<BITS, GPC, BF16>(cur, w, q, tg, lane, magic, acc);
-    uint32_t sw[2] = {s[0][q], s[1][q]};
-    if (q < GPC - 1 || !late) pf_epilogue<BITS, GPC, BF16, WTOK>(acc, sw, cur, q, tg, lane, tot);
-    else { ps[0] = sw[0]; ps[1] = sw[1]; }
-  }
+  pf_chunk_body<BITS, GPC, BF16>(smem + slot * S::kStageBytes, smem + slotp * S::kStageBytes,
+                                 smem + slot2 * S::kStageBytes, sp, g, f0, late, first, c, last, wave, lane,
+                                 w, s, nw, ns, ps, magic, acc, tot);
 }
 
 // Chunks [c_begin, c_end) of the reduction, two per iteration so that the
 // two register sets of weight words alternate without copies.
-template <int BITS, int GPC, bool BF16, int WTOK>
-__device__ __forceinline__ void pf_loop(const PfStream (&sp)[2], const PrefillGemm& g, int f0, int tg,
-                                        bool active, bool late, int c_begin, int c_end, unsigned char* smem,
-                                        int wave, int lane, f32x16 (&tot)[kPfWaveTiles][2]) {
-  using S = PfShape<WTOK>;
+template <int BITS, int GPC, bool BF16>
+__device__ __forceinline__ void pf_loop(const PfStream& sp, const PrefillGemm& g, int f0, bool late, int c_begin,
+                                        int c_end, unsigned char* smem, int wave, int lane,
+                                        f32x16 (&tot)[PfCfg::kTiles]) {
+  using S = PfCfg;
   if (c_begin >= c_end) return;
   const uint32_t magic = vgpr_constant(Fmt<!BF16>::kMagic2);
   const int last = c_end - 1;
-  uint32_t wa[2][2][BITS], sa[2][GPC], wb[2][2][BITS], sb[2][GPC], ps[2] = {0u, 0u};
-  f32x16 acc[kPfWaveTiles][2];
-#pragma unroll
-  for (int j = 0; j < 2; ++j) pf_load<BITS, GPC>(wa[j], sa[j], sp[j], c_begin);
-  pf_stage<GPC, WTOK>(smem, g, f0, c_begin, wave, lane);
-  pf_stage<GPC, WTOK>(smem + S::kStageBytes, g, f0, c_begin + 1 < last ? c_begin + 1 : last, wave, lane);
+  uint32_t wa[2][BITS], sa[GPC], wb[2][BITS], sb[GPC], ps = 0u;
+  f32x16 acc[S::kTiles];
+  pf_load<BITS, GPC>(wa, sa, sp, c_begin);
+  pf_stage<GPC>(smem, g, f0, c_begin, wave, lane);
+  pf_stage<GPC>(smem + S::kStageBytes, g, f0, c_begin + 1 < last ? c_begin + 1 : last, wave, lane);
   int slot = 0;
   for (int c = c_begin; c < c_end; c += 2) {
-    pf_chunk<BITS, GPC, BF16, WTOK>(sp, g, f0, tg, active, late, c == c_begin, c, last, slot, smem, wave, lane,
-                                    wa, sa, wb, sb, ps, magic, acc, tot);
+    pf_chunk<BITS, GPC, BF16>(sp, g, f0, late, c == c_begin, c, last, slot, smem, wave, lane, wa, sa, wb, sb, ps,
+                              magic, acc, tot);
     slot = slot + 1 == kPfSlots ? 0 : slot + 1;
     if (c + 1 < c_end)
-      pf_chunk<BITS, GPC, BF16, WTOK>(sp, g, f0, tg, active, late, false, c + 1, last, slot, smem, wave, lane,
-                                      wb, sb, wa, sa, ps, magic, acc, tot);
+      pf_chunk<BITS, GPC, BF16>(sp, g, f0, late, false, c + 1, last, slot, smem, wave, lane, wb, sb, wa, sa, ps,
+                                magic, acc, tot);
     slot = slot + 1 == kPfSlots ? 0 : slot + 1;
   }
   // the late waves' last epilogue: the last chunk's stage is the slot before `slot`
-  if (active && late)
-    pf_epilogue<BITS, GPC, BF16, WTOK>(acc, ps, smem + (slot == 0 ? kPfSlots - 1 : slot - 1) * S::kStageBytes,
-                                 GPC - 1, tg, lane, tot);
+  if (late)
+    pf_epilogue<BITS, GPC>(acc, ps, smem + (slot == 0 ? kPfSlots - 1 : slot - 1) * S::kStageBytes, GPC - 1, lane,
+                           tot);
   wait_vmcnt<0>();   // the clamped re-reads of the last chunks land before LDS is reused
 }
 
@@ -319,110 +318,105 @@ prefill_kernel(LayerArgs L, const int32_t* __restrict__ offsets, PrefillTables t
   const int e = tb.mt_e[mt], j = tb.mt_j[mt];
   const int f0 = tb.ftile_base[e] + S::kTiles * j;
   const int nf = tb.ftile_base[e + 1] - f0;
-  const int nmt = nf < S::kTiles ? nf : S::kTiles;
+  const int nmt = nf < S::kTiles ? nf : S::kTiles;   // fragment rows of this m-tile that hold the expert's rows
   const int lane = threadIdx.x & 63, wave = wave_id();
-  const int tg = wave / S::kWrow, rg = wave - tg * S::kWrow;
-  const bool active = 2 * tg < nmt;   // wave-uniform; idle waves still stage and synchronise
   const bool late = wave >= kPfWaves / 2;   // shares a SIMD with wave - 4: runs half a phase later
   const int ntiles = g.K / kTileCols;
   const int c_begin = split * g.c_per_split;
   const int c_end = (c_begin + g.c_per_split) < ntiles ? (c_begin + g.c_per_split) : ntiles;
   const int bits = L.cum_bits[e + 1] - L.cum_bits[e];
 
-  int row[2];
-  PfStream sp[2];
-  // gate/up: the last row tile may cover only the first 128 of its 256 ffn
-  // rows (ffn is a multiple of 128); its surplus waves read the tile's first
-  // rows again (in bounds) and write nothing.
-  bool rows_valid = true;
-  if (GATEUP) {
-    row[0] = row[1] = nt * S::kRowsGateUp + 32 * rg;
-    if (row[0] + 32 > L.ffn) {
-      rows_valid = false;
-      row[0] = row[1] = nt * S::kRowsGateUp + 32 * (rg & 3);
-    }
-    sp[0] = pf_stream(L, e, 0, row[0], g.K, bits, lane);
-    sp[1] = pf_stream(L, e, 1, row[1], g.K, bits, lane);
-  } else {
-    int r0 = nt * S::kRowsDown + 64 * rg;
-    if (r0 + 64 > L.d) r0 = L.d - 64;   // surplus waves of the last tile repeat the last rows
-    row[0] = r0;
-    row[1] = r0 + 32;
-    sp[0] = pf_stream(L, e, 2, row[0], g.K, bits, lane);
-    sp[1] = pf_stream(L, e, 2, row[1], g.K, bits, lane);
-  }
+  // This wave's 32 weight rows.  ffn and d are multiples of 128, so a block of
+  // 32 rows lies wholly inside or outside its matrix; the surplus waves of
+  // the last down tile read the matrix's last rows (in bounds) and write nothing.
+  const int rb = GATEUP ? wave >> 1 : wave;
+  int row = nt * (GATEUP ? S::kRowsGateUp : S::kRowsDown) + 32 * rb;
+  const bool row_valid = row < (GATEUP ? L.ffn : L.d);
+  if (!row_valid) row = (GATEUP ? L.ffn : L.d) - 32;
+  const PfStream sp = pf_stream(L, e, GATEUP ? (wave & 1) : 2, row, g.K, bits, lane);
 
-  f32x16 tot[kPfWaveTiles][2];
+  f32x16 tot[S::kTiles];
 #pragma unroll
-  for (int t = 0; t < kPfWaveTiles; ++t)
+  for (int t = 0; t < S::kTiles; ++t)
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) tot[t][s][i] = 0.0f;
+    for (int i = 0; i < 16; ++i) tot[t][i] = 0.0f;
 
   if (bits == 1)
-    pf_loop<1, GPC, GATEUP, kPfWtok>(sp, g, f0, tg, active, late, c_begin, c_end, smem, wave, lane, tot);
+    pf_loop<1, GPC, GATEUP>(sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
   else if (bits == 2)
-    pf_loop<2, GPC, GATEUP, kPfWtok>(sp, g, f0, tg, active, late, c_begin, c_end, smem, wave, lane, tot);
+    pf_loop<2, GPC, GATEUP>(sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
   else
-    pf_loop<3, GPC, GATEUP, kPfWtok>(sp, g, f0, tg, active, late, c_begin, c_end, smem, wave, lane, tot);
+    pf_loop<3, GPC, GATEUP>(sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
 
   // D layout: lane holds column n = lane%32 (weight row) and, for i < 16,
   // row m = 8*(i/4) + 4*(lane/32) + i%4 (token) of each 32x32 tile.
   const int n = lane & 31;
   if (GATEUP) {
-    // h = silu(gate) * up rounded to fp16; then the group sums of the rounded
-    // h: per wave over its 32 columns (butterfly in a fixed order), then over
-    // the workgroup's 128 columns in LDS (row groups in order).
-    const int col = row[0] + n;
-    unsigned char* hb = reinterpret_cast<unsigned char*>(g.h);
-    __syncthreads();                       // the ring is free: reuse it for the partial sums
-    float* part = reinterpret_cast<float*>(smem);   // [tg][rg][64 rows]
+    // The up waves hand their totals to the gate waves of the same rows
+    // through LDS; the gate waves form h = silu(gate) * up rounded to fp16 in
+    // an LDS copy of the workgroup's h tile, laid out as in global memory (per
+    // fragment row, 8 KB: its 128 columns are 8 consecutive 1 KB fragments),
+    // which all threads then store with 16-byte writes; the group sums of the
+    // rounded h are read back from that copy, each in column order.
+    __syncthreads();                       // the ring is free
+    float* upt = reinterpret_cast<float*>(smem);                               // [rb][t][i][64 lanes]
+    unsigned char* ht = smem + kPfWaves / 2 * S::kTiles * 16 * 64 * 4;         // [t][8 fragments]
+    if (wave & 1) {
 #pragma unroll
-    for (int t = 0; t < kPfWaveTiles; ++t) {
-      const int f = f0 + 2 * tg + t;
-      if (active && rows_valid && 2 * tg + t < nmt) {
+      for (int t = 0; t < S::kTiles; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) upt[((rb * S::kTiles + t) * 16 + i) * 64 + lane] = tot[t][i];
+    }
+    __syncthreads();
+    if (!(wave & 1)) {
+      const int c = 32 * rb + n;           // column within the workgroup's 128
+#pragma unroll
+      for (int t = 0; t < S::kTiles; ++t) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int m = 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-          const uint16_t h16 = float_to_half_sat(silu(tot[t][0][i]) * tot[t][1][i]);
-          *reinterpret_cast<uint16_t*>(hb + frag_offset(f, m, col, L.ffn)) = h16;
-          float v = half_bits_to_float(h16);
-#pragma unroll
-          for (int off = 1; off < 32; off <<= 1) v += __shfl_xor(v, off);
-          if (n == 0) part[(tg * S::kWrow + rg) * 64 + t * 32 + m] = v;
+          const float up = upt[((rb * S::kTiles + t) * 16 + i) * 64 + lane];
+          *reinterpret_cast<uint16_t*>(ht + (size_t)t * 8 * kPfFragBytes + frag_offset(0, m, c, 128)) =
+              float_to_half_sat(silu(tot[t][i]) * up);
         }
       }
     }
     __syncthreads();
-    const int gpw = L.G / 32;                       // row groups (32 columns each) per group
+    unsigned char* hb = reinterpret_cast<unsigned char*>(g.h);
+    for (int idx = threadIdx.x; idx < nmt * 8 * kPfFragBytes / 16; idx += blockDim.x) {
+      const int t = idx / (8 * kPfFragBytes / 16), p = idx - t * (8 * kPfFragBytes / 16);
+      *reinterpret_cast<u32x4*>(hb + frag_offset(f0 + t, 0, nt * S::kRowsGateUp, L.ffn) + 16 * p) =
+          *reinterpret_cast<const u32x4*>(ht + (size_t)t * 8 * kPfFragBytes + 16 * p);
+    }
     const int ngw = S::kRowsGateUp / L.G;           // groups in this workgroup
-    const int ng_valid = (L.ffn - nt * S::kRowsGateUp) / L.G;   // groups inside ffn
-    for (int idx = threadIdx.x; idx < kPfWtok * 64 * ngw; idx += blockDim.x) {
-      const int q = idx % ngw, r = (idx / ngw) % 64, tg2 = idx / (ngw * 64);
-      if (2 * tg2 + r / 32 >= nmt || q >= ng_valid) continue;
+    for (int idx = threadIdx.x; idx < nmt * 32 * ngw; idx += blockDim.x) {
+      const int r = idx % (nmt * 32), q = idx / (nmt * 32);
+      const int t = r >> 5, m = r & 31;
       float v = 0.0f;
-      for (int k = 0; k < gpw; ++k) v += part[(tg2 * S::kWrow + q * gpw + k) * 64 + r];
-      const int f = f0 + 2 * tg2 + r / 32;
-      g.hsum[((size_t)f * (L.ffn / L.G) + (nt * S::kRowsGateUp) / L.G + q) * 32 + (r & 31)] = v;
+      for (int c0 = q * L.G; c0 < (q + 1) * L.G; c0 += 8) {
+        const u32x4 h8 = *reinterpret_cast<const u32x4*>(ht + (size_t)t * 8 * kPfFragBytes + frag_offset(0, m, c0, 128));
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          v += half_bits_to_float(h8[w] & 0xffffu);
+          v += half_bits_to_float(h8[w] >> 16);
+        }
+      }
+      g.hsum[((size_t)(f0 + t) * (L.ffn / L.G) + (nt * S::kRowsGateUp) / L.G + q) * 32 + m] = v;
     }
   } else {
-    if (!active) return;
+    if (!row_valid) return;
     int ebase, ecount;
     expert_range_offsets(offsets, e, tb.P, ebase, ecount);
     const int pbase = ebase + S::kTokens * j;
     const int pend = ebase + ecount;
     float* out = g.partial + (size_t)split * g.part_stride;
 #pragma unroll
-    for (int t = 0; t < kPfWaveTiles; ++t) {
+    for (int t = 0; t < S::kTiles; ++t) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int m = 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-        const int pos = pbase + (2 * tg + t) * 32 + m;
-        if (pos < pend) {
-#pragma unroll
-          for (int s = 0; s < 2; ++s) out[(size_t)pos * L.d + row[s] + n] = tot[t][s][i];
-        }
+        const int pos = pbase + t * 32 + m;
+        if (pos < pend) out[(size_t)pos * L.d + row + n] = tot[t][i];
       }
     }
   }

@@ -16,7 +16,7 @@
 // raw != 0 the helpers' range checks are bypassed (raw counts, offsets,
 // tokens and positions): the test uses that to show its garbage inputs do
 // reach past the buffers, so that a zero count means the checks held.
-#include "../../paper_2410_06270_amd/csrc/mc_device.hpp"
+#include "../../paper_2410_06270_amd/csrc/prefill.hpp"   // PfCfg; includes mc_device.hpp
 
 #include <vector>
 
@@ -30,6 +30,9 @@ inline void check(long long idx, long long size) {
 }
 
 }  // namespace
+
+// Tokens per prefill m-tile (the workspace capacities depend on it).
+extern "C" int route_audit_mt_tokens() { return PfCfg::kTokens; }
 
 extern "C" long long route_audit(int T, int E, int k, int d, int ffn, const int32_t* counts,
                                  const int32_t* offsets, const int32_t* pair_token, const int32_t* pair_pos,
@@ -69,14 +72,14 @@ extern "C" long long route_audit(int T, int E, int k, int d, int ffn, const int3
       const int pos = cpos(pair_pos[t * k + r]);
       if (raw || pos >= 0) check((long long)pos * d + d - 1, (long long)P * d);
     }
-  // prefill set-up: fragment rows of 32 and m-tiles of 64 per expert, the
-  // tables left empty when they would not fit their capacity
+  // prefill set-up: fragment rows of 32 and m-tiles of PfCfg::kTokens per
+  // expert, the tables left empty when they would not fit their capacity
   std::vector<int> ftile_base(E + 1, 0), ftile_e(f_max > 0 ? f_max : 1, -1);
   int nf_tot = 0, nm_tot = 0;
   for (int e = 0; e < E; ++e) {
     const int c = ccount(counts[e]);
     nf_tot += (c + 31) / 32;
-    nm_tot += (c + 63) / 64;
+    nm_tot += (c + PfCfg::kTokens - 1) / PfCfg::kTokens;
   }
   if (nf_tot <= f_max && nm_tot <= mt_max) {
     int fb = 0;
@@ -108,16 +111,18 @@ extern "C" long long route_audit(int T, int E, int k, int d, int ffn, const int3
     }
     check(f, f_max);                                          // the tiled copy written
   }
-  // prefill down GEMM: m-tiles of 64 pairs of each expert, partial writes
+  // prefill GEMMs: m-tiles of PfCfg::kTokens pairs of each expert, the
+  // staged fragment rows and the down GEMM's partial writes
   for (int e = 0; e < E; ++e) {
     if (!(nf_tot <= f_max && nm_tot <= mt_max)) break;
     const int c = ccount(counts[e]);
     int ebase, ecount;
     range_off(e, ebase, ecount);
-    for (int j = 0; 64 * j < c; ++j) {
-      check(ftile_base[e] + 2 * j + 1, f_max + 2);             // staged fragment rows (2 padding rows)
-      for (int m = 0; m < 64; ++m) {
-        const int pos = ebase + 64 * j + m;
+    for (int j = 0; PfCfg::kTokens * j < c; ++j) {
+      // staged fragment rows (kTiles padding rows past f_max)
+      check(ftile_base[e] + PfCfg::kTiles * j + PfCfg::kTiles - 1, f_max + PfCfg::kTiles);
+      for (int m = 0; m < PfCfg::kTokens; ++m) {
+        const int pos = ebase + PfCfg::kTokens * j + m;
         if (pos < ebase + ecount) check((long long)pos * d + d - 1, (long long)P * d);
       }
     }

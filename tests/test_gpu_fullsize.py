@@ -3,8 +3,9 @@ ffn=14336, E=8, widths [3,3,3,2,2,2,2,3], G=128) in the launch configuration
 the benchmark times.  Packed words are compared in full for one expert; the
 layer output is compared on sampled tokens x rows, which the oracle computes
 one by one from its own quantization of the same fp32 weights: every token
-and row for decode batches, and for prefill one token from every 64-token
-m-tile of every expert over rows covering every 512-row tile."""
+and row for decode batches, and for prefill one token from every 64 routed
+pairs of every expert (two per 128-token m-tile of the grouped GEMMs) over
+rows covering every 256-row tile of the down GEMM."""
 import numpy as np
 import pytest
 
@@ -87,9 +88,9 @@ def test_mixtral_decode_sampled(mc, mixtral, T):
         toks, rows = list(range(T)), None
     else:
         # prefill: the first and last tokens, a pruned and a protected token,
-        # and one token from every 64-token m-tile of every expert (at a
-        # position that moves through the tile), over rows that cover every
-        # 512-row tile of the down GEMM (its first and last rows included)
+        # and one token from every 64 pairs of every expert (at a position
+        # that moves through them), over rows that cover every 256-row tile
+        # of the down GEMM (its first and last rows included)
         toks = {0, T - 1}
         pr = np.nonzero(ref["kept"][:, 1] == 0)[0]
         if len(pr):
@@ -106,9 +107,9 @@ def test_mixtral_decode_sampled(mc, mixtral, T):
         toks = sorted(toks)
         g = np.random.default_rng(T)
         rows = {0, d - 1}
-        for t0 in range(0, d, 512):
-            rows |= {t0, t0 + 511}
-            rows |= set((t0 + g.choice(512, 24, replace=False)).tolist())
+        for t0 in range(0, d, 256):
+            rows |= {t0, t0 + 255}
+            rows |= set((t0 + g.choice(256, 12, replace=False)).tolist())
         rows = sorted(rows)
     need = sorted({int(ref["topk_idx"][t, rr]) for t in toks for rr in range(k) if ref["kept"][t, rr]})
     logical = [None] * E

@@ -6,7 +6,7 @@ Eq. 5 read for k > 2).
 Decode (16 tokens) is compared on every output; prefill (2048 tokens, the
 grouped GEMMs) on tokens chosen so that every expert holding a token is
 covered (experts 16..63 included) together with the first, middle and last
-64-token m-tile of the hottest expert, every row."""
+128-token m-tile of the hottest expert, every row."""
 import numpy as np
 import pytest
 
@@ -101,11 +101,12 @@ def test_olmoe_prefill_every_expert(mc, olmoe):
     for e in np.nonzero(counts)[0]:           # one token of every expert holding one
         toks.add(int(pt[offsets[e] + counts[e] // 2]))
     hot = int(np.argmax(counts))
-    n_mt = (int(counts[hot]) + 63) // 64
+    MT = 128                                  # tokens per m-tile of the grouped GEMMs
+    n_mt = (int(counts[hot]) + MT - 1) // MT
     assert n_mt >= 3
     for j in (0, n_mt // 2, n_mt - 1):        # first, middle and last m-tile of the hottest expert
-        lo = offsets[hot] + 64 * j
-        hi = min(offsets[hot] + 64 * (j + 1), offsets[hot + 1])
+        lo = offsets[hot] + MT * j
+        hi = min(offsets[hot] + MT * (j + 1), offsets[hot + 1])
         for p in (lo, (lo + hi) // 2, hi - 1):
             toks.add(int(pt[p]))
     toks = sorted(toks)

@@ -21,26 +21,28 @@ import synthetic
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "tests", "native", "route_audit.hip")
-HDR = os.path.join(ROOT, "paper_2410_06270_amd", "csrc", "mc_device.hpp")
+HDRS = [os.path.join(ROOT, "paper_2410_06270_amd", "csrc", h) for h in ("mc_device.hpp", "prefill.hpp",
+                                                                          "forward_engine.hpp")]
 LIB = os.path.join(ROOT, "_build", "route_audit.so")
 
 
 @pytest.fixture(scope="module")
 def audit():
     os.makedirs(os.path.dirname(LIB), exist_ok=True)
-    if (not os.path.exists(LIB) or os.path.getmtime(LIB) < max(os.path.getmtime(SRC), os.path.getmtime(HDR))):
+    if (not os.path.exists(LIB) or os.path.getmtime(LIB) < max(os.path.getmtime(f) for f in [SRC] + HDRS)):
         subprocess.check_call(["hipcc", "--offload-arch=gfx950", "-O1", "-std=c++17", "-shared", "-fPIC",
                                "-o", LIB + ".tmp", SRC])
         os.replace(LIB + ".tmp", LIB)
     lib = ctypes.CDLL(LIB)
     lib.route_audit.restype = ctypes.c_longlong
+    mt_tokens = lib.route_audit_mt_tokens()
     p = ctypes.c_void_p
 
     def run(T, E, k, d, ffn, counts, offsets, pair_token, pair_pos, raw=False):
         arrs = [np.ascontiguousarray(a, dtype=np.int32) for a in (counts, offsets, pair_token, pair_pos)]
         P = T * k
         f_max = (P + 31 * E) // 32          # the prefill workspace's capacities
-        mt_max = (P + 63 * E) // 64
+        mt_max = (P + (mt_tokens - 1) * E) // mt_tokens
         return lib.route_audit(T, E, k, d, ffn, *[p(a.ctypes.data) for a in arrs], f_max, mt_max, int(raw))
     return run
 
