@@ -102,12 +102,15 @@ PrefillLayout prefill_layout(int T, int E, int k, int d, int ffn) {
   pl.f_max = (int)((P + (size_t)(kPfFragRows - 1) * E) / kPfFragRows);
   pl.mt_max = (int)((P + (size_t)(PfCfg::kTokens - 1) * E) / PfCfg::kTokens);
   const int nt_down = (d + PfCfg::kRowsDown - 1) / PfCfg::kRowsDown;
-  const int wgs = pl.mt_max * nt_down;
-  int s = (1024 + wgs - 1) / wgs;
+  // Split the down GEMM's reduction so that its workgroups fill the 256 CUs
+  // in whole rounds: pick s minimising rounds(s) / s (the time of one round
+  // shrinks as 1/s), the smallest on ties; at least 8 chunks per split.
+  const long long wgs = (long long)pl.mt_max * nt_down;
   int maxs = (ffn / kTileCols) / 8;
   if (maxs > 4) maxs = 4;
-  if (s > maxs) s = maxs;
-  if (s < 1) s = 1;
+  int s = 1;
+  for (int c = 2; c <= maxs; ++c)
+    if ((double)((wgs * c + 255) / 256) / c < (double)((wgs * s + 255) / 256) / s - 1e-9) s = c;
   pl.nsplit = s;
   // the GEMMs stage whole m-tiles: kTiles - 1 padding fragment rows past the last one
   const size_t rows = (size_t)(pl.f_max + PfCfg::kTiles) * kPfFragRows;
