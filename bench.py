@@ -56,8 +56,9 @@ def parse():
     p.add_argument("--no-router", action="store_true", help="skip the router-logits measurement")
     p.add_argument("--no-gptq", action="store_true", help="skip the GPTQ measurement")
     p.add_argument("--stack-steps", type=int, default=10)
-    p.add_argument("--graph", action="store_true",
-                   help="also time HIP-graph replays of the step (reported as ms_per_step_graph)")
+    p.add_argument("--no-graph", action="store_true",
+                   help="time eager launches only (by default the decode steps are also captured in HIP "
+                        "graphs and the replays timed: ms_per_step_graph)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run a plain device-to-device copy of MIB MiB 5 times (reference "
                         "for the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -209,24 +210,33 @@ def traffic_from_profiles(kernel, workload, hash_now):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(synthetic, T, min_seconds=10.0, max_reps=30):
-    """The oracle on the same decode batch and layer shape: routing of all T
-    tokens and the SwiGLU forward over every kept pair, on random codes and
-    fp16 scale/zero of the real shapes (the timing does not depend on values).
-    The batch is run repeatedly until at least min_seconds of CPU work have
-    been timed (at most max_reps runs); the rate is tokens over total time."""
-    import numpy as np
-    import oracle
-    c = synthetic.config(2)
-    E, d, ffn, k, G, bits, tau = c["E"], c["d"], c["ffn"], c["k"], c["G"], c["bits"], c["tau"][0]
-    lg = synthetic.logits(2, T)
-    imp = synthetic.important_mask(2, T)
-    x = synthetic.activations(2, T)
-    g = np.random.default_rng(7)
-    rt = oracle.route(lg, imp, k, tau)
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _omp_set_threads(n):
+    """Thread count of the OpenMP runtime the oracle's C library runs on."""
+    import ctypes
+    try:
+        ctypes.CDLL("libgomp.so.1").omp_set_num_threads(int(n))
+        return True
+    except (OSError, AttributeError):
+        return False
+
+
+def _random_logical(np, g, E, d, ffn, G, bits, used):
+    """Random codes and fp16 scale/zero of the real shapes for the experts in
+    ``used`` (the oracle's time does not depend on the values)."""
     logical = []
     for e in range(E):
-        if rt["counts"][e] == 0:
+        if not used[e]:
             logical.append(None)
             continue
         per = []
@@ -237,19 +247,84 @@ def cpu_baseline(synthetic, T, min_seconds=10.0, max_reps=30):
             z = g.uniform(0, 2 ** bits[e] - 1, (R, K // G)).astype(np.float16).view(np.uint16)
             per.append((q, s, z))
         logical.append(per)
-    el, reps = 0.0, 0
-    while el < min_seconds and reps < max_reps:
-        t0 = time.perf_counter()
-        rt = oracle.route(lg, imp, k, tau)
-        oracle.moe_forward(x, rt, logical, G)
-        el += time.perf_counter() - t0
-        reps += 1
+    return logical
+
+
+def cpu_baseline(synthetic, T, min_seconds=8.0, max_reps=30):
+    """The oracle timed on this host, on random codes and fp16 scale/zero of
+    the benchmarked shapes (its time does not depend on the values):
+      * the headline figure: the full T-token Mixtral-shaped decode batch
+        (routing + SwiGLU forward over every kept pair), repeated until at
+        least min_seconds of work, with the runtime's default thread count;
+      * the same batch restricted to 4 of its tokens on one thread;
+      * the 4096-token prefill batch (tau = 0) restricted to a slice of its
+        first 256 tokens (every kept pair of those tokens);
+      * one layer of the 32-layer stack at T = 1 and T = 64 (the stack's
+        per-token rate is the one-layer rate / 32).
+    Rates are tokens per second of the sample; the model, nproc and threads
+    of the host are reported with them."""
+    import numpy as np
+    import oracle
+    c = synthetic.config(2)
+    E, d, ffn, k, G, bits, tau = c["E"], c["d"], c["ffn"], c["k"], c["G"], c["bits"], c["tau"][0]
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return dict(value=reps * T / el, unit="tokens/s", cores=threads, kind="oracle",
-                seconds=round(el, 3), runs=reps,
-                sample="%d runs of the full T=%d decode batch: routing + SwiGLU forward over its %d kept "
-                       "pairs on the d=4096/ffn=14336/E=8 layer (random codes, same shapes), %d OpenMP threads"
-                       % (reps, T, int(rt["counts"].sum()), threads))
+    _omp_set_threads(threads)
+    g = np.random.default_rng(7)
+    logical = _random_logical(np, g, E, d, ffn, G, bits, [True] * E)
+
+    def timed(fn, min_s, reps_max):
+        el, reps = 0.0, 0
+        while (el < min_s and reps < reps_max) or reps == 0:
+            t0 = time.perf_counter()
+            fn()
+            el += time.perf_counter() - t0
+            reps += 1
+        return el, reps
+
+    lg, imp, x = synthetic.logits(2, T), synthetic.important_mask(2, T), synthetic.activations(2, T)
+    rt = oracle.route(lg, imp, k, tau)
+    el, reps = timed(lambda: oracle.moe_forward(x, oracle.route(lg, imp, k, tau), logical, G), min_seconds,
+                     max_reps)
+    out = dict(value=reps * T / el, unit="tokens/s", cores=threads, kind="oracle",
+               seconds=round(el, 3), runs=reps, cpu_model=_cpu_model(), nproc=os.cpu_count(),
+               affinity=len(os.sched_getaffinity(0)), threads=threads,
+               sample="%d runs of the full T=%d decode batch: routing + SwiGLU forward over its %d kept "
+                      "pairs on the d=4096/ffn=14336/E=8 layer (random codes of the same shapes), "
+                      "%d OpenMP threads" % (reps, T, int(rt["counts"].sum()), threads))
+    # one thread, 4 tokens of the same batch
+    if _omp_set_threads(1):
+        toks = list(range(4))
+        el1, r1 = timed(lambda: oracle.moe_forward(x, rt, logical, G, tokens=toks), 2.0, 5)
+        out["single_thread"] = dict(value=round(r1 * len(toks) / el1, 3), unit="tokens/s", threads=1,
+                                    seconds=round(el1, 3), sample="%d runs of 4 tokens of the T=%d decode batch"
+                                    % (r1, T))
+        _omp_set_threads(threads)
+    # prefill slice: the first 256 tokens of the 4096-token batch at tau = 0
+    c3 = synthetic.config(3)
+    lg3, imp3, x3 = synthetic.logits(3, 4096), synthetic.important_mask(3, 4096), synthetic.activations(3, 4096)
+    rt3 = oracle.route(lg3, imp3, c3["k"], 0.0)
+    toks3 = list(range(256))
+    el3, r3 = timed(lambda: oracle.moe_forward(x3, rt3, logical, G, tokens=toks3), 0.0, 1)
+    out["prefill_slice"] = dict(value=round(256 * r3 / el3, 3), unit="tokens/s", threads=threads,
+                                seconds=round(el3, 3), sample="the first 256 tokens (%d kept pairs) of the "
+                                "T=4096 Mixtral-shaped prefill batch, tau = 0"
+                                % int(rt3["kept"][:256].sum()))
+    # stack slice: one layer at T = 1 and T = 64
+    c5 = synthetic.config(5)
+    st = {}
+    for T5 in (1, 64):
+        lg5 = synthetic.stack_logits(5, 0, T5)
+        mk5 = synthetic.stack_mask(5, 0, T5)
+        x5 = synthetic.activations(5, T5)
+        rt5 = oracle.route(lg5, mk5, c5["k"], c5["tau"][0])
+        el5, r5 = timed(lambda: oracle.moe_forward(x5, rt5, logical, G), 1.0, 10)
+        st["T%d" % T5] = dict(layer_tokens_per_s=round(T5 * r5 / el5, 3),
+                              stack_tokens_per_s=round(T5 * r5 / el5 / c5["layers"], 4),
+                              seconds=round(el5, 3), runs=r5)
+    out["stack_layer_slice"] = dict(st, threads=threads, sample="layer 0 of the 32-layer stack (routing "
+                                    "from that layer's logits, expert forward; no RMSNorm/residual), "
+                                    "stack rate = layer rate / 32")
+    return out
 
 
 def measure_step(mc, torch, wl, steps, warmup):
@@ -421,14 +496,16 @@ def gptq_entry(mc, torch, synthetic):
     return dict(workload="mixtral_8x7b_expert_gptq", group=128, runs=runs)
 
 
-def stack_entry(mc, torch, synthetic, steps, warmup):
+def stack_entry(mc, torch, synthetic, steps, warmup, graph=True):
     """The 32-layer Mixtral-shaped expert stack resident in HBM: 32 packed
     layers (widths [3,3,3,2,2,2,2,3] in a seeded order per layer, weights
     N(0, 0.02^2) drawn on the device with a seeded torch generator), each
     layer routed from its own logits (N(0,1) + per-layer expert bias
     N(0, 0.5^2)) with 10 % protected tokens and tau = 0.3, each behind an
     RMSNorm and joined by residual connections (no attention).  One step =
-    one mc_moe_stack_forward over all 32 layers.  Algorithmic bytes: packed
+    one mc_moe_stack_forward over all 32 layers; decode batches are also
+    captured whole (all 32 layers, one HIP graph) and the replays timed
+    (ms_per_step_graph).  Algorithmic bytes: packed
     bytes of every expert a layer routes at least one token to, plus per layer
     the bf16 activations read (norm input, expert input, residual) and written
     (normalised input, output) and the logits."""
@@ -477,8 +554,25 @@ def stack_entry(mc, torch, synthetic, steps, warmup):
         ev1.record()
         torch.cuda.synchronize()
         ms = ev0.elapsed_time(ev1) / steps
+        ms_graph = None
+        if graph and T <= 64:
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                run()
+            for _ in range(warmup):
+                gr.replay()
+            torch.cuda.synchronize()
+            ev0.record()
+            for _ in range(steps):
+                gr.replay()
+            ev1.record()
+            torch.cuda.synchronize()
+            ms_graph = ev0.elapsed_time(ev1) / steps
+            del gr
         flops = 6 * d * ffn * kept
         runs.append(dict(tokens=T, path="decode" if T <= 64 else "prefill", ms_per_step=round(ms, 4),
+                         ms_per_step_graph=ms_graph and round(ms_graph, 4),
+                         tokens_per_s_graph=ms_graph and round(T / (ms_graph / 1e3), 1),
                          tokens_per_s=round(T / (ms / 1e3), 1),
                          alg_bytes=wbytes + act, hbm_gbs=round((wbytes + act) / (ms * 1e6), 1),
                          hbm_frac=round((wbytes + act) / (ms * 1e6) / HBM_PEAK_GBS, 4),
@@ -525,7 +619,7 @@ def main():
         wl.set_tokens(mc, torch, synthetic, T)
         ms, wall = time_steps(mc, torch, wl, args.steps, args.warmup)
         ms_graph = None
-        if args.graph:
+        if not args.no_graph:
             ms_graph, _ = time_steps(mc, torch, wl, args.steps, args.warmup, capture_steps(mc, torch, wl))
         kt = kernel_times(mc, torch, wl, args.steps)
         ab = wl.alg_bytes()
@@ -544,7 +638,8 @@ def main():
                               gateup_hbm_frac=round(m["alg"]["gateup"] / (m["kernels"]["gateup"]["avg_us"] * 1e3) / HBM_PEAK_GBS, 4),
                               experts_touched=len(m["touched"])))
     main_m = measure(args.tokens)
-    ms = main_m["ms"]
+    ms_eager = main_m["ms"]
+    ms = ms_eager                 # the headline: eager launches (graph replays are reported beside them)
     T = args.tokens
     kt = main_m["kernels"]
     ab = main_m["alg"]
@@ -563,7 +658,12 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms, 5),
         "ms_per_step_graph": main_m["ms_graph"] and round(main_m["ms_graph"], 5),
-        "timing": "eager launches of route_and_prune + moe_forward per step, HIP events",
+        "ms_per_step_eager": round(ms_eager, 5),
+        "timing": "eager launches of route_and_prune + moe_forward per step, HIP events around the timed "
+                  "steps; ms_per_step_graph: the same steps as HIP-graph replays (one graph per layer copy)",
+        "kernel_timing": "kernels_us: HIP events around each kernel on its stream in a separate eager pass "
+                         "(each figure carries the events' own overhead, about 1-3 us); the roofline's "
+                         "avg_launch_us is the gate/up kernel's",
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -609,7 +709,7 @@ def main():
     if not args.no_router:
         out["router"] = router_entry(mc, torch, synthetic, 50, 5)
     if not args.no_stack:
-        out["stack"] = stack_entry(mc, torch, synthetic, args.stack_steps, 2)
+        out["stack"] = stack_entry(mc, torch, synthetic, args.stack_steps, 2, graph=not args.no_graph)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(synthetic, T)
     print(json.dumps(out), flush=True)
