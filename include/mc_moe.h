@@ -20,6 +20,9 @@
  *   mc_odp_threshold, mc_pmq_significance, mc_pmq_allocate
  *                      host helpers: the pruning threshold, expert
  *                      significance and the Eq. 4 width allocation
+ *   mc_pmq_error_workspace, mc_pmq_expert_error
+ *                      the per-expert, per-width reconstruction error the
+ *                      Eq. 4 allocation takes, on the device
  *
  * Conventions for every call
  *   - Pointers are DEVICE pointers unless the comment says "host".
@@ -347,6 +350,28 @@ mc_status mc_pmq_significance(const float *logits_host, int T, int E, int k, dou
  * non-finite inputs, alpha or beta < 0, gamma <= 0). */
 mc_status mc_pmq_allocate(const double *phi, const double *w, const double *eps, int E, double alpha,
                           double beta, double gamma, int total_bits, int *bits, double *objective);
+
+/* The reconstruction error that Eq. 4 takes (Sec. 3.2.2, the equation
+ * before Eq. 4), measured on one MoE layer and a calibration batch:
+ *   eps[e][b-1] = || F(theta) - F(theta[e -> Q(e, b)]) ||_F,   b = 1, 2, 3,
+ * F the layer output of Eq. 1 over the batch's T tokens (routing r, the
+ * weights theta: w_gate, w_up [E][ffn][d], w_down [E][d][ffn], fp32, DEVICE),
+ * Q(e, b) expert e alone quantized at b bits by mc_pack's min-max RTN
+ * quantizer (group size `group`).  Since only the tokens that keep e change,
+ * eps[e][b-1]^2 = sum over e's kept pairs of ||w_r (E_e^(b)(x_t) - E_e(x_t))||^2:
+ * E_e(x_t) from fp32 weights in fp32 arithmetic (h = silu(g) * u unrounded),
+ * E_e^(b)(x_t) from the packed forward's own kernels.  x_bf16 [T][d] DEVICE;
+ * r: the batch's routing from mc_route_and_prune (the paper measures the
+ * unpruned model: threshold 0); eps_host: HOST [E][3] output.  Workspace
+ * (DEVICE) of mc_pmq_error_workspace bytes: the layer packed at each width in
+ * turn, the forward's buffers and the dense outputs.  Offline call: it waits
+ * for the stream before returning.  Errors: MC_EINVAL (shapes as mc_pack and
+ * mc_moe_forward, NULL pointers, routing of another E), MC_ENOSPACE (short
+ * workspace), MC_EUNSUPPORTED, MC_EHIP. */
+mc_status mc_pmq_error_workspace(int T, int E, int k, int d, int ffn, int group, size_t *bytes);
+mc_status mc_pmq_expert_error(const float *w_gate, const float *w_up, const float *w_down, int E, int d,
+                              int ffn, int group, const uint16_t *x_bf16, const mc_routing *r,
+                              double *eps_host, void *workspace, size_t ws_bytes, void *stream);
 
 /* Instrumentation.  mc_timing_enable(1) clears the record and brackets every
  * kernel launch made afterwards by two HIP events on the launch stream;

@@ -30,7 +30,10 @@ What it computes (Mixture Compressor for MoE LLMs, ICLR 2025):
   and the protected set (the top floor(rho*L + 1/2) tokens);
 * ``median_ratio``  -- the pruning threshold mu as the median of w1/w0;
 * ``pmq_significance`` / ``pmq_allocate`` -- Sec. 3.2: expert access
-  frequency and mean routing weight, and the Eq. 4 width allocation.
+  frequency and mean routing weight, and the Eq. 4 width allocation;
+* ``pmq_expert_error`` -- Sec. 3.2.2: the F-norm change of one MoE layer's
+  output when only expert e is quantized at b bits (the errors Eq. 4 takes),
+  with ``dense_expert_forward`` the unquantized SwiGLU expert.
 
 Everything floating point is fp64 except operations whose precision the
 definition fixes (fp32 scale/zero arithmetic, the fp32 k = 2 logit gap).
@@ -77,6 +80,10 @@ PINS = {
     "pmq_significance": "hand example (golden); sum phi = k and sum w = 1; tie order",
     "pmq_allocate": "hand-enumerated example (golden); enumeration of every width vector; "
                     "constraints; significance ordering",
+    "dense_expert_forward": "one hand-computed token (closed-form silu); linearity of the down projection",
+    "pmq_expert_error": "the definition taken literally (two whole-layer outputs, one with only expert e "
+                        "quantized); zero for an expert no token keeps; zero at 1 bit for weights on "
+                        "the 1-bit grid; equal to the per-token brute-force sum",
 }
 
 
@@ -631,6 +638,44 @@ def pmq_allocate(phi, w, eps, total_bits: int, alpha=1.0, beta=1.0, gamma=2.0):
 
 
 # ------------------------------------------------------------- importance ---
+
+def dense_expert_forward(X: np.ndarray, Wg: np.ndarray, Wu: np.ndarray, Wd: np.ndarray) -> np.ndarray:
+    """The SwiGLU expert with unquantized weights, fp64: rows of X [n][d] ->
+    Wd (silu(Wg x) * (Wu x)); Wg, Wu [ffn][d], Wd [d][ffn]."""
+    X = np.asarray(X, dtype=np.float64)
+    g = X @ np.asarray(Wg, dtype=np.float64).T
+    u = X @ np.asarray(Wu, dtype=np.float64).T
+    h = g / (1.0 + np.exp(-g)) * u
+    return h @ np.asarray(Wd, dtype=np.float64).T
+
+
+def pmq_expert_error(Wg, Wu, Wd, x_bf16: np.ndarray, routing, G: int) -> np.ndarray:
+    """Sec. 3.2.2: eps[e][b-1] = ||F(theta) - F(theta[e -> Q(e, b)])||_F for
+    b = 1, 2, 3, F the MoE layer output (Eq. 1) over the batch, theta the
+    fp32 weights Wg, Wu [E][ffn][d], Wd [E][d][ffn], Q the Sec. 3.1 quantizer
+    (``quantize``) at b bits, group size G.  Only the tokens that keep e see
+    the change, by w_r (E_e^(b)(x_t) - E_e(x_t)) each, so eps[e][b-1]^2 sums
+    the squared norms of those terms; the quantized expert runs on its exact
+    dequantized weights (``expert_forward``)."""
+    X = bf16_to_float64(x_bf16)
+    E = len(Wg)
+    k = routing["topk_idx"].shape[1]
+    T = X.shape[0]
+    eps = np.zeros((E, 3), np.float64)
+    for e in range(E):
+        sel = [(t, r) for t in range(T) for r in range(k)
+               if routing["topk_idx"][t, r] == e and routing["kept"][t, r]]
+        if not sel:
+            continue
+        Xe = X[[t for t, _ in sel]]
+        w = np.array([routing["topk_w"][t, r] for t, r in sel], np.float64)
+        Y = dense_expert_forward(Xe, Wg[e], Wu[e], Wd[e])
+        for b in (1, 2, 3):
+            logical_e = [quantize(np.asarray(W[e], np.float32), b, G) for W in (Wg, Wu, Wd)]
+            _, Yq = expert_forward(Xe, logical_e, G)
+            eps[e, b - 1] = math.sqrt(float((((Yq - Y) * w[:, None]) ** 2).sum()))
+    return eps
+
 
 def protect_count(L: int, rho: float) -> int:
     """Tokens protected out of L at fraction rho: floor(rho * L + 1/2)."""

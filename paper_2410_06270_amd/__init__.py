@@ -27,6 +27,8 @@ from ._binding import (  # noqa: F401
     pack,
     pack_sizes,
     pmq_allocate,
+    pmq_error_workspace,
+    pmq_expert_error,
     pmq_significance,
     route_and_prune,
     route_forward,

@@ -107,6 +107,10 @@ def load():
         lib.mc_pmq_significance.argtypes = [P, I, I, I, P, P]
         lib.mc_pmq_allocate.restype = st
         lib.mc_pmq_allocate.argtypes = [P, P, P, I, D, D, D, I, P, ctypes.POINTER(D)]
+        lib.mc_pmq_error_workspace.restype = st
+        lib.mc_pmq_error_workspace.argtypes = [I, I, I, I, I, I, ctypes.POINTER(S)]
+        lib.mc_pmq_expert_error.restype = st
+        lib.mc_pmq_expert_error.argtypes = [P, P, P, I, I, I, I, P, ctypes.POINTER(_Routing), P, P, S, P]
         lib.mc_timing_enable.restype = st
         lib.mc_timing_enable.argtypes = [I]
         lib.mc_timing_read.restype = st
@@ -363,6 +367,29 @@ def pmq_allocate(phi, w, eps, total_bits: int, alpha: float = 1.0, beta: float =
                                   float(gamma), int(total_bits), bits.ctypes.data_as(ctypes.c_void_p),
                                   ctypes.byref(obj)))
     return [int(b) for b in bits], obj.value
+
+
+def pmq_error_workspace(T: int, E: int, k: int, d: int, ffn: int, group: int) -> int:
+    b = ctypes.c_size_t()
+    _check(load().mc_pmq_error_workspace(T, E, k, d, ffn, group, ctypes.byref(b)))
+    return b.value
+
+
+def pmq_expert_error(w_gate, w_up, w_down, x, routing: Routing, group: int, workspace, stream=None):
+    """eps [E][3] (numpy fp64): the reconstruction error of each expert at 1,
+    2 and 3 bits on the calibration batch x [T][d] (bf16 or int16 bits) routed
+    by ``routing``; fp32 device weights as for pack()."""
+    import numpy as np
+    for t in (w_gate, w_up, w_down):
+        assert t.dtype == torch.float32 and t.is_contiguous() and t.is_cuda
+    assert x.is_contiguous() and x.element_size() == 2 and workspace.is_contiguous()
+    E, ffn, d = w_gate.shape
+    eps = np.empty((E, 3), np.float64)
+    _check(load().mc_pmq_expert_error(_ptr(w_gate), _ptr(w_up), _ptr(w_down), E, d, ffn, int(group), _ptr(x),
+                                      ctypes.byref(routing.desc), eps.ctypes.data_as(ctypes.c_void_p),
+                                      _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                      _stream(stream)))
+    return eps
 
 
 def timing_enable(on: bool = True):

@@ -122,6 +122,32 @@ mc_status check_routing(const mc_routing* r) {
 
 }  // namespace
 
+namespace {
+
+size_t up256(size_t b) { return (b + 255) / 256 * 256; }
+
+// Workspace of mc_pmq_expert_error: the layer packed at 3 bits (the widest),
+// its scale/zero words, the forward's workspace, the dense h [P][ffn] and
+// y [P][d] (fp32) and eps [E][3] (fp64).
+struct PmqLayout {
+  size_t words, sz, fws, h, y, eps, total;
+};
+
+PmqLayout pmq_layout(int T, int E, int k, int d, int ffn, int G) {
+  PmqLayout o;
+  const size_t P = (size_t)T * k;
+  o.words = 0;
+  o.sz = o.words + up256(3 * (size_t)E * d * ffn * 3 / 8);
+  o.fws = o.sz + up256(3 * (size_t)E * d * ffn / G * 4);
+  o.h = o.fws + up256(mc::forward_workspace_bytes(T, E, k, d, ffn));
+  o.y = o.h + up256(P * ffn * sizeof(float));
+  o.eps = o.y + up256(P * d * sizeof(float));
+  o.total = o.eps + up256((size_t)E * 3 * sizeof(double));
+  return o;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* mc_last_error(void) { return g_err; }
@@ -367,6 +393,71 @@ mc_status mc_moe_route_forward(const uint16_t* x_bf16, const float* logits, cons
   return hip_status(mc::launch_forward(x_bf16, layer_args(L), *r, y_bf16, workspace, nullptr,
                                        static_cast<hipStream_t>(stream), &ra),
                     "mc_moe_route_forward launch");
+}
+
+// -------------------------------------------------- PMQ reconstruction error --
+
+mc_status mc_pmq_error_workspace(int T, int E, int k, int d, int ffn, int group, size_t* bytes) {
+  mc_status s = mc_forward_workspace(T, E, k, d, ffn, bytes);
+  if (s != MC_OK) return s;
+  std::vector<int> three(E, 3);
+  s = check_shape(E, d, ffn, three.data(), group);
+  if (s != MC_OK) return s;
+  *bytes = pmq_layout(T, E, k, d, ffn, group).total;
+  return MC_OK;
+}
+
+mc_status mc_pmq_expert_error(const float* w_gate, const float* w_up, const float* w_down, int E, int d, int ffn,
+                              int group, const uint16_t* x_bf16, const mc_routing* r, double* eps_host,
+                              void* workspace, size_t ws_bytes, void* stream) {
+  mc_status s = check_routing(r);
+  if (s != MC_OK) return s;
+  if (r->E != E) return fail(MC_EINVAL, "routing has E=%d, the weights E=%d", r->E, E);
+  size_t need = 0;
+  s = mc_pmq_error_workspace(r->T, E, r->k, d, ffn, group, &need);
+  if (s != MC_OK) return s;
+  if (!w_gate || !w_up || !w_down || !x_bf16 || !eps_host || !workspace)
+    return fail(MC_EINVAL, "weight, x, eps or workspace pointer is NULL");
+  if (ws_bytes < need) return fail(MC_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+  const PmqLayout o = pmq_layout(r->T, E, r->k, d, ffn, group);
+  char* ws = static_cast<char*>(workspace);
+  float* h = reinterpret_cast<float*>(ws + o.h);
+  float* y = reinterpret_cast<float*>(ws + o.y);
+  double* eps = reinterpret_cast<double*>(ws + o.eps);
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  s = hip_status(mc::launch_dense_expert(w_gate, w_up, w_down, E, d, ffn, x_bf16, *r, h, y, st),
+                 "mc_pmq_expert_error dense launch");
+  if (s != MC_OK) return s;
+  for (int b = 1; b <= 3; ++b) {
+    std::vector<int> bits(E, b);
+    mc_layer L;
+    L.E = E;
+    L.d = d;
+    L.ffn = ffn;
+    L.group = group;
+    L.bits_host = bits.data();
+    L.words = ws + o.words;
+    L.sz = reinterpret_cast<uint32_t*>(ws + o.sz);
+    sizes(E, d, ffn, bits.data(), group, &L.words_bytes, &L.sz_bytes);
+    const mc::LayerArgs a = layer_args(&L);
+    s = hip_status(mc::launch_pack(w_gate, w_up, w_down, a, static_cast<uint32_t*>(L.words), L.sz, false, st),
+                   "mc_pmq_expert_error pack launch");
+    if (s != MC_OK) return s;
+    float* partial = nullptr;
+    size_t part_stride = 0;
+    int nsplit = 1;
+    s = hip_status(mc::launch_expert_partials(x_bf16, a, *r, ws + o.fws, &partial, &part_stride, &nsplit, st),
+                   "mc_pmq_expert_error forward launch");
+    if (s != MC_OK) return s;
+    s = hip_status(mc::launch_pmq_error(partial, part_stride, nsplit, y, *r, d, b, eps, st),
+                   "mc_pmq_expert_error error launch");
+    if (s != MC_OK) return s;
+  }
+  s = hip_status(hipMemcpyAsync(eps_host, eps, (size_t)E * 3 * sizeof(double), hipMemcpyDeviceToHost, st),
+                 "mc_pmq_expert_error copy");
+  if (s != MC_OK) return s;
+  return hip_status(hipStreamSynchronize(st), "mc_pmq_expert_error synchronize");
 }
 
 mc_status mc_stack_workspace(int T, int E, int k, int d, int ffn, size_t* bytes) {

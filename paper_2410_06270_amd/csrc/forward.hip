@@ -236,22 +236,11 @@ static hipError_t launch_combine(const float* partial, size_t part_stride, int n
   return hipGetLastError();
 }
 
-hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
-                          void* ws, const uint16_t* residual, hipStream_t stream, const RouteArgs* route,
-                          uint16_t* xn_next) {
+hipError_t launch_expert_partials(const uint16_t* x, const LayerArgs& L, const mc_routing& r, void* ws,
+                                  float** partial_out, size_t* part_stride_out, int* nsplit_out,
+                                  hipStream_t stream) {
   const int T = r.T, k = r.k;
-  if (route) {
-    const hipError_t err = launch_route(route->logits, route->important, route->delta32, route->tau, r, stream);
-    if (err != hipSuccess) return err;
-  }
-  if (T > kDecodeMaxT) {
-    float* partial = nullptr;
-    size_t part_stride = 0;
-    int nsplit = 1;
-    const hipError_t err = launch_prefill(x, L, r, ws, &partial, &part_stride, &nsplit, stream);
-    if (err != hipSuccess) return err;
-    return launch_combine(partial, part_stride, nsplit, r, L.d, residual, y, xn_next, stream);
-  }
+  if (T > kDecodeMaxT) return launch_prefill(x, L, r, ws, partial_out, part_stride_out, nsplit_out, stream);
   const size_t P = (size_t)T * k;
   DecodeArgs a;
   a.x = x;
@@ -270,6 +259,9 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
   if (s_gu > 1) p += round256((size_t)s_gu * 2 * P * L.ffn * sizeof(float));
   float* partial = reinterpret_cast<float*>(p);
   const size_t part_stride = P * L.d;
+  *partial_out = partial;
+  *part_stride_out = part_stride;
+  *nsplit_out = nsplit;
 
   a.h = nullptr;
   a.gu_in = nullptr;
@@ -302,6 +294,20 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
   else if (L.G == 64) err = launch_decode<2, false>(L, a, stream);
   else err = launch_decode<4, false>(L, a, stream);
   timing_end(stream, kSiteDown);
+  return err;
+}
+
+hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routing& r, uint16_t* y,
+                          void* ws, const uint16_t* residual, hipStream_t stream, const RouteArgs* route,
+                          uint16_t* xn_next) {
+  if (route) {
+    const hipError_t err = launch_route(route->logits, route->important, route->delta32, route->tau, r, stream);
+    if (err != hipSuccess) return err;
+  }
+  float* partial = nullptr;
+  size_t part_stride = 0;
+  int nsplit = 1;
+  const hipError_t err = launch_expert_partials(x, L, r, ws, &partial, &part_stride, &nsplit, stream);
   if (err != hipSuccess) return err;
   return launch_combine(partial, part_stride, nsplit, r, L.d, residual, y, xn_next, stream);
 }

@@ -49,6 +49,18 @@ struct RouteArgs {
   float delta32;             // fp32 logit-gap threshold (k = 2)
   double tau;                // normalised-weight threshold (k > 2)
 };
+// The expert outputs of every kept pair, unweighted and split over the
+// reduction: partial[s][pos][0..d) for s < nsplit, pos the pair's CSR
+// position (the forward's workspace holds them; launch_forward combines them).
+hipError_t launch_expert_partials(const uint16_t* x, const LayerArgs& L, const mc_routing& r, void* ws,
+                                  float** partial, size_t* part_stride, int* nsplit, hipStream_t stream);
+// The reconstruction error of Sec. 3.2.2 (pmq.hip): the dense fp32 expert
+// outputs of every kept pair (h [P][ffn], y [P][d], fp32 weights [E][N][K]),
+// and eps[e][b-1] from the packed forward's per-pair partials against them.
+hipError_t launch_dense_expert(const float* wg, const float* wu, const float* wd, int E, int d, int ffn,
+                               const uint16_t* x, const mc_routing& r, float* h, float* y, hipStream_t stream);
+hipError_t launch_pmq_error(const float* partial, size_t part_stride, int nsplit, const float* dense,
+                            const mc_routing& r, int d, int b, double* eps, hipStream_t stream);
 // residual (may be null): y = bf16(residual + sum_r w_r E_{e_r}(x)).
 // route (may be null): route the batch first (the routing kernels).
 // xn_next (may be null): also write RMSNorm(y) there, the next stack layer's
