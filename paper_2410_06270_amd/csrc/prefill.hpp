@@ -175,48 +175,66 @@ __device__ __forceinline__ void pf_stage(unsigned char* stage, const PrefillGemm
             stage + S::kFragBytes + half * 1024);
 }
 
-// Group epilogue: tot += s 2^b * (acc - (1 + z 2^-b) * S_g); per lane its
-// row's s and z (word sw), S_g of the tile rows from the stage.
-template <int BITS, int GPC>
-__device__ __forceinline__ void pf_epilogue(const f32x16 (&acc)[PfCfg::kTiles], uint32_t sw,
-                                            const unsigned char* stage, int q, int lane,
-                                            f32x16 (&tot)[PfCfg::kTiles]) {
+// S_g of group q for the rows this lane's accumulators hold, from the stage:
+// sx[t][k4][r] is row 8*k4 + 4*(lane/32) + r of fragment row t.
+template <int GPC>
+__device__ __forceinline__ void pf_sums(const unsigned char* stage, int q, int lane,
+                                        f32x4 (&sx)[PfCfg::kTiles][4]) {
   const float* ssum = reinterpret_cast<const float*>(stage + PfCfg::kFragBytes);
-  const float sj = half_bits_to_float(sw & 0xffffu) * (float)(1 << BITS);
-  const float cj = fmaf(half_bits_to_float(sw >> 16), 1.0f / (float)(1 << BITS), 1.0f);
 #pragma unroll
   for (int t = 0; t < PfCfg::kTiles; ++t) {
     const float* sr = ssum + (t * GPC + q) * 32 + 4 * (lane >> 5);
-    f32x4 sx[4];
 #pragma unroll
-    for (int k4 = 0; k4 < 4; ++k4) sx[k4] = *reinterpret_cast<const f32x4*>(sr + 8 * k4);
+    for (int k4 = 0; k4 < 4; ++k4) sx[t][k4] = *reinterpret_cast<const f32x4*>(sr + 8 * k4);
+  }
+}
+
+// Group epilogue: tot += s 2^b * (acc - (1 + z 2^-b) * S_g); per lane its
+// row's s and z (word sw), S_g of the tile rows read beforehand (pf_sums).
+template <int BITS>
+__device__ __forceinline__ void pf_epilogue(const f32x16 (&acc)[PfCfg::kTiles], uint32_t sw,
+                                            const f32x4 (&sx)[PfCfg::kTiles][4], f32x16 (&tot)[PfCfg::kTiles]) {
+  const float sj = half_bits_to_float(sw & 0xffffu) * (float)(1 << BITS);
+  const float cj = fmaf(half_bits_to_float(sw >> 16), 1.0f / (float)(1 << BITS), 1.0f);
+#pragma unroll
+  for (int t = 0; t < PfCfg::kTiles; ++t)
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const float u = fmaf(-cj, sx[i >> 2][i & 3], acc[t][i]);
+      const float u = fmaf(-cj, sx[t][i >> 2][i & 3], acc[t][i]);
       tot[t][i] = fmaf(sj, u, tot[t][i]);
     }
-  }
 }
 
 // MFMAs of group q of the chunk in `stage` with the words `w`: per step the
 // eight codes of this lane's row feed the MFMAs of all kTiles fragment rows.
+// The A fragments of step v+1 are read while the MFMAs of step v run.
 template <int BITS, int GPC, bool BF16>
 __device__ __forceinline__ void pf_group(const unsigned char* stage, const uint32_t (&w)[2][BITS], int q, int lane,
                                          uint32_t magic, f32x16 (&acc)[PfCfg::kTiles]) {
   constexpr int KV = 8 / GPC;   // MFMA steps per group
   const unsigned char* arow = stage + lane * 16;
+  u32x4 a[2][PfCfg::kTiles];
+#pragma unroll
+  for (int t = 0; t < PfCfg::kTiles; ++t) a[0][t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + q * KV) * kPfFragBytes);
 #pragma unroll
   for (int vv = 0; vv < KV; ++vv) {
     const int v = q * KV + vv;
-    u32x4 a[PfCfg::kTiles];
+    if (vv + 1 < KV) {
 #pragma unroll
-    for (int t = 0; t < PfCfg::kTiles; ++t) a[t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + v) * kPfFragBytes);
+      for (int t = 0; t < PfCfg::kTiles; ++t)
+        a[(vv + 1) & 1][t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + v + 1) * kPfFragBytes);
+    }
     const u32x4 b = pf_codes<BITS, BF16>(w[v & 1], v >> 1, magic);
 #pragma unroll
     for (int t = 0; t < PfCfg::kTiles; ++t) {
       const f32x16 z = {};
-      acc[t] = pf_mfma<BF16>(a[t], b, vv == 0 ? z : acc[t]);
+      acc[t] = pf_mfma<BF16>(a[vv & 1][t], b, vv == 0 ? z : acc[t]);
     }
+    // one step per scheduling region: left free, the scheduler ran each
+    // fragment row's eight dependent MFMAs back to back, each behind its own
+    // LDS read, instead of the four independent MFMAs of a step
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -229,14 +247,22 @@ __device__ __forceinline__ void pf_chunk_body(const unsigned char* __restrict__ 
                                               const uint32_t (&s)[GPC], uint32_t (&nw)[2][BITS],
                                               uint32_t (&ns)[GPC], uint32_t& ps, uint32_t magic,
                                               f32x16 (&acc)[PfCfg::kTiles], f32x16 (&tot)[PfCfg::kTiles]) {
-  if (late && !first) pf_epilogue<BITS, GPC>(acc, ps, prev, GPC - 1, lane, tot);
+  f32x4 sx[PfCfg::kTiles][4];
+  if (late && !first) {
+    pf_sums<GPC>(prev, GPC - 1, lane, sx);
+    pf_epilogue<BITS>(acc, ps, sx, tot);
+  }
   pf_load<BITS, GPC>(nw, ns, sp, c + 1 < last ? c + 1 : last);
   __builtin_amdgcn_sched_barrier(0);   // the words go out before the stage (counted waits)
   pf_stage<GPC>(next, g, f0, c + 2 < last ? c + 2 : last, wave, lane);
 #pragma unroll
   for (int q = 0; q < GPC; ++q) {
+    const bool epi = q < GPC - 1 || !late;
     pf_group<BITS, GPC, BF16>(cur, w, q, lane, magic, acc);
-    if (q < GPC - 1 || !late) pf_epilogue<BITS, GPC>(acc, s[q], cur, q, lane, tot);
+    if (epi) {
+      pf_sums<GPC>(cur, q, lane, sx);
+      pf_epilogue<BITS>(acc, s[q], sx, tot);
+    }
     else ps = s[q];
   }
 }
@@ -298,8 +324,11 @@ __device__ __forceinline__ void pf_loop(const PfStream& sp, const PrefillGemm& g
   }
   // the late waves' last epilogue: the last chunk's stage is the slot before `slot`
   if (late)
-    pf_epilogue<BITS, GPC>(acc, ps, smem + (slot == 0 ? kPfSlots - 1 : slot - 1) * S::kStageBytes, GPC - 1, lane,
-                           tot);
+  {
+    f32x4 sx[S::kTiles][4];
+    pf_sums<GPC>(smem + (slot == 0 ? kPfSlots - 1 : slot - 1) * S::kStageBytes, GPC - 1, lane, sx);
+    pf_epilogue<BITS>(acc, ps, sx, tot);
+  }
   wait_vmcnt<0>();   // the clamped re-reads of the last chunks land before LDS is reused
 }
 
