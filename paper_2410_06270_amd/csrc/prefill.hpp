@@ -59,8 +59,8 @@ struct PfCfg {
   static_assert(kTiles * 4 * 32 * 4 <= kSumBytes, "group sums of a chunk");
   static_assert(kLdsBytes <= kLdsPerCu, "prefill stages fit the LDS of a CU");
   static_assert(kRowsGateUp % 128 == 0, "a gate/up workgroup covers whole groups of h columns");
-  static_assert(kPfWaves / 2 * kTiles * 16 * 64 * 4 + kTiles * 8 * kPfFragBytes <= kLdsBytes,
-                "the up totals and the h tile fit the ring");
+  static_assert(kPfWaves * 2 * 16 * 64 * 4 + kTiles * 8 * kPfFragBytes <= kLdsBytes,
+                "the exchanged totals and the h tile fit the ring");
 };
 
 // Expert-to-tile tables written by the set-up kernel into the workspace.
@@ -381,32 +381,40 @@ prefill_kernel(LayerArgs L, const int32_t* __restrict__ offsets, PrefillTables t
   // row m = 8*(i/4) + 4*(lane/32) + i%4 (token) of each 32x32 tile.
   const int n = lane & 31;
   if (GATEUP) {
-    // The up waves hand their totals to the gate waves of the same rows
-    // through LDS; the gate waves form h = silu(gate) * up rounded to fp16 in
-    // an LDS copy of the workgroup's h tile, laid out as in global memory (per
-    // fragment row, 8 KB: its 128 columns are 8 consecutive 1 KB fragments),
-    // which all threads then store with 16-byte writes; the group sums of the
-    // rounded h are read back from that copy, each in column order.
+    // The gate and up waves of the same rows (waves 2r, 2r+1) share the h
+    // pass: each hands the other the half of its totals the other needs
+    // (gate: fragment rows 2 and 3, up: 0 and 1) through LDS, and forms
+    // h = silu(gate) * up rounded to fp16 for its own half, into an LDS copy
+    // of the workgroup's h tile laid out as in global memory (per fragment
+    // row 8 KB: its 128 columns are 8 consecutive 1 KB fragments); all
+    // threads then store the tile with 16-byte writes, and the group sums of
+    // the rounded h are read back from it, each in column order.
     __syncthreads();                       // the ring is free
-    float* upt = reinterpret_cast<float*>(smem);                               // [rb][t][i][64 lanes]
-    unsigned char* ht = smem + kPfWaves / 2 * S::kTiles * 16 * 64 * 4;         // [t][8 fragments]
-    if (wave & 1) {
+    float* xch = reinterpret_cast<float*>(smem);                               // [wave][2 rows][i][64 lanes]
+    unsigned char* ht = smem + kPfWaves * 2 * 16 * 64 * 4;                     // [t][8 fragments]
+    const bool upw = wave & 1;
+    static_assert(S::kTiles == 4, "the h pass splits four fragment rows in halves");
 #pragma unroll
-      for (int t = 0; t < S::kTiles; ++t)
+    for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) upt[((rb * S::kTiles + t) * 16 + i) * 64 + lane] = tot[t][i];
-    }
+      for (int i = 0; i < 16; ++i) xch[((wave * 2 + tt) * 16 + i) * 64 + lane] = upw ? tot[tt][i] : tot[tt + 2][i];
     __syncthreads();
-    if (!(wave & 1)) {
+    {
       const int c = 32 * rb + n;           // column within the workgroup's 128
+      const int partner = wave ^ 1;
 #pragma unroll
-      for (int t = 0; t < S::kTiles; ++t) {
+      for (int tt = 0; tt < 2; ++tt) {
+        const int t = upw ? tt + 2 : tt;   // the fragment row this wave forms
+        if (t < nmt) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int m = 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-          const float up = upt[((rb * S::kTiles + t) * 16 + i) * 64 + lane];
-          *reinterpret_cast<uint16_t*>(ht + (size_t)t * 8 * kPfFragBytes + frag_offset(0, m, c, 128)) =
-              float_to_half_sat(silu(tot[t][i]) * up);
+          for (int i = 0; i < 16; ++i) {
+            const int m = 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+            const float other = xch[((partner * 2 + tt) * 16 + i) * 64 + lane];
+            const float mine = upw ? tot[tt + 2][i] : tot[tt][i];
+            const float gv = upw ? other : mine, uv = upw ? mine : other;
+            *reinterpret_cast<uint16_t*>(ht + (size_t)t * 8 * kPfFragBytes + frag_offset(0, m, c, 128)) =
+                float_to_half_sat(silu(gv) * uv);
+          }
         }
       }
     }
