@@ -8,9 +8,12 @@
 // The weights are never rounded.  As in the decode kernels, the codes enter
 // the MFMA as the exact values 1 + q 2^-b (code in the top b mantissa bits of
 // 1.0), and the scale and zero of each group are applied to the fp32 group sum:
-//   sum_{k in g} x_k s (q_k - z) = s 2^b * (acc_g - (1 + z 2^-b) * S_g),
-//   acc_g = sum_k x_k (1 + q_k 2^-b) (MFMA),  S_g = sum_{k in g} x_k,
-// so per group of G columns each output costs two fp32 fmas.
+//   sum_{k in g} x_k s (q_k - z) = s 2^b * acc_g - s 2^b (1 + z 2^-b) * S_g,
+//   acc_g = sum_k x_k (1 + q_k 2^-b) (MFMA),  S_g = sum_{k in g} x_k.
+// The first term costs one fp32 fma per output and group; the second, summed
+// over the groups, is a product of the token-by-group sums S_g and the
+// group-by-row coefficients, taken in fp32 on v_mfma_f32_32x32x2_f32 (two
+// groups per MFMA) into the same totals.
 //  * gate/up: x stays bf16 (exact), codes in bf16, v_mfma_f32_32x32x16_bf16;
 //  * down: h is rounded once to fp16 (the only rounding on the path besides
 //    fp32 accumulation), codes in fp16, v_mfma_f32_32x32x16_f16.
@@ -175,35 +178,61 @@ __device__ __forceinline__ void pf_stage(unsigned char* stage, const PrefillGemm
             stage + S::kFragBytes + half * 1024);
 }
 
-// S_g of group q for the rows this lane's accumulators hold, from the stage:
-// sx[t][k4][r] is row 8*k4 + 4*(lane/32) + r of fragment row t.
-template <int GPC>
-__device__ __forceinline__ void pf_sums(const unsigned char* stage, int q, int lane,
-                                        f32x4 (&sx)[PfCfg::kTiles][4]) {
-  const float* ssum = reinterpret_cast<const float*>(stage + PfCfg::kFragBytes);
-#pragma unroll
-  for (int t = 0; t < PfCfg::kTiles; ++t) {
-    const float* sr = ssum + (t * GPC + q) * 32 + 4 * (lane >> 5);
-#pragma unroll
-    for (int k4 = 0; k4 < 4; ++k4) sx[t][k4] = *reinterpret_cast<const f32x4*>(sr + 8 * k4);
-  }
-}
-
-// Group epilogue: tot += s 2^b * (acc - (1 + z 2^-b) * S_g); per lane its
-// row's s and z (word sw), S_g of the tile rows read beforehand (pf_sums).
+// Group epilogue: tot += s 2^b * acc_g (the scale of this lane's row, word
+// sw).  The zero-point part of the group's term, -(s 2^b (1 + z 2^-b)) * S_g,
+// goes to the correction (PfZero).
 template <int BITS>
 __device__ __forceinline__ void pf_epilogue(const f32x16 (&acc)[PfCfg::kTiles], uint32_t sw,
-                                            const f32x4 (&sx)[PfCfg::kTiles][4], f32x16 (&tot)[PfCfg::kTiles]) {
+                                            f32x16 (&tot)[PfCfg::kTiles]) {
   const float sj = half_bits_to_float(sw & 0xffffu) * (float)(1 << BITS);
-  const float cj = fmaf(half_bits_to_float(sw >> 16), 1.0f / (float)(1 << BITS), 1.0f);
 #pragma unroll
   for (int t = 0; t < PfCfg::kTiles; ++t)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float u = fmaf(-cj, sx[t][i >> 2][i & 3], acc[t][i]);
-      tot[t][i] = fmaf(sj, u, tot[t][i]);
-    }
+    for (int i = 0; i < 16; ++i) tot[t][i] = fmaf(sj, acc[t][i], tot[t][i]);
 }
+
+// The zero-point correction, sum over groups g of -(s_g 2^b (1 + z_g 2^-b))
+// * S_g (S_g the group sum of a token row), as a product [tokens x groups] .
+// [groups x weight rows] on v_mfma_f32_32x32x2_f32, two groups per MFMA: the
+// lanes of half h hold group g of each pair with g % 2 == h (A: S_g of token
+// lane % 32 per fragment row; B: the coefficient of weight row lane % 32).
+// Groups are numbered from the first of the loop's range; take() records one
+// group's operands from the stage and its scale/zero word, and after each
+// odd-numbered group the pair's four MFMAs add into tot.
+struct PfZero {
+  float a[PfCfg::kTiles];
+  float b;
+  template <int BITS, int GPC>
+  __device__ __forceinline__ void take(const unsigned char* stage, int q, uint32_t sw, int rel, int lane,
+                                       f32x16 (&tot)[PfCfg::kTiles]) {
+    const bool mine = (rel & 1) == (lane >> 5);
+    const float* ssum = reinterpret_cast<const float*>(stage + PfCfg::kFragBytes);
+    const float sj = half_bits_to_float(sw & 0xffffu) * (float)(1 << BITS);
+    const float cj = fmaf(half_bits_to_float(sw >> 16), 1.0f / (float)(1 << BITS), 1.0f);
+#pragma unroll
+    for (int t = 0; t < PfCfg::kTiles; ++t) {
+      const float v = ssum[(t * GPC + q) * 32 + (lane & 31)];
+      a[t] = mine ? v : a[t];
+    }
+    b = mine ? -(sj * cj) : b;
+    if (rel & 1) flush(tot);
+  }
+  __device__ __forceinline__ void flush(f32x16 (&tot)[PfCfg::kTiles]) {
+#pragma unroll
+    for (int t = 0; t < PfCfg::kTiles; ++t) tot[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[t], b, tot[t], 0, 0, 0);
+  }
+  // an odd number of groups leaves half a pair: its other half is zero
+  __device__ __forceinline__ void finish(int ngroups, int lane, f32x16 (&tot)[PfCfg::kTiles]) {
+    if (ngroups & 1) {
+      if (lane >> 5) {
+#pragma unroll
+        for (int t = 0; t < PfCfg::kTiles; ++t) a[t] = 0.0f;
+        b = 0.0f;
+      }
+      flush(tot);
+    }
+  }
+};
 
 // MFMAs of group q of the chunk in `stage` with the words `w`: per step the
 // eight codes of this lane's row feed the MFMAs of all kTiles fragment rows.
@@ -240,30 +269,22 @@ __device__ __forceinline__ void pf_group(const unsigned char* stage, const uint3
 
 template <int BITS, int GPC, bool BF16>
 __device__ __forceinline__ void pf_chunk_body(const unsigned char* __restrict__ cur,
-                                              const unsigned char* __restrict__ prev,
                                               unsigned char* __restrict__ next, const PfStream& sp,
                                               const PrefillGemm& g, int f0, bool late, bool first, int c, int last,
-                                              int wave, int lane, const uint32_t (&w)[2][BITS],
+                                              int rel0, int wave, int lane, const uint32_t (&w)[2][BITS],
                                               const uint32_t (&s)[GPC], uint32_t (&nw)[2][BITS],
-                                              uint32_t (&ns)[GPC], uint32_t& ps, uint32_t magic,
+                                              uint32_t (&ns)[GPC], uint32_t& ps, uint32_t magic, PfZero& zc,
                                               f32x16 (&acc)[PfCfg::kTiles], f32x16 (&tot)[PfCfg::kTiles]) {
-  f32x4 sx[PfCfg::kTiles][4];
-  if (late && !first) {
-    pf_sums<GPC>(prev, GPC - 1, lane, sx);
-    pf_epilogue<BITS>(acc, ps, sx, tot);
-  }
+  if (late && !first) pf_epilogue<BITS>(acc, ps, tot);
   pf_load<BITS, GPC>(nw, ns, sp, c + 1 < last ? c + 1 : last);
   __builtin_amdgcn_sched_barrier(0);   // the words go out before the stage (counted waits)
   pf_stage<GPC>(next, g, f0, c + 2 < last ? c + 2 : last, wave, lane);
 #pragma unroll
   for (int q = 0; q < GPC; ++q) {
-    const bool epi = q < GPC - 1 || !late;
     pf_group<BITS, GPC, BF16>(cur, w, q, lane, magic, acc);
-    if (epi) {
-      pf_sums<GPC>(cur, q, lane, sx);
-      pf_epilogue<BITS>(acc, s[q], sx, tot);
-    }
+    if (q < GPC - 1 || !late) pf_epilogue<BITS>(acc, s[q], tot);
     else ps = s[q];
+    zc.take<BITS, GPC>(cur, q, s[q], rel0 + q, lane, tot);
   }
 }
 
@@ -278,10 +299,10 @@ __device__ __forceinline__ void pf_chunk_body(const unsigned char* __restrict__ 
 // MFMAs.
 template <int BITS, int GPC, bool BF16>
 __device__ __forceinline__ void pf_chunk(const PfStream& sp, const PrefillGemm& g, int f0, bool late, bool first,
-                                         int c, int last, int slot, unsigned char* smem, int wave, int lane,
-                                         const uint32_t (&w)[2][BITS], const uint32_t (&s)[GPC],
+                                         int c, int last, int rel0, int slot, unsigned char* smem, int wave,
+                                         int lane, const uint32_t (&w)[2][BITS], const uint32_t (&s)[GPC],
                                          uint32_t (&nw)[2][BITS], uint32_t (&ns)[GPC], uint32_t& ps, uint32_t magic,
-                                         f32x16 (&acc)[PfCfg::kTiles], f32x16 (&tot)[PfCfg::kTiles]) {
+                                         PfZero& zc, f32x16 (&acc)[PfCfg::kTiles], f32x16 (&tot)[PfCfg::kTiles]) {
   using S = PfCfg;
   // Stage c has landed in LDS once at most the loads issued after it (stage
   // c+1) are outstanding; the plain barrier then publishes it (a fenced
@@ -290,11 +311,9 @@ __device__ __forceinline__ void pf_chunk(const PfStream& sp, const PrefillGemm& 
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-  const int slotp = slot == 0 ? kPfSlots - 1 : slot - 1;
   const int slot2 = slot + 2 >= kPfSlots ? slot + 2 - kPfSlots : slot + 2;
-  pf_chunk_body<BITS, GPC, BF16>(smem + slot * S::kStageBytes, smem + slotp * S::kStageBytes,
-                                 smem + slot2 * S::kStageBytes, sp, g, f0, late, first, c, last, wave, lane,
-                                 w, s, nw, ns, ps, magic, acc, tot);
+  pf_chunk_body<BITS, GPC, BF16>(smem + slot * S::kStageBytes, smem + slot2 * S::kStageBytes, sp, g, f0, late,
+                                 first, c, last, rel0, wave, lane, w, s, nw, ns, ps, magic, zc, acc, tot);
 }
 
 // Chunks [c_begin, c_end) of the reduction, two per iteration so that the
@@ -312,23 +331,20 @@ __device__ __forceinline__ void pf_loop(const PfStream& sp, const PrefillGemm& g
   pf_load<BITS, GPC>(wa, sa, sp, c_begin);
   pf_stage<GPC>(smem, g, f0, c_begin, wave, lane);
   pf_stage<GPC>(smem + S::kStageBytes, g, f0, c_begin + 1 < last ? c_begin + 1 : last, wave, lane);
+  PfZero zc{};
   int slot = 0;
-  for (int c = c_begin; c < c_end; c += 2) {
-    pf_chunk<BITS, GPC, BF16>(sp, g, f0, late, c == c_begin, c, last, slot, smem, wave, lane, wa, sa, wb, sb, ps,
-                              magic, acc, tot);
+  for (int it = 0, c = c_begin; c < c_end; ++it, c += 2) {
+    const int rel0 = it * 2 * GPC;   // even: the parity of a group's number is known per call site
+    pf_chunk<BITS, GPC, BF16>(sp, g, f0, late, c == c_begin, c, last, rel0, slot, smem, wave, lane, wa, sa, wb, sb,
+                              ps, magic, zc, acc, tot);
     slot = slot + 1 == kPfSlots ? 0 : slot + 1;
     if (c + 1 < c_end)
-      pf_chunk<BITS, GPC, BF16>(sp, g, f0, late, false, c + 1, last, slot, smem, wave, lane, wb, sb, wa, sa, ps,
-                                magic, acc, tot);
+      pf_chunk<BITS, GPC, BF16>(sp, g, f0, late, false, c + 1, last, rel0 + GPC, slot, smem, wave, lane, wb, sb, wa,
+                                sa, ps, magic, zc, acc, tot);
     slot = slot + 1 == kPfSlots ? 0 : slot + 1;
   }
-  // the late waves' last epilogue: the last chunk's stage is the slot before `slot`
-  if (late)
-  {
-    f32x4 sx[S::kTiles][4];
-    pf_sums<GPC>(smem + (slot == 0 ? kPfSlots - 1 : slot - 1) * S::kStageBytes, GPC - 1, lane, sx);
-    pf_epilogue<BITS>(acc, ps, sx, tot);
-  }
+  if (late) pf_epilogue<BITS>(acc, ps, tot);   // the late waves' deferred last epilogue
+  zc.finish((c_end - c_begin) * GPC, lane, tot);
   wait_vmcnt<0>();   // the clamped re-reads of the last chunks land before LDS is reused
 }
 
