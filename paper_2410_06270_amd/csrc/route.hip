@@ -8,8 +8,9 @@
 // (fp64).  Sec. 3.3.2: a protected token keeps every selected expert.  The
 // kept weights are renormalised over the kept ranks.
 //
-// Selection (one wavefront per token): lanes hold the logits, every key's
-// rank is counted against all keys broadcast in turn, lane r then evaluates
+// Selection (one segment of S lanes per token, S the power of two covering
+// the experts, 64/S tokens per wavefront): lanes hold the logits, every key's
+// rank is counted against the segment's keys in turn, lane r then evaluates
 // rank r; the softmax sums add the ranks in order.
 // Lists: per-expert token lists in ascending token order, built with ballots
 // and popcount prefixes (list positions never depend on timing, so the lists
@@ -57,15 +58,18 @@ __device__ __forceinline__ int list_pass(int pass, int e, int run, int c0, int n
 
 __global__ void __launch_bounds__(256) route_select_kernel(const float* __restrict__ logits,
                                                            const uint8_t* __restrict__ important,
-                                                           int T, int E, int k, float delta32,
+                                                           int T, int E, int S, int k, float delta32,
                                                            double tau, int32_t* topk_idx,
                                                            float* topk_w, uint8_t* kept,
                                                            int32_t* pair_pos) {
   __shared__ __attribute__((aligned(16))) unsigned char scratch[4][kSelScratchBytes];
-  const int t = blockIdx.x * (blockDim.x >> 6) + wave_id();
-  if (t >= T) return;
-  select_token(logits + (size_t)t * E, important != nullptr ? important + t : nullptr, t, E, k, delta32, tau,
-               topk_idx, topk_w, kept, pair_pos, true, nullptr, nullptr, sel_scratch(scratch[wave_id()]));
+  const int lane = threadIdx.x & 63, ns = 64 / S;
+  const int t0 = (blockIdx.x * (blockDim.x >> 6) + wave_id()) * ns;
+  if (t0 >= T) return;
+  const int t = t0 + lane / S;
+  const SelInput in = sel_load(logits, important, t, T, E, S);
+  select_token(in, t, T, E, S, k, delta32, tau, topk_idx, topk_w, kept, pair_pos, true, nullptr, nullptr,
+               sel_scratch(scratch[wave_id()]));
 }
 
 // Tokens per list block: a multiple of 64, at most kListBlocks blocks.
@@ -132,9 +136,14 @@ __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
   __shared__ __attribute__((aligned(16))) unsigned char scratch[kCsrThreads / 64][kSelScratchBytes];
   const int wave = wave_id(), nwaves = blockDim.x >> 6;
   const SelScratch sc = sel_scratch(scratch[wave]);
-  for (int t = wave; t < T; t += nwaves)
-    select_token(logits + (size_t)t * E, important != nullptr ? important + t : nullptr, t, E, k, delta32, tau,
-                 topk_idx, topk_w, kept, pair_pos, true, ent, wsel, sc);
+  const int S = sel_segment(E), ns = 64 / S;
+  // a wave selects ns tokens at once; T * E <= kRouteFusedMaxTE makes one
+  // round of the 16 waves enough
+  for (int t0 = wave * ns; t0 < T; t0 += nwaves * ns) {
+    const int t = t0 + (threadIdx.x & 63) / S;
+    const SelInput in = sel_load(logits, important, t, T, E, S);
+    select_token(in, t, T, E, S, k, delta32, tau, topk_idx, topk_w, kept, pair_pos, true, ent, wsel, sc);
+  }
   __syncthreads();
   if (wave != 0) return;
   const RouteLds s{ent, wsel, cnt, base, bal};
@@ -153,9 +162,9 @@ hipError_t launch_route(const float* logits, const uint8_t* important, float del
     return hipGetLastError();
   }
   timing_begin(stream, kSiteRouteSelect);
-  hipLaunchKernelGGL(route_select_kernel, dim3((r.T + 3) / 4), dim3(256), 0, stream, logits,
-                     important, r.T, r.E, r.k, delta32, tau, r.topk_idx, r.topk_w, r.kept,
-                     r.pair_pos);
+  const int S = sel_segment(r.E), per_wg = 4 * (64 / S);   // tokens per workgroup
+  hipLaunchKernelGGL(route_select_kernel, dim3((r.T + per_wg - 1) / per_wg), dim3(256), 0, stream, logits,
+                     important, r.T, r.E, S, r.k, delta32, tau, r.topk_idx, r.topk_w, r.kept, r.pair_pos);
   timing_end(stream, kSiteRouteSelect);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;

@@ -13,97 +13,122 @@ __device__ __forceinline__ uint32_t ordered_bits(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Per-wave LDS scratch of the selection: the token's E keys, the k selected
-// (expert, logit) pairs in rank order and their exp terms.
+// Lane segments of the selection: a wave selects 64 / S tokens at once, one
+// per segment of S lanes, S the smallest power of two >= E (at most 64; with
+// more than 64 experts lane q holds experts q, q+64, ...).
+__host__ __device__ constexpr int sel_segment(int E) { return E <= 1 ? 1 : E <= 64 ? 1 << (32 - __builtin_clz(E - 1)) : 64; }
+
+// Per-wave LDS scratch of the selection: the segments' keys (segment g at
+// [g*S, g*S + E)), and per segment its k selected (expert, logit) pairs in
+// rank order and their exp terms (segment g at [g*k, g*k + k); 64/S segments
+// of k <= S entries).
 struct SelScratch {
-  unsigned long long* key;   // [E]
-  int* sel_e;                // [k]
-  float* sel_l;              // [k]
-  double* ex;                // [k]
+  unsigned long long* key;   // [max(64, E)]
+  int* sel_e;                // [64]
+  float* sel_l;              // [64]
+  double* ex;                // [64]
 };
-constexpr int kSelScratchBytes = MC_MAX_EXPERTS * 8 + MC_MAX_TOPK * (4 + 4 + 8);
+constexpr int kSelScratchBytes = MC_MAX_EXPERTS * 8 + 64 * (4 + 4 + 8);
 
 __device__ __forceinline__ SelScratch sel_scratch(unsigned char* base) {
   SelScratch s;
   s.key = reinterpret_cast<unsigned long long*>(base);
   s.ex = reinterpret_cast<double*>(base + MC_MAX_EXPERTS * 8);
-  s.sel_e = reinterpret_cast<int*>(base + MC_MAX_EXPERTS * 8 + MC_MAX_TOPK * 8);
-  s.sel_l = reinterpret_cast<float*>(base + MC_MAX_EXPERTS * 8 + MC_MAX_TOPK * 12);
+  s.sel_e = reinterpret_cast<int*>(base + MC_MAX_EXPERTS * 8 + 64 * 8);
+  s.sel_l = reinterpret_cast<float*>(base + MC_MAX_EXPERTS * 8 + 64 * 12);
   return s;
 }
 
-// Selects and prunes token t (one wavefront).  Lanes hold the logits (lane l
-// has experts l, l+64, ...) as distinct 64-bit keys (ordered logit bits, then
-// the complement of the expert index, so larger key = earlier rank); the keys
-// go to the wave's LDS scratch and each key's rank is the number of larger
-// keys, read back as broadcasts.  The rank-r pair goes to slot r, lane r < k
-// takes it; the softmax sums run over the ranks in order (fp64).  Lane r < k
-// writes rank r's outputs (when `publish`); when s_ent/s_w are given it also
-// records them in LDS (expert, or 0xffff if pruned).  l: the token's E logits
-// and prot_src: its protection flag (NULL: unprotected), in memory or LDS.
-static __device__ void select_token(const float* l, const uint8_t* prot_src, int t, int E, int k, float delta32,
+// The lane's share of token t's inputs (t >= T: none): the logits of experts
+// q, q+S, ... (q the lane within its segment of S lanes) and the protection
+// flag (important NULL: unprotected).
+struct SelInput {
+  float lv[4];
+  int prot;
+};
+
+__device__ __forceinline__ SelInput sel_load(const float* __restrict__ logits, const uint8_t* __restrict__ important,
+                                             int t, int T, int E, int S) {
+  const int q = (threadIdx.x & 63) & (S - 1);
+  const bool tv = t < T;
+  SelInput in;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = q + S * j;
+    in.lv[j] = (tv && e < E) ? logits[(size_t)t * E + e] : 0.0f;
+  }
+  in.prot = (tv && important != nullptr) ? (int)important[t] : 0;
+  return in;
+}
+
+// Selects and prunes token t (one segment of S lanes of the wave; every lane
+// of the wave calls it, each segment with its own token; t >= T: nothing is
+// written).  The lanes hold the logits as distinct 64-bit keys (ordered logit
+// bits, then the complement of the expert index, so larger key = earlier
+// rank); the keys go to the segment's LDS scratch and each key's rank is the
+// number of larger keys of the segment.  The rank-r pair goes to slot r,
+// lane r < k of the segment takes it; the softmax sums run over the ranks in
+// order (fp64).  Lane r < k writes rank r's outputs (when `publish`); when
+// s_ent/s_w are given it also records them in LDS (expert, or 0xffff if
+// pruned).
+static __device__ void select_token(const SelInput& in, int t, int T, int E, int S, int k, float delta32,
                                     double tau, int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
                                     uint8_t* __restrict__ kept, int32_t* __restrict__ pair_pos, bool publish,
                                     uint16_t* s_ent, float* s_w, const SelScratch& sc) {
   const int lane = threadIdx.x & 63;
-  float lv[4];
+  const int q = lane & (S - 1), seg = lane >> __builtin_ctz((unsigned)S);
+  const int kb = seg * S, sb = seg * k;   // the segment's keys and selection slots
+  const float* lv = in.lv;
+  const int prot_flag = in.prot;
   unsigned long long key[4];
   int rank[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int e = lane + 64 * j;
-    lv[j] = (e < E) ? l[e] : 0.0f;
-  }
-  // the protection flag is loaded beside the logits (one memory round trip)
-  const int prot_flag = prot_src != nullptr ? (int)*prot_src : 0;
-  asm volatile("" ::"v"(lv[0]), "v"(lv[1]), "v"(lv[2]), "v"(lv[3]), "v"(prot_flag));
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = lane + 64 * j;
+    const int e = q + S * j;
     key[j] = (e < E) ? (((unsigned long long)ordered_bits(lv[j]) << 32) | (unsigned)(0xffff - e)) : 0ull;
     rank[j] = 0;
-    if (e < E) sc.key[e] = key[j];
+    if (e < E) sc.key[kb + e] = key[j];
   }
   __builtin_amdgcn_wave_barrier();
-  const int nj = (E + 63) >> 6;                      // keys per lane (wave-uniform)
+  const int nj = (E + S - 1) / S;                    // keys per lane (wave-uniform)
   int e2 = 0;
   for (; e2 + 4 <= E; e2 += 4) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const unsigned long long o = sc.key[e2 + u];
+      const unsigned long long o = sc.key[kb + e2 + u];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (j < nj) rank[j] += o > key[j] ? 1 : 0;
     }
   }
   for (; e2 < E; ++e2) {
-    const unsigned long long o = sc.key[e2];
+    const unsigned long long o = sc.key[kb + e2];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       if (j < nj) rank[j] += o > key[j] ? 1 : 0;
   }
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int e = lane + 64 * j;
+    const int e = q + S * j;
     if (e < E && rank[j] < k) {
-      sc.sel_e[rank[j]] = e;
-      sc.sel_l[rank[j]] = lv[j];
+      sc.sel_e[sb + rank[j]] = e;
+      sc.sel_l[sb + rank[j]] = lv[j];
     }
   }
   __builtin_amdgcn_wave_barrier();
-  const bool mine = lane < k;
-  const int my_e = mine ? sc.sel_e[lane] : 0;
-  const float my_l = mine ? sc.sel_l[lane] : 0.0f;
-  const float l0 = sc.sel_l[0];
-  const float l1 = k < 2 ? l0 : sc.sel_l[1];
+  const bool mine = q < k;
+  const int my_e = mine ? sc.sel_e[sb + q] : 0;
+  const float my_l = mine ? sc.sel_l[sb + q] : 0.0f;
+  const float l0 = sc.sel_l[sb];
+  const float l1 = k < 2 ? l0 : sc.sel_l[sb + 1];
   const bool prot = prot_flag != 0;
   const double ex = mine ? exp((double)my_l - (double)l0) : 0.0;
-  if (mine) sc.ex[lane] = ex;
+  if (mine) sc.ex[sb + q] = ex;
   __builtin_amdgcn_wave_barrier();
   double sum_all = 0.0;
-  for (int r = 0; r < k; ++r) sum_all += sc.ex[r];
+  for (int r = 0; r < k; ++r) sum_all += sc.ex[sb + r];
   bool keep = mine;
-  if (mine && lane > 0 && !prot) {
+  if (mine && q > 0 && !prot) {
     if (k == 2) {
       const float gap = l0 - l1;
       keep = !(gap > delta32);
@@ -111,12 +136,12 @@ static __device__ void select_token(const float* l, const uint8_t* prot_src, int
       keep = !(ex < tau * sum_all);
     }
   }
-  const unsigned long long kb = __ballot(keep);
+  const unsigned long long kbits = __ballot(keep) >> kb;   // this segment's ranks from bit 0
   double sum_kept = 0.0;
   for (int r = 0; r < k; ++r)
-    if ((kb >> r) & 1ull) sum_kept += sc.ex[r];
-  if (mine) {
-    const size_t o = (size_t)t * k + lane;
+    if ((kbits >> r) & 1ull) sum_kept += sc.ex[sb + r];
+  if (mine && t < T) {
+    const size_t o = (size_t)t * k + q;
     const float w = keep ? (float)(ex / sum_kept) : 0.0f;
     if (publish) {
       topk_idx[o] = my_e;
@@ -129,7 +154,7 @@ static __device__ void select_token(const float* l, const uint8_t* prot_src, int
       s_w[o] = w;
     }
   }
-  __builtin_amdgcn_wave_barrier();   // the scratch is free for the wave's next token
+  __builtin_amdgcn_wave_barrier();   // the scratch is free for the wave's next tokens
 }
 
 // Exclusive scan of cnt[0..E) into base[] and offsets[0..E] (one wave: each

@@ -161,6 +161,26 @@ def test_route_edge_cases(mc):
         assert_routing_equal(r, ref, T, k)
 
 
+@pytest.mark.parametrize("T,E,k,tau", [
+    (40, 5, 3, 0.2), (100, 5, 3, 0.2),     # E not a power of two: segments of 8 lanes, k > 2
+    (64, 2, 2, 0.3), (200, 2, 2, 0.3),     # 32 tokens per wavefront
+    (31, 16, 4, 0.2), (500, 16, 4, 0.2),
+    (15, 33, 3, 0.3), (70, 33, 3, 0.3),    # one 64-lane segment, 31 lanes idle
+])
+def test_route_lane_segments(mc, T, E, k, tau):
+    """Tokens selected side by side in segments of a wavefront (small batches
+    in one launch, larger ones by the selection kernel), with a protection
+    mask and ties, against the oracle."""
+    g = np.random.default_rng(1000 + T * E)
+    lg = g.standard_normal((T, E)).astype(np.float32)
+    lg[::3, 1] = lg[::3, 0]
+    imp = (g.random(T) < 0.25).astype(np.uint8)
+    assert_margin(lg, imp, k, tau)
+    ref = oracle.route(lg, imp, k, tau)
+    r = route_gpu(mc, lg, imp, k, tau)
+    assert_routing_equal(r, ref, T, k)
+
+
 def layer_case(cid=1, E=None, bits=None, d=None, ffn=None):
     c = synthetic.config(cid)
     E = E or c["E"]
