@@ -24,8 +24,11 @@
 //
 // The activations of an item (x for gate/up; h, or the gate/up partials, for
 // down) are staged once into an LDS slab covering the item's whole reduction
-// range; the weight ring of each wave is issued before the staging, so the
-// staging latency overlaps the first weight loads.
+// range.  Copied rows (x, or h) go out as direct-to-LDS loads ahead of each
+// wave's weight ring, and the wave waits only for them (a counted wait that
+// leaves the ring in flight): the loop starts as soon as the slab has landed,
+// while the ring is still arriving, and the weight stream never stops for the
+// staging.
 #pragma once
 
 #include "forward_engine.hpp"
@@ -239,15 +242,16 @@ __device__ __forceinline__ int dec_part_start(int N, int D, int w, int nw) {
 }
 
 // Streams this wave's part of the piece (row units [u0, u1), C chunks each;
-// D divides C) against the slab that stage() fills, writes every row unit it
-// completes with emit(u, t), and reduces the row units split over several
-// waves.  The weight ring of D chunks is issued before the staging.  Vector
+// D divides C) against the slab that stage_early() and stage_late() fill
+// (before and after the first D chunks of the weight ring are issued), writes
+// every row unit it completes with emit(u, t), and reduces the row units
+// split over several waves.  Vector
 // memory stores happen only between row units (outside the unrolled ring), so
 // the compiler's load counting keeps the ring in flight.
-template <int BITS, int GPC, bool F16, int D, typename StageFn, typename EmitFn>
+template <int BITS, int GPC, bool F16, int D, typename EarlyFn, typename LateFn, typename EmitFn>
 __device__ __forceinline__ void decode_run(const DecGeom& g, int u0, int u1, int C, int w0, int w1,
-                                           const uint16_t* arow, const float* sxs, float* tails, StageFn stage,
-                                           EmitFn emit) {
+                                           const uint16_t* arow, const float* sxs, float* tails,
+                                           EarlyFn stage_early, LateFn stage_late, EmitFn emit) {
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int nw = w1 - w0, wl = wave - w0;       // this piece's waves, this wave among them
   const int N = (u1 - u0) * C;
@@ -260,6 +264,7 @@ __device__ __forceinline__ void decode_run(const DecGeom& g, int u0, int u1, int
   int pleft = qb - qa - 1;
   uint32_t wr[D][2][BITS];
   uint32_t sr[D][2][GPC];
+  stage_early();
   if (qa < qb) {
 #pragma unroll
     for (int j = 0; j < D; ++j) {
@@ -267,8 +272,14 @@ __device__ __forceinline__ void decode_run(const DecGeom& g, int u0, int u1, int
       cursor_next(pc, g, pleft > 0);
       pleft = pleft > 0 ? pleft - 1 : 0;
     }
+    // the staging copies, issued before the ring, have landed once at most
+    // the ring's loads (2 + 2 GPC instructions a chunk) are outstanding
+    wait_vmcnt<D * (2 + 2 * GPC)>();
+  } else {
+    wait_vmcnt<0>();
   }
-  stage();
+  asm volatile("" ::: "memory");
+  stage_late();
 
   f32x4 acc[2][1], tot[2][1], head[2];
   zero2(head);
@@ -405,7 +416,13 @@ __device__ __forceinline__ void decode_piece(const LayerArgs& L, const DecodeArg
   const int kw = C * kTileCols;
   const int RS = kw + kRowPad;
   uint16_t* zrow = xs + (size_t)nt * RS;
-  auto stage = [&]() {
+  // Staging in two parts around the weight ring's first loads: the copies
+  // of x (or h) go out as direct-to-LDS loads before the ring (stage_early),
+  // so that they land first and the loop can start while the ring is still
+  // arriving; their sums, or the h rows formed from the gate/up partials,
+  // follow the ring (stage_late).
+  const bool copy_rows = GATEUP || a.gu_split == 1;
+  auto stage_early = [&]() {
     for (int i = wl * 64 + lane; i < RS / 8; i += nw * 64)
       *reinterpret_cast<u32x4*>(zrow + 8 * i) = u32x4{0u, 0u, 0u, 0u};
     if (GATEUP) {
@@ -413,13 +430,17 @@ __device__ __forceinline__ void decode_piece(const LayerArgs& L, const DecodeArg
       // the row of each staged segment is a register read, not a dependent
       // global load per segment
       const int tok = (lane < nt) ? clamp_token(a.pair_token[pbase + lane], a.T) : 0;
-      stage_rows<false, true>(
-          xs, sxs, [&](int m) { return a.x + (size_t)__builtin_amdgcn_readlane(tok, m) * K; },
-          [](int, int) { return 0.0f; }, nt, kDecTok, c0 * kTileCols, kw, RS, L.G, wl, nw);
+      stage_rows_issue(
+          xs, [&](int m) { return a.x + (size_t)__builtin_amdgcn_readlane(tok, m) * K; }, nt, c0 * kTileCols, kw,
+          RS, wl, nw);
     } else if (a.gu_split == 1) {
-      stage_rows<true, true>(
-          xs, sxs, [&](int m) { return a.h + (size_t)(pbase + m) * K; }, [](int, int) { return 0.0f; }, nt,
-          kDecTok, c0 * kTileCols, kw, RS, L.G, wl, nw);
+      stage_rows_issue(xs, [&](int m) { return a.h + (size_t)(pbase + m) * K; }, nt, c0 * kTileCols, kw, RS, wl,
+                       nw);
+    }
+  };
+  auto stage_late = [&]() {
+    if (copy_rows) {
+      stage_rows_sums<F16>(xs, sxs, nt, kDecTok, kw, RS, L.G, wl, nw);
     } else {
       // h from the gate/up partial sums (added in split order), rounded to
       // fp16 as an unsplit gate/up epilogue forms it
@@ -476,11 +497,11 @@ __device__ __forceinline__ void decode_piece(const LayerArgs& L, const DecodeArg
   // chunk c + j of a unit and the unrolled loop needs no remainder
   constexpr int DM = prefetch_depth(1, GPC);
   if (C % DM == 0)
-    decode_run<BITS, GPC, F16, DM>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage, emit);
+    decode_run<BITS, GPC, F16, DM>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage_early, stage_late, emit);
   else if (C % 2 == 0)
-    decode_run<BITS, GPC, F16, 2>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage, emit);
+    decode_run<BITS, GPC, F16, 2>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage_early, stage_late, emit);
   else
-    decode_run<BITS, GPC, F16, 1>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage, emit);
+    decode_run<BITS, GPC, F16, 1>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage_early, stage_late, emit);
 }
 
 constexpr int kDecMaxPieces = 8;   // pieces planned per round (a share crosses few items)

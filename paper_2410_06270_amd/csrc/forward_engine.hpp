@@ -154,18 +154,20 @@ __device__ __forceinline__ void load_words_so(uint32_t (&w)[BITS], rsrc_t r, uin
 // the sums of each group of G columns, sxs[group][rows].
 
 // Rows that are plain copies of global memory (x; h when the gate/up reduction
-// was not split), row m starting at row_src(m): direct-to-LDS 16-byte loads,
-// 64 consecutive pieces of a row per wave instruction, so every wave has all
-// its loads in flight at once.  With SUMS each wave then forms the group sums
-// of its own row segments (a segment is 512 columns, a whole number of groups;
-// the G/8 lanes of a group add in a fixed butterfly order); otherwise the sums
-// are read from sum_src(m, g) for the slab's groups g.  The waves w of the
-// nwaves that stage this slab (a workgroup may stage several slabs at once)
-// take its segments in turn; the final barrier is the workgroup's.
-template <bool F16, bool SUMS, typename RowFn, typename SumFn>
-__device__ __forceinline__ void stage_rows(uint16_t* xs, float* sxs, RowFn row_src, SumFn sum_src,
-                                           int nt, int rows, int ks, int kw, int RS, int G, int wave,
-                                           int nwaves) {
+// was not split), row m starting at row_src(m), in two halves so that other
+// loads can be issued between them:
+//  * stage_rows_issue: direct-to-LDS 16-byte loads, 64 consecutive pieces of
+//    a row per wave instruction, so every wave has all its loads in flight at
+//    once;
+//  * stage_rows_sums, once the caller has waited for those loads: each wave
+//    forms the group sums of its own row segments (a segment is 512 columns,
+//    a whole number of groups; the G/8 lanes of a group add in a fixed
+//    butterfly order), then the workgroup's barrier.
+// The waves w of the nwaves that stage this slab (a workgroup may stage
+// several slabs at once) take its segments in turn.
+template <typename RowFn>
+__device__ __forceinline__ void stage_rows_issue(uint16_t* xs, RowFn row_src, int nt, int ks, int kw, int RS,
+                                                 int wave, int nwaves) {
   const int lane = threadIdx.x & 63;
   const int pieces = kw >> 3;
   const int segs = (pieces + 63) >> 6;
@@ -175,25 +177,23 @@ __device__ __forceinline__ void stage_rows(uint16_t* xs, float* sxs, RowFn row_s
     const int p = sg * 64 + lane;
     if (p < pieces) lds_dma16(row_src(m) + ks + 8 * p, xs + (size_t)m * RS + sg * 512);
   }
-  if constexpr (!SUMS) {
-    const int ngs = kw / G;
-    for (int i = wave * 64 + lane; i < nt * ngs; i += nwaves * 64) {
-      const int m = i / ngs, g = i - m * ngs;
-      sxs[g * rows + m] = sum_src(m, g);
-    }
-  }
-  wait_vmcnt<0>();
-  asm volatile("" ::: "memory");
-  if constexpr (SUMS) {
-    const int gp = G >> 3;
-    for (int s = wave; s < nseg; s += nwaves) {
-      const int m = s / segs, sg = s - m * segs;
-      const int p = sg * 64 + lane;
-      float sum = 0.0f;
-      if (p < pieces) sum = sum8<F16>(*reinterpret_cast<const u32x4*>(xs + (size_t)m * RS + 8 * p));
-      for (int off = 1; off < gp; off <<= 1) sum += __shfl_xor(sum, off);
-      if (p < pieces && (p % gp) == 0) sxs[(p / gp) * rows + m] = sum;
-    }
+}
+
+template <bool F16>
+__device__ __forceinline__ void stage_rows_sums(const uint16_t* xs, float* sxs, int nt, int rows, int kw, int RS,
+                                                int G, int wave, int nwaves) {
+  const int lane = threadIdx.x & 63;
+  const int pieces = kw >> 3;
+  const int segs = (pieces + 63) >> 6;
+  const int nseg = nt * segs;
+  const int gp = G >> 3;
+  for (int s = wave; s < nseg; s += nwaves) {
+    const int m = s / segs, sg = s - m * segs;
+    const int p = sg * 64 + lane;
+    float sum = 0.0f;
+    if (p < pieces) sum = sum8<F16>(*reinterpret_cast<const u32x4*>(xs + (size_t)m * RS + 8 * p));
+    for (int off = 1; off < gp; off <<= 1) sum += __shfl_xor(sum, off);
+    if (p < pieces && (p % gp) == 0) sxs[(p / gp) * rows + m] = sum;
   }
   __syncthreads();
 }
