@@ -440,7 +440,7 @@ __device__ __forceinline__ void decode_piece(const LayerArgs& L, const DecodeArg
   };
   auto stage_late = [&]() {
     if (copy_rows) {
-      stage_rows_sums<F16>(xs, sxs, nt, kDecTok, kw, RS, L.G, wl, nw);
+      stage_rows_sums<F16, 16 / GPC>(xs, sxs, nt, kDecTok, kw, RS, wl, nw);
     } else {
       // h from the gate/up partial sums (added in split order), rounded to
       // fp16 as an unsplit gate/up epilogue forms it
@@ -464,7 +464,7 @@ __device__ __forceinline__ void decode_piece(const LayerArgs& L, const DecodeArg
         }
         return v;
       };
-      stage_pieces<true>(xs, sxs, piece, nt, kDecTok, c0 * kTileCols, kw, RS, L.G, wl, nw);
+      stage_pieces<true, 16 / GPC>(xs, sxs, piece, nt, kDecTok, c0 * kTileCols, kw, RS, wl, nw);
     }
   };
 

@@ -179,34 +179,51 @@ __device__ __forceinline__ void stage_rows_issue(uint16_t* xs, RowFn row_src, in
   }
 }
 
-template <bool F16>
+// Sum over aligned groups of GP = 4, 8 or 16 lanes by a butterfly of DPP
+// lane moves (register moves, no LDS round trips): partners at distance 1
+// and 2 (quad permutations), then the other quad of each 8 (half-row mirror),
+// then the other 8 of each 16 (row mirror).  After every step all lanes of a
+// block hold the same bits (own + partner, and fp32 addition commutes), so
+// the result is that of the xor butterfly with distances 1, 2, 4, 8.
+template <int GP>
+__device__ __forceinline__ float lane_group_sum(float v) {
+  static_assert(GP == 4 || GP == 8 || GP == 16, "DPP rows hold 16 lanes");
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xb1, 0xf, 0xf, false));    // [1,0,3,2]
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4e, 0xf, 0xf, false));    // [2,3,0,1]
+  if constexpr (GP >= 8)
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xf, 0xf, false));  // half mirror
+  if constexpr (GP >= 16)
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xf, 0xf, false));  // mirror
+  return v;
+}
+
+// GP = G/8: the lanes of a group (each lane holds 8 columns).
+template <bool F16, int GP>
 __device__ __forceinline__ void stage_rows_sums(const uint16_t* xs, float* sxs, int nt, int rows, int kw, int RS,
-                                                int G, int wave, int nwaves) {
+                                                int wave, int nwaves) {
   const int lane = threadIdx.x & 63;
   const int pieces = kw >> 3;
   const int segs = (pieces + 63) >> 6;
   const int nseg = nt * segs;
-  const int gp = G >> 3;
   for (int s = wave; s < nseg; s += nwaves) {
     const int m = s / segs, sg = s - m * segs;
     const int p = sg * 64 + lane;
     float sum = 0.0f;
     if (p < pieces) sum = sum8<F16>(*reinterpret_cast<const u32x4*>(xs + (size_t)m * RS + 8 * p));
-    for (int off = 1; off < gp; off <<= 1) sum += __shfl_xor(sum, off);
-    if (p < pieces && (p % gp) == 0) sxs[(p / gp) * rows + m] = sum;
+    sum = lane_group_sum<GP>(sum);
+    if (p < pieces && (p % GP) == 0) sxs[(p / GP) * rows + m] = sum;
   }
   __syncthreads();
 }
 
 // Rows computed piece by piece (8 columns, 16 bytes) by src(m, k); the group
 // sums are those of the computed values.  Waves as for stage_rows.
-template <bool F16, typename PieceFn>
+template <bool F16, int GP, typename PieceFn>
 __device__ __forceinline__ void stage_pieces(uint16_t* xs, float* sxs, PieceFn src, int nt, int rows,
-                                             int ks, int kw, int RS, int G, int wave, int nwaves) {
+                                             int ks, int kw, int RS, int wave, int nwaves) {
   const int lane = threadIdx.x & 63;
   const int pieces = kw >> 3;
   const int total = nt * pieces;
-  const int gp = G >> 3;
   for (int base = wave * 64; base < total; base += nwaves * 64) {
     const int idx = base + lane;
     const bool valid = idx < total;
@@ -219,8 +236,8 @@ __device__ __forceinline__ void stage_pieces(uint16_t* xs, float* sxs, PieceFn s
       *reinterpret_cast<u32x4*>(xs + (size_t)m * RS + 8 * p) = v;
       sum = sum8<F16>(v);
     }
-    for (int off = 1; off < gp; off <<= 1) sum += __shfl_xor(sum, off);
-    if (valid && (p % gp) == 0) sxs[(p / gp) * rows + m] = sum;
+    sum = lane_group_sum<GP>(sum);
+    if (valid && (p % GP) == 0) sxs[(p / GP) * rows + m] = sum;
   }
   __syncthreads();
 }
