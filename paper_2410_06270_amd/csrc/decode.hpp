@@ -36,6 +36,7 @@
 namespace mc {
 
 constexpr int kDecTok = 16;                   // pairs of a work item (MFMA M)
+static_assert(kDecodeMaxT * MC_MAX_TOPK <= 512, "the decode pair list fits its LDS copy");
 constexpr int kDecWaves = 16;                 // one 1024-thread workgroup per CU
 constexpr int kDecSlabBytes = 146 * 1024;     // activation slab (x or h rows)
 constexpr int kDecSumBytes = 9 * 1024;        // group sums of the slab
@@ -371,7 +372,7 @@ __device__ __forceinline__ void decode_run(const DecGeom& g, int u0, int u1, int
 // of its activations and the writing of its outputs, then decode_run.
 template <int BITS, int GPC, bool GATEUP>
 __device__ __forceinline__ void decode_piece(const LayerArgs& L, const DecodeArgs& a, unsigned char* smem,
-                                             const DecPiece& p) {
+                                             const int32_t* s_tok, const DecPiece& p) {
   const int e = p.e, s = p.s, C = p.C, u0 = p.u0, u1 = p.u1, pbase = p.pbase, nt = p.nt;
   constexpr bool F16 = !GATEUP;
   const int lane = threadIdx.x & 63;
@@ -426,10 +427,10 @@ __device__ __forceinline__ void decode_piece(const LayerArgs& L, const DecodeArg
     for (int i = wl * 64 + lane; i < RS / 8; i += nw * 64)
       *reinterpret_cast<u32x4*>(zrow + 8 * i) = u32x4{0u, 0u, 0u, 0u};
     if (GATEUP) {
-      // lane m < nt holds the token of pair pbase + m: one load round, then
-      // the row of each staged segment is a register read, not a dependent
-      // global load per segment
-      const int tok = (lane < nt) ? clamp_token(a.pair_token[pbase + lane], a.T) : 0;
+      // lane m < nt holds the token of pair pbase + m (from the workgroup's
+      // LDS copy of the pair list), so the row of each staged segment is a
+      // register read, not a dependent global load per segment
+      const int tok = (lane < nt) ? clamp_token(s_tok[pbase + lane], a.T) : 0;
       stage_rows_issue(
           xs, [&](int m) { return a.x + (size_t)__builtin_amdgcn_readlane(tok, m) * K; }, nt, c0 * kTileCols, kw,
           RS, wl, nw);
@@ -513,6 +514,10 @@ struct DecPlan {
   int more;              // another round follows
   uint32_t pos;          // where the next round starts
 };
+// dynamic (slab, sums) and static (plan, pair list) LDS of the decode kernel
+static_assert(kDecSlabBytes + kDecSumBytes + sizeof(DecPlan) + sizeof(int32_t) * kDecodeMaxT * MC_MAX_TOPK <=
+                  kLdsPerCu,
+              "decode LDS");
 
 // Pieces [b0, b1) of the plan run together: every piece gets one wave, the
 // other waves are shared out in proportion to the pieces' chunks.
@@ -580,6 +585,10 @@ decode_kernel(LayerArgs L, DecodeArgs a) {
   // the workgroup's pieces, planned by wave 0 (the other waves would only
   // repeat the same scalar work on their SIMDs)
   __shared__ DecPlan plan;
+  // gate/up: the batch's pair list (token of each kept-pair slot), copied by
+  // the other waves while wave 0 plans, so that staging needs no global load
+  // round trip before its copies go out
+  __shared__ int32_t s_tok[GATEUP ? kDecodeMaxT * MC_MAX_TOPK : 1];
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int K = GATEUP ? L.d : L.ffn;
   const int ntiles = K / kTileCols;
@@ -598,6 +607,8 @@ decode_kernel(LayerArgs L, DecodeArgs a) {
     lo = q * blockIdx.x + (rm * blockIdx.x) / a.nwg;
     hi = q * (blockIdx.x + 1) + (rm * (blockIdx.x + 1)) / a.nwg;
     plan_round<GPC>(L, a, &x0, incl0, R, ntiles, lo, hi, lo, plan);
+  } else if (GATEUP) {
+    for (int i = (wave - 1) * 64 + lane; i < a.P; i += (kDecWaves - 1) * 64) s_tok[i] = a.pair_token[i];
   }
   __syncthreads();
   for (;;) {
@@ -610,11 +621,11 @@ decode_kernel(LayerArgs L, DecodeArgs a) {
         if (plan.piece[i].batch == bt && plan.piece[i].w0 <= wave && wave < plan.piece[i].w1) mine = i;
       const DecPiece p = plan.piece[mine];
       if (p.b == 1)
-        decode_piece<1, GPC, GATEUP>(L, a, smem, p);
+        decode_piece<1, GPC, GATEUP>(L, a, smem, s_tok, p);
       else if (p.b == 2)
-        decode_piece<2, GPC, GATEUP>(L, a, smem, p);
+        decode_piece<2, GPC, GATEUP>(L, a, smem, s_tok, p);
       else
-        decode_piece<3, GPC, GATEUP>(L, a, smem, p);
+        decode_piece<3, GPC, GATEUP>(L, a, smem, s_tok, p);
     }
     if (!more) break;
     __syncthreads();                 // every wave has read the plan and left the slab
