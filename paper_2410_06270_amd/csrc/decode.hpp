@@ -37,7 +37,7 @@ namespace mc {
 
 constexpr int kDecTok = 16;                   // pairs of a work item (MFMA M)
 static_assert(kDecodeMaxT * MC_MAX_TOPK <= 512, "the decode pair list fits its LDS copy");
-constexpr int kDecWaves = 16;                 // one 1024-thread workgroup per CU
+constexpr int kDecWaves = 16;                 // waves of a workgroup (one workgroup per CU), at most
 constexpr int kDecSlabBytes = 146 * 1024;     // activation slab (x or h rows)
 constexpr int kDecSumBytes = 9 * 1024;        // group sums of the slab
 static_assert(kDecSlabBytes + kDecSumBytes + 128 <= kLdsPerCu, "decode LDS");
@@ -521,6 +521,7 @@ static_assert(kDecSlabBytes + kDecSumBytes + sizeof(DecPlan) + sizeof(int32_t) *
 
 // Pieces [b0, b1) of the plan run together: every piece gets one wave, the
 // other waves are shared out in proportion to the pieces' chunks.
+template <int NW>
 __device__ __forceinline__ void share_waves(DecPlan& plan, int b0, int b1) {
   const int nb = b1 - b0;
   uint32_t tot = 0;
@@ -528,16 +529,16 @@ __device__ __forceinline__ void share_waves(DecPlan& plan, int b0, int b1) {
   uint32_t cum = 0;
   for (int i = b0; i < b1; ++i) {
     DecPiece& p = plan.piece[i];
-    p.w0 = (i - b0) + (int)(((unsigned long long)(kDecWaves - nb) * cum) / tot);
+    p.w0 = (i - b0) + (int)(((unsigned long long)(NW - nb) * cum) / tot);
     cum += (uint32_t)(p.u1 - p.u0) * p.C;
-    p.w1 = (i - b0) + 1 + (int)(((unsigned long long)(kDecWaves - nb) * cum) / tot);
+    p.w1 = (i - b0) + 1 + (int)(((unsigned long long)(NW - nb) * cum) / tot);
   }
 }
 
 // Plans pieces from pos on (wave 0): up to kDecMaxPieces of them, the first
 // from the cached lanes x0 when pos == lo; then groups consecutive pieces
 // whose slabs fit the LDS together into batches.
-template <int GPC>
+template <int GPC, int NW>
 __device__ __forceinline__ void plan_round(const LayerArgs& L, const DecodeArgs& a, const DecLane* x0,
                                            uint32_t incl0, int R, int ntiles, uint32_t lo, uint32_t hi,
                                            uint32_t pos, DecPlan& plan) {
@@ -558,8 +559,8 @@ __device__ __forceinline__ void plan_round(const LayerArgs& L, const DecodeArgs&
       DecPiece& p = plan.piece[i];
       const int slab = (((p.nt + 1) * (p.C * kTileCols + kRowPad) * 2) + 15) & ~15;
       const int sum = kDecTok * p.C * GPC * 4;
-      if (i > b0 && (used_slab + slab > kDecSlabBytes || used_sum + sum > kDecSumBytes || i - b0 >= kDecWaves)) {
-        share_waves(plan, b0, i);
+      if (i > b0 && (used_slab + slab > kDecSlabBytes || used_sum + sum > kDecSumBytes || i - b0 >= NW)) {
+        share_waves<NW>(plan, b0, i);
         b0 = i;
         ++batch;
         used_slab = used_sum = 0;
@@ -570,7 +571,7 @@ __device__ __forceinline__ void plan_round(const LayerArgs& L, const DecodeArgs&
       used_slab += slab;
       used_sum += sum;
     }
-    if (n > 0) share_waves(plan, b0, n);
+    if (n > 0) share_waves<NW>(plan, b0, n);
     plan.n = n;
     plan.nbatch = n > 0 ? batch + 1 : 0;
     plan.more = pos < hi;
@@ -578,9 +579,10 @@ __device__ __forceinline__ void plan_round(const LayerArgs& L, const DecodeArgs&
   }
 }
 
-template <int GPC, bool GATEUP>
-__global__ void __launch_bounds__(64 * kDecWaves) __attribute__((amdgpu_waves_per_eu(4)))
+template <int GPC, bool GATEUP, int NW>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4)))
 decode_kernel(LayerArgs L, DecodeArgs a) {
+  static_assert(NW >= 2 && NW <= kDecWaves, "waves of the decode workgroup");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   // the workgroup's pieces, planned by wave 0 (the other waves would only
   // repeat the same scalar work on their SIMDs)
@@ -606,9 +608,9 @@ decode_kernel(LayerArgs L, DecodeArgs a) {
     const uint32_t q = total / (uint32_t)a.nwg, rm = total % (uint32_t)a.nwg;
     lo = q * blockIdx.x + (rm * blockIdx.x) / a.nwg;
     hi = q * (blockIdx.x + 1) + (rm * (blockIdx.x + 1)) / a.nwg;
-    plan_round<GPC>(L, a, &x0, incl0, R, ntiles, lo, hi, lo, plan);
+    plan_round<GPC, NW>(L, a, &x0, incl0, R, ntiles, lo, hi, lo, plan);
   } else if (GATEUP) {
-    for (int i = (wave - 1) * 64 + lane; i < a.P; i += (kDecWaves - 1) * 64) s_tok[i] = a.pair_token[i];
+    for (int i = (wave - 1) * 64 + lane; i < a.P; i += (NW - 1) * 64) s_tok[i] = a.pair_token[i];
   }
   __syncthreads();
   for (;;) {
@@ -629,20 +631,34 @@ decode_kernel(LayerArgs L, DecodeArgs a) {
     }
     if (!more) break;
     __syncthreads();                 // every wave has read the plan and left the slab
-    if (wave == 0) plan_round<GPC>(L, a, nullptr, 0, R, ntiles, lo, hi, plan.pos, plan);
+    if (wave == 0) plan_round<GPC, NW>(L, a, nullptr, 0, R, ntiles, lo, hi, plan.pos, plan);
     __syncthreads();
   }
 }
 
-template <int GPC, bool GATEUP>
-hipError_t launch_decode(const LayerArgs& L, const DecodeArgs& a, hipStream_t stream) {
+// Waves of the decode workgroup.  Small batches, whose items hold one or two
+// tokens, run best with 8 (each wave streams twice the chunks and the
+// per-piece set-up, staging and tail reduction are shared by fewer waves);
+// larger ones with 16, whose staging and reductions of the fuller slabs go
+// faster on more waves.  Measured on the Mixtral- and OLMoE-shaped layers:
+// 8 waves win for gate/up up to 8 tokens, for down up to 4.
+inline int decode_waves(bool gateup, int T) { return T <= (gateup ? 8 : 4) ? 8 : 16; }
+
+template <int GPC, bool GATEUP, int NW>
+hipError_t launch_decode_nw(const LayerArgs& L, const DecodeArgs& a, hipStream_t stream) {
   constexpr int lds = kDecSlabBytes + kDecSumBytes;
   // set once per instantiation (thread-safe static initialisation)
-  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&decode_kernel<GPC, GATEUP>),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&decode_kernel<GPC, GATEUP, NW>), hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((decode_kernel<GPC, GATEUP>), dim3(a.nwg), dim3(64 * kDecWaves), lds, stream, L, a);
+  hipLaunchKernelGGL((decode_kernel<GPC, GATEUP, NW>), dim3(a.nwg), dim3(64 * NW), lds, stream, L, a);
   return hipGetLastError();
+}
+
+template <int GPC, bool GATEUP>
+hipError_t launch_decode(const LayerArgs& L, const DecodeArgs& a, hipStream_t stream) {
+  return decode_waves(GATEUP, a.T) == 8 ? launch_decode_nw<GPC, GATEUP, 8>(L, a, stream)
+                                        : launch_decode_nw<GPC, GATEUP, 16>(L, a, stream);
 }
 
 }  // namespace mc
