@@ -5,8 +5,7 @@
 
 namespace mc {
 
-constexpr int kRouteFusedMaxT = 64;    // up to this many tokens routing runs in one launch...
-constexpr int kRouteFusedMaxTE = 512;  // ...while T * E stays within this (one workgroup selects every token)
+constexpr int kRouteFusedMaxT = 64;    // up to this many tokens routing may run in one launch
 constexpr int kDecodeMaxT = 64;        // up to this many tokens one workgroup holds all of an expert's tokens
 
 enum TimingSite {

@@ -117,11 +117,19 @@ __global__ void __launch_bounds__(kCsrThreads) route_scatter_kernel(
               pair_w, pair_pos);
 }
 
-// Small batches (T <= 64 tokens and T * E <= 512, so that one workgroup's
-// selections stay short: measured at 64 experts, 32 tokens take 20 us here
-// against 11.5 us in the two-launch path): one launch.  The waves select
-// tokens in parallel (the selections kept in LDS), then wave 0 builds the
-// lists (small_batch_lists).
+// Small batches run in one launch: at most kRouteFusedMaxT tokens (a lane per
+// token in the lists) that one round of the workgroup's 16 waves selects
+// (64/S tokens a wave; measured: 64 experts, 16 tokens: 8.6 us against 11.0
+// in two launches).  With more than 64 experts a lane ranks several keys and
+// a selection is slower: there T * E <= 512 (as measured at 64 experts before
+// the ranks were batched: 32 tokens took 20 us against 11.5 in two launches).
+// Larger batches spread the selections over many CUs.
+__host__ __device__ constexpr bool route_fused_fits(int T, int E) {
+  return T <= kRouteFusedMaxT && (E <= 64 ? T <= (kCsrThreads / 64) * (64 / sel_segment(E)) : T * E <= 512);
+}
+
+// The small-batch kernel: the waves select the tokens side by side (the
+// selections kept in LDS), then wave 0 builds the lists (small_batch_lists).
 __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
     const float* __restrict__ logits, const uint8_t* __restrict__ important, int T, int E, int k,
     float delta32, double tau, int32_t* topk_idx, float* topk_w, uint8_t* kept, int32_t* counts,
@@ -137,8 +145,8 @@ __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
   const int wave = wave_id(), nwaves = blockDim.x >> 6;
   const SelScratch sc = sel_scratch(scratch[wave]);
   const int S = sel_segment(E), ns = 64 / S;
-  // a wave selects ns tokens at once; T * E <= kRouteFusedMaxTE makes one
-  // round of the 16 waves enough
+  // a wave selects ns tokens at once; route_fused_fits makes one round of
+  // the 16 waves enough
   for (int t0 = wave * ns; t0 < T; t0 += nwaves * ns) {
     const int t = t0 + (threadIdx.x & 63) / S;
     const SelInput in = sel_load(logits, important, t, T, E, S);
@@ -152,7 +160,7 @@ __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
 
 hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,
                         const mc_routing& r, hipStream_t stream) {
-  if (r.T <= kRouteFusedMaxT && r.T * r.E <= kRouteFusedMaxTE) {
+  if (route_fused_fits(r.T, r.E)) {
     timing_begin(stream, kSiteRouteFused);
     hipLaunchKernelGGL(route_fused_kernel, dim3(1), dim3(kCsrThreads), 0, stream, logits,
                        important, r.T, r.E, r.k, delta32, tau, r.topk_idx, r.topk_w, r.kept,

@@ -92,6 +92,26 @@ static __device__ void select_token(const SelInput& in, int t, int T, int E, int
   __builtin_amdgcn_wave_barrier();
   const int nj = (E + S - 1) / S;                    // keys per lane (wave-uniform)
   int e2 = 0;
+  if (nj == 1) {
+    // one key per lane (E <= 64): sixteen broadcast reads in flight per wait
+    int r0 = 0;
+    for (; e2 + 16 <= E; e2 += 16) {
+      unsigned long long o[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) o[u] = sc.key[kb + e2 + u];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) r0 += o[u] > key[0] ? 1 : 0;
+    }
+    for (; e2 + 4 <= E; e2 += 4) {
+      unsigned long long o[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) o[u] = sc.key[kb + e2 + u];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) r0 += o[u] > key[0] ? 1 : 0;
+    }
+    for (; e2 < E; ++e2) r0 += sc.key[kb + e2] > key[0] ? 1 : 0;
+    rank[0] = r0;
+  }
   for (; e2 + 4 <= E; e2 += 4) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {

@@ -166,6 +166,7 @@ def test_route_edge_cases(mc):
     (64, 2, 2, 0.3), (200, 2, 2, 0.3),     # 32 tokens per wavefront
     (31, 16, 4, 0.2), (500, 16, 4, 0.2),
     (15, 33, 3, 0.3), (70, 33, 3, 0.3),    # one 64-lane segment, 31 lanes idle
+    (48, 16, 4, 0.2), (16, 33, 3, 0.3),    # one launch: one round of the 16 waves (T * E > 512)
 ])
 def test_route_lane_segments(mc, T, E, k, tau):
     """Tokens selected side by side in segments of a wavefront (small batches
