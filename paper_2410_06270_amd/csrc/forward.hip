@@ -23,26 +23,49 @@ __device__ __forceinline__ f32x4 combine4(const float* __restrict__ partial, siz
     acc[2] = bf16_bits_to_float(rv.y & 0xffffu);
     acc[3] = bf16_bits_to_float(rv.y >> 16);
   }
-  for (int r = 0; r < k; ++r) {
-    const int pos = checked_pos(pair_pos[(size_t)t * k + r], P);
-    if (pos < 0) continue;
-    const float w = topk_w[(size_t)t * k + r];
-    f32x4 sum;
-    if constexpr (NSPLIT == 0) {
-      sum = *reinterpret_cast<const f32x4*>(partial + (size_t)pos * d + i);
-      for (int s = 1; s < nsplit; ++s)
-        sum += *reinterpret_cast<const f32x4*>(partial + s * part_stride + (size_t)pos * d + i);
-    } else {
-      f32x4 v[NSPLIT];
+  // every rank's list position and weight are loaded first, then the rows
+  // of RB ranks at a time (absent ranks read row 0, in bounds, and are
+  // dropped), so that the rows' loads do not wait on one another; the sums
+  // still run in rank order
+  int pos[MC_MAX_TOPK];
+  float wr[MC_MAX_TOPK];
 #pragma unroll
-      for (int s = 0; s < NSPLIT; ++s)
-        v[s] = *reinterpret_cast<const f32x4*>(partial + s * part_stride + (size_t)pos * d + i);
-      sum = v[0];
+  for (int r = 0; r < MC_MAX_TOPK; ++r) {
+    pos[r] = r < k ? checked_pos(pair_pos[(size_t)t * k + r], P) : -1;
+    wr[r] = r < k ? topk_w[(size_t)t * k + r] : 0.0f;
+  }
+  if constexpr (NSPLIT == 0) {
 #pragma unroll
-      for (int s = 1; s < NSPLIT; ++s) sum += v[s];
+    for (int r = 0; r < MC_MAX_TOPK; ++r) {
+      if (pos[r] < 0) continue;
+      const float* row = partial + (size_t)pos[r] * d + i;
+      f32x4 sum = *reinterpret_cast<const f32x4*>(row);
+      for (int s = 1; s < nsplit; ++s) sum += *reinterpret_cast<const f32x4*>(row + s * part_stride);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[c] = fmaf(wr[r], sum[c], acc[c]);
     }
+  } else {
+    constexpr int RB = NSPLIT <= 4 ? 4 : 2;   // ranks in flight (RB * NSPLIT rows of 16 bytes)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) acc[c] = fmaf(w, sum[c], acc[c]);
+    for (int r0 = 0; r0 < MC_MAX_TOPK; r0 += RB) {
+      if (r0 >= k) break;
+      f32x4 v[RB][NSPLIT];
+#pragma unroll
+      for (int j = 0; j < RB; ++j) {
+        const float* row = partial + (size_t)(pos[r0 + j] >= 0 ? pos[r0 + j] : 0) * d + i;
+#pragma unroll
+        for (int s = 0; s < NSPLIT; ++s) v[j][s] = *reinterpret_cast<const f32x4*>(row + s * part_stride);
+      }
+#pragma unroll
+      for (int j = 0; j < RB; ++j) {
+        if (pos[r0 + j] < 0) continue;
+        f32x4 sum = v[j][0];
+#pragma unroll
+        for (int s = 1; s < NSPLIT; ++s) sum += v[j][s];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c] = fmaf(wr[r0 + j], sum[c], acc[c]);
+      }
+    }
   }
   return acc;
 }
