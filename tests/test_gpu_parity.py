@@ -276,8 +276,8 @@ def test_forward_max_tokens_sampled(mc, tiny):
     (1, 4, 384, 256, 257, None),      # d not a multiple of the 256-row down tile
     (1, 4, 256, 512, 600, 1),         # one expert takes every token: 600 + ~rest, 3 m-tiles
     (4, 16, 2048, 1024, 300, None),   # G = 64, 16 experts, top-8, ragged experts
-    (1, 4, 256, 384, 300, None),      # ffn % 256 = 128: the last gate/up row tile is half full
-    (1, 4, 256, 128, 300, None),      # ffn = 128: one half-full gate/up row tile
+    (1, 4, 256, 384, 300, None),      # ffn = 384: three 128-row gate/up tiles (ffn % 256 = 128)
+    (1, 4, 256, 128, 300, None),      # ffn = 128: a single gate/up row tile
 ])
 def test_forward_prefill_shapes(mc, cid, E, d, ffn, T, hot):
     """Batches above 64 tokens go through the grouped GEMMs: partial 256-token
