@@ -274,7 +274,7 @@ def test_forward_max_tokens_sampled(mc, tiny):
 @pytest.mark.parametrize("cid,E,d,ffn,T,hot", [
     (1, 4, 256, 512, 300, None),      # G = 32, ragged 32-row fragments
     (1, 4, 384, 256, 257, None),      # d not a multiple of the 256-row down tile
-    (1, 4, 256, 512, 600, 1),         # one expert takes every token: 600 + ~rest, 3 m-tiles
+    (1, 4, 256, 512, 600, 1),         # one expert takes every token: 600+ pairs, five 128-token m-tiles
     (4, 16, 2048, 1024, 300, None),   # G = 64, 16 experts, top-8, ragged experts
     (1, 4, 256, 384, 300, None),      # ffn = 384: three 128-row gate/up tiles (ffn % 256 = 128)
     (1, 4, 256, 128, 300, None),      # ffn = 128: a single gate/up row tile
