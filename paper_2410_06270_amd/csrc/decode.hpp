@@ -495,9 +495,16 @@ __device__ __forceinline__ void decode_piece(const LayerArgs& L, const DecodeArg
 
   const uint16_t* arow = ((lane & 15) < nt ? xs + (size_t)(lane & 15) * RS : zrow) + 8 * (lane >> 4);
   // ring depth: the deepest that divides C, so that ring slot j always holds
-  // chunk c + j of a unit and the unrolled loop needs no remainder
+  // chunk c + j of a unit and the unrolled loop needs no remainder.  The
+  // waves' parts are whole groups of D chunks, so a small piece (a few groups
+  // per wave) is shared out unevenly: there the shallower ring halves the
+  // grain (measured on the OLMoE-shaped layer, 92 chunks a workgroup at 16
+  // tokens: gate/up 20.4 -> 18.9 us).  With 8 waves or fewer the shallow
+  // ring keeps too few bytes in flight, so it takes a smaller piece to pay.
   constexpr int DM = prefetch_depth(1, GPC);
-  if (C % DM == 0)
+  const int nchunks = (u1 - u0) * C, nwp = p.w1 - p.w0;
+  const bool deep = DM == 2 || nchunks >= (nwp > 8 ? 4 : 3) * DM * nwp;
+  if (C % DM == 0 && deep)
     decode_run<BITS, GPC, F16, DM>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage_early, stage_late, emit);
   else if (C % 2 == 0)
     decode_run<BITS, GPC, F16, 2>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage_early, stage_late, emit);
