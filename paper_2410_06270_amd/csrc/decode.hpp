@@ -499,14 +499,16 @@ __device__ __forceinline__ void decode_piece(const LayerArgs& L, const DecodeArg
   // waves' parts are whole groups of D chunks, so a small piece (a few groups
   // per wave) is shared out unevenly: there the shallower ring halves the
   // grain (measured on the OLMoE-shaped layer, 92 chunks a workgroup at 16
-  // tokens: gate/up 20.4 -> 18.9 us).  With 8 waves or fewer the shallow
-  // ring keeps too few bytes in flight, so it takes a smaller piece to pay.
+  // tokens: gate/up 20.4 -> 18.9 us), and below two groups of two chunks a
+  // wave the one-chunk ring (down there, 46 chunks a workgroup: 14.6 ->
+  // 13.9 us).  With 8 waves or fewer the shallow ring keeps too few bytes in
+  // flight, so it takes a smaller piece to pay.
   constexpr int DM = prefetch_depth(1, GPC);
   const int nchunks = (u1 - u0) * C, nwp = p.w1 - p.w0;
   const bool deep = DM == 2 || nchunks >= (nwp > 8 ? 4 : 3) * DM * nwp;
   if (C % DM == 0 && deep)
     decode_run<BITS, GPC, F16, DM>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage_early, stage_late, emit);
-  else if (C % 2 == 0)
+  else if (C % 2 == 0 && nchunks >= 2 * 2 * nwp)
     decode_run<BITS, GPC, F16, 2>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage_early, stage_late, emit);
   else
     decode_run<BITS, GPC, F16, 1>(g, u0, u1, C, p.w0, p.w1, arow, sxs, tails, stage_early, stage_late, emit);
