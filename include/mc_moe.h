@@ -266,8 +266,11 @@ mc_status mc_moe_route_forward(const uint16_t *x_bf16, const float *logits, cons
                                void *workspace, size_t ws_bytes, void *stream);
 
 /* Workspace bytes mc_moe_stack_forward needs: the normalised layer input
- * (T*d bf16, rounded up to 256 bytes) + mc_forward_workspace.
- * Errors: MC_EINVAL. */
+ * (T*d bf16, rounded up to 256 bytes); for batches that route in one
+ * workgroup (T <= 64 and T <= 16*64/S, S the least power of two >= E, up to
+ * 64 experts; T*E <= 512 above) the routing buffers of 8 layers, which are
+ * then routed together (each buffer rounded up to 256 bytes); and
+ * mc_forward_workspace.  Errors: MC_EINVAL. */
 mc_status mc_stack_workspace(int T, int E, int k, int d, int ffn, size_t *bytes);
 
 /* A stack of n_layers MoE layers joined by residual connections: the expert

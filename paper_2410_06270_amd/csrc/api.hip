@@ -501,9 +501,11 @@ mc_status mc_moe_stack_forward(const uint16_t* x_bf16, int n_layers, const mc_la
     return fail(MC_EINVAL, "x, y and tmp must not overlap");
   const size_t need = mc::stack_workspace_bytes(r->T, r->E, r->k, layers[0].d, layers[0].ffn);
   if (ws_bytes < need) return fail(MC_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+  const int T = r->T, E = r->E, k = r->k;
   uint16_t* xn = static_cast<uint16_t*>(workspace);
-  void* fws = static_cast<char*>(workspace) + (need - mc::forward_workspace_bytes(r->T, r->E, r->k,
-                                                                                   layers[0].d, layers[0].ffn));
+  char* sets = static_cast<char*>(workspace) + ((size_t)T * layers[0].d * sizeof(uint16_t) + 255) / 256 * 256;
+  void* fws = static_cast<char*>(workspace) + (need - mc::forward_workspace_bytes(T, E, k, layers[0].d,
+                                                                                   layers[0].ffn));
   const double tau = (double)threshold;
   const float delta32 = prune_delta32(tau);
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -511,18 +513,36 @@ mc_status mc_moe_stack_forward(const uint16_t* x_bf16, int n_layers, const mc_la
   const uint16_t* in = x_bf16;
   // layer 0's input is normalised here; every later layer's input is formed
   // by the previous layer's combine (same bytes as a separate RMSNorm launch)
-  s = hip_status(mc::launch_rmsnorm(in, r->T, layers[0].d, mc::kRmsNormEps, xn, st),
+  s = hip_status(mc::launch_rmsnorm(in, T, layers[0].d, mc::kRmsNormEps, xn, st),
                  "mc_moe_stack_forward rmsnorm launch");
   if (s != MC_OK) return s;
-  for (int l = 0; l < n_layers; ++l) {
-    uint16_t* out = ((n_layers - 1 - l) % 2 == 0) ? y_bf16 : tmp_bf16;
-    const size_t te = (size_t)l * r->T;
-    const mc::RouteArgs ra{logits + te * r->E, important ? important + te : nullptr, delta32, tau};
-    s = hip_status(mc::launch_forward(xn, layer_args(&layers[l]), *r, out, fws, in, st, &ra,
-                                      l + 1 < n_layers ? xn : nullptr),
-                   "mc_moe_stack_forward forward launch");
-    if (s != MC_OK) return s;
-    in = out;
+  // A layer's routing depends on its own logits only: small batches route
+  // kRouteBatch layers in one launch, each into a routing set of the
+  // workspace (the last layer into r), before those layers run.
+  const bool batch_routes = mc::route_batch_fits(T, E);
+  mc_routing rs[mc::kRouteBatch];
+  for (int l0 = 0; l0 < n_layers; l0 += mc::kRouteBatch) {
+    const int nb = n_layers - l0 < mc::kRouteBatch ? n_layers - l0 : mc::kRouteBatch;
+    if (batch_routes) {
+      for (int b = 0; b < nb; ++b)
+        rs[b] = (l0 + b == n_layers - 1) ? *r : mc::routing_set(sets + b * mc::routing_set_bytes(T, E, k), T, E, k);
+      const size_t te = (size_t)l0 * T;
+      s = hip_status(mc::launch_route_batch(logits + te * E, important ? important + te : nullptr, delta32,
+                                            tau, rs, nb, st),
+                     "mc_moe_stack_forward routing launch");
+      if (s != MC_OK) return s;
+    }
+    for (int l = l0; l < l0 + nb; ++l) {
+      uint16_t* out = ((n_layers - 1 - l) % 2 == 0) ? y_bf16 : tmp_bf16;
+      const size_t te = (size_t)l * T;
+      const mc::RouteArgs ra{logits + te * E, important ? important + te : nullptr, delta32, tau};
+      s = hip_status(mc::launch_forward(xn, layer_args(&layers[l]), batch_routes ? rs[l - l0] : *r, out, fws,
+                                        in, st, batch_routes ? nullptr : &ra,
+                                        l + 1 < n_layers ? xn : nullptr),
+                     "mc_moe_stack_forward forward launch");
+      if (s != MC_OK) return s;
+      in = out;
+    }
   }
   return MC_OK;
 }

@@ -226,8 +226,39 @@ size_t forward_workspace_bytes(int T, int E, int k, int d, int ffn) {
   return h + gu + part;
 }
 
+size_t routing_set_bytes(int T, int E, int k) {
+  const size_t P = (size_t)T * k;
+  return 6 * round256(P * 4) + round256(P) + round256((size_t)E * 4) + round256(((size_t)E + 1) * 4) + 256;
+}
+
+mc_routing routing_set(void* base, int T, int E, int k) {
+  const size_t P = (size_t)T * k;
+  char* p = static_cast<char*>(base);
+  auto take = [&](size_t bytes) {
+    void* q = p;
+    p += round256(bytes);
+    return q;
+  };
+  mc_routing r;
+  r.T = T;
+  r.E = E;
+  r.k = k;
+  r.topk_idx = static_cast<int32_t*>(take(P * 4));
+  r.topk_w = static_cast<float*>(take(P * 4));
+  r.kept = static_cast<uint8_t*>(take(P));
+  r.counts = static_cast<int32_t*>(take((size_t)E * 4));
+  r.offsets = static_cast<int32_t*>(take(((size_t)E + 1) * 4));
+  r.pair_token = static_cast<int32_t*>(take(P * 4));
+  r.pair_rank = static_cast<int32_t*>(take(P * 4));
+  r.pair_w = static_cast<float*>(take(P * 4));
+  r.pair_pos = static_cast<int32_t*>(take(P * 4));
+  r.n_pruned = static_cast<int32_t*>(take(4));
+  return r;
+}
+
 size_t stack_workspace_bytes(int T, int E, int k, int d, int ffn) {
-  return round256((size_t)T * d * sizeof(uint16_t)) + forward_workspace_bytes(T, E, k, d, ffn);
+  const size_t routes = route_batch_fits(T, E) ? (size_t)kRouteBatch * routing_set_bytes(T, E, k) : 0;
+  return round256((size_t)T * d * sizeof(uint16_t)) + routes + forward_workspace_bytes(T, E, k, d, ffn);
 }
 
 static hipError_t launch_combine(const float* partial, size_t part_stride, int nsplit,

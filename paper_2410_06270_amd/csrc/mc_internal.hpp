@@ -27,6 +27,31 @@ hipError_t launch_export(const uint32_t* words, const uint32_t* sz, int bits, in
                          bool dequant, void* out, hipStream_t stream);
 hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,
                         const mc_routing& r, hipStream_t stream);
+// The device buffers of one routing result (those of mc_routing).
+struct RouteBufs {
+  int32_t* topk_idx;
+  float* topk_w;
+  uint8_t* kept;
+  int32_t *counts, *offsets, *pair_token, *pair_rank;
+  float* pair_w;
+  int32_t *pair_pos, *n_pruned;
+};
+constexpr int kRouteBatch = 8;          // batches routed by one launch_route_batch
+struct RouteBatch {
+  RouteBufs r[kRouteBatch];
+};
+// Whether launch_route_batch takes batches of T tokens over E experts (the
+// one-workgroup routing of small batches).
+bool route_batch_fits(int T, int E);
+// Routes nb <= kRouteBatch batches of the same shape (rs[b].T, E, k equal) in
+// one launch: batch b's logits at logits + b*T*E, its flags at important +
+// b*T (or none), its results into rs[b] as launch_route writes them.
+hipError_t launch_route_batch(const float* logits, const uint8_t* important, float delta32, double tau,
+                              const mc_routing* rs, int nb, hipStream_t stream);
+// Bytes of one set of routing buffers for T tokens (each buffer 256-aligned),
+// and the set laid out at base.
+size_t routing_set_bytes(int T, int E, int k);
+mc_routing routing_set(void* base, int T, int E, int k);
 int forward_nsplit(int T, int E, int k, int d, int ffn);
 int forward_ksplit(int T, int E, int k, int d, int ffn);
 size_t forward_workspace_bytes(int T, int E, int k, int d, int ffn);
@@ -71,7 +96,9 @@ hipError_t launch_forward(const uint16_t* x, const LayerArgs& L, const mc_routin
 // Stack of layers: xn = RMSNorm(h) (fp64, one bf16 rounding) before each layer.
 constexpr double kRmsNormEps = 1e-5;
 hipError_t launch_rmsnorm(const uint16_t* h, int T, int d, double eps, uint16_t* xn, hipStream_t stream);
-size_t stack_workspace_bytes(int T, int E, int k, int d, int ffn);   // xn [T][d] + forward workspace
+// xn [T][d], the routing sets of kRouteBatch layers when route_batch_fits,
+// and the forward workspace.
+size_t stack_workspace_bytes(int T, int E, int k, int d, int ffn);
 // logits [T][E] fp32 = x [T][d] . w [E][d]^T (bf16), fp64 sums rounded once.
 hipError_t launch_router(const uint16_t* x, const uint16_t* w, int T, int d, int E, float* logits,
                          hipStream_t stream);

@@ -128,13 +128,12 @@ __host__ __device__ constexpr bool route_fused_fits(int T, int E) {
   return T <= kRouteFusedMaxT && (E <= 64 ? T <= (kCsrThreads / 64) * (64 / sel_segment(E)) : T * E <= 512);
 }
 
-// The small-batch kernel: the waves select the tokens side by side (the
-// selections kept in LDS), then wave 0 builds the lists (small_batch_lists).
-__global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
-    const float* __restrict__ logits, const uint8_t* __restrict__ important, int T, int E, int k,
-    float delta32, double tau, int32_t* topk_idx, float* topk_w, uint8_t* kept, int32_t* counts,
-    int32_t* offsets, int32_t* pair_token, int32_t* pair_rank, float* pair_w, int32_t* pair_pos,
-    int32_t* n_pruned) {
+// The small-batch routing of one batch (a workgroup): the waves select the
+// tokens side by side (the selections kept in LDS), then wave 0 builds the
+// lists (small_batch_lists).
+__device__ __forceinline__ void route_fused_body(const float* __restrict__ logits,
+                                                 const uint8_t* __restrict__ important, int T, int E, int k,
+                                                 float delta32, double tau, const RouteBufs& o) {
   static_assert(kRouteFusedMaxT <= 64, "one lane per token");
   __shared__ uint16_t ent[kRouteFusedMaxT * MC_MAX_TOPK];
   __shared__ float wsel[kRouteFusedMaxT * MC_MAX_TOPK];
@@ -150,12 +149,50 @@ __global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
   for (int t0 = wave * ns; t0 < T; t0 += nwaves * ns) {
     const int t = t0 + (threadIdx.x & 63) / S;
     const SelInput in = sel_load(logits, important, t, T, E, S);
-    select_token(in, t, T, E, S, k, delta32, tau, topk_idx, topk_w, kept, pair_pos, true, ent, wsel, sc);
+    select_token(in, t, T, E, S, k, delta32, tau, o.topk_idx, o.topk_w, o.kept, o.pair_pos, true, ent, wsel,
+                 sc);
   }
   __syncthreads();
   if (wave != 0) return;
   const RouteLds s{ent, wsel, cnt, base, bal};
-  small_batch_lists(T, E, k, s, true, counts, offsets, pair_token, pair_rank, pair_w, pair_pos, n_pruned);
+  small_batch_lists(T, E, k, s, true, o.counts, o.offsets, o.pair_token, o.pair_rank, o.pair_w, o.pair_pos,
+                    o.n_pruned);
+}
+
+__global__ void __launch_bounds__(kCsrThreads) route_fused_kernel(
+    const float* __restrict__ logits, const uint8_t* __restrict__ important, int T, int E, int k,
+    float delta32, double tau, RouteBufs o) {
+  route_fused_body(logits, important, T, E, k, delta32, tau, o);
+}
+
+// Several batches of the same shape at once, one workgroup each: batch b's
+// logits at logits + b*T*E, its flags at important + b*T (the layers of a
+// stack, whose routing depends only on their own logits).
+__global__ void __launch_bounds__(kCsrThreads) route_fused_batch_kernel(
+    const float* __restrict__ logits, const uint8_t* __restrict__ important, int T, int E, int k,
+    float delta32, double tau, RouteBatch o) {
+  const size_t b = blockIdx.x;
+  route_fused_body(logits + b * T * E, important ? important + b * T : nullptr, T, E, k, delta32, tau,
+                   o.r[b]);
+}
+
+static RouteBufs route_bufs(const mc_routing& r) {
+  return RouteBufs{r.topk_idx, r.topk_w, r.kept, r.counts, r.offsets, r.pair_token, r.pair_rank, r.pair_w,
+                   r.pair_pos, r.n_pruned};
+}
+
+bool route_batch_fits(int T, int E) { return route_fused_fits(T, E); }
+
+hipError_t launch_route_batch(const float* logits, const uint8_t* important, float delta32, double tau,
+                              const mc_routing* rs, int nb, hipStream_t stream) {
+  if (nb < 1 || nb > kRouteBatch || !route_fused_fits(rs[0].T, rs[0].E)) return hipErrorInvalidValue;
+  RouteBatch o;
+  for (int b = 0; b < nb; ++b) o.r[b] = route_bufs(rs[b]);
+  timing_begin(stream, kSiteRouteFused);
+  hipLaunchKernelGGL(route_fused_batch_kernel, dim3(nb), dim3(kCsrThreads), 0, stream, logits, important,
+                     rs[0].T, rs[0].E, rs[0].k, delta32, tau, o);
+  timing_end(stream, kSiteRouteFused);
+  return hipGetLastError();
 }
 
 hipError_t launch_route(const float* logits, const uint8_t* important, float delta32, double tau,
@@ -163,9 +200,7 @@ hipError_t launch_route(const float* logits, const uint8_t* important, float del
   if (route_fused_fits(r.T, r.E)) {
     timing_begin(stream, kSiteRouteFused);
     hipLaunchKernelGGL(route_fused_kernel, dim3(1), dim3(kCsrThreads), 0, stream, logits,
-                       important, r.T, r.E, r.k, delta32, tau, r.topk_idx, r.topk_w, r.kept,
-                       r.counts, r.offsets, r.pair_token, r.pair_rank, r.pair_w, r.pair_pos,
-                       r.n_pruned);
+                       important, r.T, r.E, r.k, delta32, tau, route_bufs(r));
     timing_end(stream, kSiteRouteFused);
     return hipGetLastError();
   }

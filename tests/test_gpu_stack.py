@@ -126,6 +126,41 @@ def test_stack_call_equals_chain_of_layers(mc, small_stack, T):
     np.testing.assert_array_equal(three, h3)
 
 
+@pytest.mark.parametrize("T,n", [(1, 8), (8, 11), (64, 17), (130, 9)])
+def test_stack_many_layers_equals_chain(mc, small_stack, T, n):
+    """More layers than one routing launch covers (small batches route 8
+    layers at a time, each into its own buffers, the last layer into r): the
+    n-layer call equals the chain of one-layer calls bit for bit, and r then
+    holds the last layer's routing as mc_route_and_prune writes it.  The four
+    packed layers are reused in turn; every layer has its own logits and
+    protected tokens."""
+    E, d, ffn, k = SMALL["E"], SMALL["d"], SMALL["ffn"], SMALL["k"]
+    x = synthetic.activations(1, T, d=d)
+    lgs = [synthetic.stack_logits(5, l, T, E=E) for l in range(n)]
+    masks = [synthetic.stack_mask(5, l, T) for l in range(n)]
+    Ls = [small_stack[l % 4][2] for l in range(n)]
+    r = mc.Routing(T, E, k)
+    y = torch.empty((T, d), dtype=torch.int16, device="cuda")
+    tmp = torch.empty((T, d), dtype=torch.int16, device="cuda")
+    ws = torch.empty(mc.stack_workspace(T, E, k, d, ffn), dtype=torch.uint8, device="cuda")
+    mc.stack_forward(to_dev(x.view(np.int16)), Ls, to_dev(np.stack(lgs)), to_dev(np.stack(masks)), TAU, r, y,
+                     tmp, ws)
+    torch.cuda.synchronize()
+    whole = y.cpu().numpy().view(np.uint16)
+    h = x
+    for l in range(n):
+        h = run_stack(mc, h, [Ls[l]], [lgs[l]], [masks[l]], k, E, d, ffn)
+    np.testing.assert_array_equal(whole, h)
+    ref = mc.Routing(T, E, k)
+    mc.route_and_prune(to_dev(lgs[-1]), to_dev(masks[-1]), TAU, ref)
+    torch.cuda.synchronize()
+    P = int(ref.offsets[E].item())
+    for name in ("topk_idx", "topk_w", "kept", "counts", "offsets", "pair_pos", "n_pruned"):
+        assert torch.equal(getattr(r, name), getattr(ref, name)), name
+    for name in ("pair_token", "pair_rank", "pair_w"):
+        assert torch.equal(getattr(r, name)[:P], getattr(ref, name)[:P]), name
+
+
 def test_stack_rejects_aliased_buffers(mc, small_stack):
     E, d, ffn, k = SMALL["E"], SMALL["d"], SMALL["ffn"], SMALL["k"]
     T = 4
