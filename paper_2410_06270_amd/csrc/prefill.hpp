@@ -181,12 +181,12 @@ __device__ __forceinline__ void pf_stage(unsigned char* stage, const PrefillGemm
 // Group epilogue: tot += s 2^b * acc_g (the scale of this lane's row, word
 // sw).  The zero-point part of the group's term, -(s 2^b (1 + z 2^-b)) * S_g,
 // goes to the correction (PfZero).
-template <int BITS>
+template <int BITS, int NT>
 __device__ __forceinline__ void pf_epilogue(const f32x16 (&acc)[PfCfg::kTiles], uint32_t sw,
                                             f32x16 (&tot)[PfCfg::kTiles]) {
   const float sj = half_bits_to_float(sw & 0xffffu) * (float)(1 << BITS);
 #pragma unroll
-  for (int t = 0; t < PfCfg::kTiles; ++t)
+  for (int t = 0; t < NT; ++t)
 #pragma unroll
     for (int i = 0; i < 16; ++i) tot[t][i] = fmaf(sj, acc[t][i], tot[t][i]);
 }
@@ -198,7 +198,9 @@ __device__ __forceinline__ void pf_epilogue(const f32x16 (&acc)[PfCfg::kTiles], 
 // lane % 32 per fragment row; B: the coefficient of weight row lane % 32).
 // Groups are numbered from the first of the loop's range; take() records one
 // group's operands from the stage and its scale/zero word, and after each
-// odd-numbered group the pair's four MFMAs add into tot.
+// odd-numbered group the pair's MFMAs (one per live fragment row, NT) add
+// into tot.
+template <int NT>
 struct PfZero {
   float a[PfCfg::kTiles];
   float b;
@@ -210,7 +212,7 @@ struct PfZero {
     const float sj = half_bits_to_float(sw & 0xffffu) * (float)(1 << BITS);
     const float cj = fmaf(half_bits_to_float(sw >> 16), 1.0f / (float)(1 << BITS), 1.0f);
 #pragma unroll
-    for (int t = 0; t < PfCfg::kTiles; ++t) {
+    for (int t = 0; t < NT; ++t) {
       const float v = ssum[(t * GPC + q) * 32 + (lane & 31)];
       a[t] = mine ? v : a[t];
     }
@@ -219,14 +221,14 @@ struct PfZero {
   }
   __device__ __forceinline__ void flush(f32x16 (&tot)[PfCfg::kTiles]) {
 #pragma unroll
-    for (int t = 0; t < PfCfg::kTiles; ++t) tot[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[t], b, tot[t], 0, 0, 0);
+    for (int t = 0; t < NT; ++t) tot[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[t], b, tot[t], 0, 0, 0);
   }
   // an odd number of groups leaves half a pair: its other half is zero
   __device__ __forceinline__ void finish(int ngroups, int lane, f32x16 (&tot)[PfCfg::kTiles]) {
     if (ngroups & 1) {
       if (lane >> 5) {
 #pragma unroll
-        for (int t = 0; t < PfCfg::kTiles; ++t) a[t] = 0.0f;
+        for (int t = 0; t < NT; ++t) a[t] = 0.0f;
         b = 0.0f;
       }
       flush(tot);
@@ -235,27 +237,28 @@ struct PfZero {
 };
 
 // MFMAs of group q of the chunk in `stage` with the words `w`: per step the
-// eight codes of this lane's row feed the MFMAs of all kTiles fragment rows.
-// The A fragments of step v+1 are read while the MFMAs of step v run.
-template <int BITS, int GPC, bool BF16>
+// eight codes of this lane's row feed the MFMAs of the NT fragment rows that
+// hold the expert's tokens (the m-tile's others are padding: skipped).  The
+// A fragments of step v+1 are read while the MFMAs of step v run.
+template <int BITS, int GPC, bool BF16, int NT>
 __device__ __forceinline__ void pf_group(const unsigned char* stage, const uint32_t (&w)[2][BITS], int q, int lane,
                                          uint32_t magic, f32x16 (&acc)[PfCfg::kTiles]) {
   constexpr int KV = 8 / GPC;   // MFMA steps per group
   const unsigned char* arow = stage + lane * 16;
   u32x4 a[2][PfCfg::kTiles];
 #pragma unroll
-  for (int t = 0; t < PfCfg::kTiles; ++t) a[0][t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + q * KV) * kPfFragBytes);
+  for (int t = 0; t < NT; ++t) a[0][t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + q * KV) * kPfFragBytes);
 #pragma unroll
   for (int vv = 0; vv < KV; ++vv) {
     const int v = q * KV + vv;
     if (vv + 1 < KV) {
 #pragma unroll
-      for (int t = 0; t < PfCfg::kTiles; ++t)
+      for (int t = 0; t < NT; ++t)
         a[(vv + 1) & 1][t] = *reinterpret_cast<const u32x4*>(arow + (t * 8 + v + 1) * kPfFragBytes);
     }
     const u32x4 b = pf_codes<BITS, BF16>(w[v & 1], v >> 1, magic);
 #pragma unroll
-    for (int t = 0; t < PfCfg::kTiles; ++t) {
+    for (int t = 0; t < NT; ++t) {
       const f32x16 z = {};
       acc[t] = pf_mfma<BF16>(a[vv & 1][t], b, vv == 0 ? z : acc[t]);
     }
@@ -267,24 +270,24 @@ __device__ __forceinline__ void pf_group(const unsigned char* stage, const uint3
   }
 }
 
-template <int BITS, int GPC, bool BF16>
+template <int BITS, int GPC, bool BF16, int NT>
 __device__ __forceinline__ void pf_chunk_body(const unsigned char* __restrict__ cur,
                                               unsigned char* __restrict__ next, const PfStream& sp,
                                               const PrefillGemm& g, int f0, bool late, bool first, int c, int last,
                                               int rel0, int wave, int lane, const uint32_t (&w)[2][BITS],
                                               const uint32_t (&s)[GPC], uint32_t (&nw)[2][BITS],
-                                              uint32_t (&ns)[GPC], uint32_t& ps, uint32_t magic, PfZero& zc,
+                                              uint32_t (&ns)[GPC], uint32_t& ps, uint32_t magic, PfZero<NT>& zc,
                                               f32x16 (&acc)[PfCfg::kTiles], f32x16 (&tot)[PfCfg::kTiles]) {
-  if (late && !first) pf_epilogue<BITS>(acc, ps, tot);
+  if (late && !first) pf_epilogue<BITS, NT>(acc, ps, tot);
   pf_load<BITS, GPC>(nw, ns, sp, c + 1 < last ? c + 1 : last);
   __builtin_amdgcn_sched_barrier(0);   // the words go out before the stage (counted waits)
   pf_stage<GPC>(next, g, f0, c + 2 < last ? c + 2 : last, wave, lane);
 #pragma unroll
   for (int q = 0; q < GPC; ++q) {
-    pf_group<BITS, GPC, BF16>(cur, w, q, lane, magic, acc);
-    if (q < GPC - 1 || !late) pf_epilogue<BITS>(acc, s[q], tot);
+    pf_group<BITS, GPC, BF16, NT>(cur, w, q, lane, magic, acc);
+    if (q < GPC - 1 || !late) pf_epilogue<BITS, NT>(acc, s[q], tot);
     else ps = s[q];
-    zc.take<BITS, GPC>(cur, q, s[q], rel0 + q, lane, tot);
+    zc.template take<BITS, GPC>(cur, q, s[q], rel0 + q, lane, tot);
   }
 }
 
@@ -297,12 +300,12 @@ __device__ __forceinline__ void pf_chunk_body(const unsigned char* __restrict__ 
 // scale word `ps` and its stage, kept by the fourth LDS slot) and defers its
 // own last group's epilogue, so that one wave's epilogue overlaps the other's
 // MFMAs.
-template <int BITS, int GPC, bool BF16>
+template <int BITS, int GPC, bool BF16, int NT>
 __device__ __forceinline__ void pf_chunk(const PfStream& sp, const PrefillGemm& g, int f0, bool late, bool first,
                                          int c, int last, int rel0, int slot, unsigned char* smem, int wave,
                                          int lane, const uint32_t (&w)[2][BITS], const uint32_t (&s)[GPC],
                                          uint32_t (&nw)[2][BITS], uint32_t (&ns)[GPC], uint32_t& ps, uint32_t magic,
-                                         PfZero& zc, f32x16 (&acc)[PfCfg::kTiles], f32x16 (&tot)[PfCfg::kTiles]) {
+                                         PfZero<NT>& zc, f32x16 (&acc)[PfCfg::kTiles], f32x16 (&tot)[PfCfg::kTiles]) {
   using S = PfCfg;
   // Stage c has landed in LDS once at most the loads issued after it (stage
   // c+1) are outstanding; the plain barrier then publishes it (a fenced
@@ -312,13 +315,13 @@ __device__ __forceinline__ void pf_chunk(const PfStream& sp, const PrefillGemm& 
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
   const int slot2 = slot + 2 >= kPfSlots ? slot + 2 - kPfSlots : slot + 2;
-  pf_chunk_body<BITS, GPC, BF16>(smem + slot * S::kStageBytes, smem + slot2 * S::kStageBytes, sp, g, f0, late,
+  pf_chunk_body<BITS, GPC, BF16, NT>(smem + slot * S::kStageBytes, smem + slot2 * S::kStageBytes, sp, g, f0, late,
                                  first, c, last, rel0, wave, lane, w, s, nw, ns, ps, magic, zc, acc, tot);
 }
 
 // Chunks [c_begin, c_end) of the reduction, two per iteration so that the
 // two register sets of weight words alternate without copies.
-template <int BITS, int GPC, bool BF16>
+template <int BITS, int GPC, bool BF16, int NT>
 __device__ __forceinline__ void pf_loop(const PfStream& sp, const PrefillGemm& g, int f0, bool late, int c_begin,
                                         int c_end, unsigned char* smem, int wave, int lane,
                                         f32x16 (&tot)[PfCfg::kTiles]) {
@@ -331,21 +334,33 @@ __device__ __forceinline__ void pf_loop(const PfStream& sp, const PrefillGemm& g
   pf_load<BITS, GPC>(wa, sa, sp, c_begin);
   pf_stage<GPC>(smem, g, f0, c_begin, wave, lane);
   pf_stage<GPC>(smem + S::kStageBytes, g, f0, c_begin + 1 < last ? c_begin + 1 : last, wave, lane);
-  PfZero zc{};
+  PfZero<NT> zc{};
   int slot = 0;
   for (int it = 0, c = c_begin; c < c_end; ++it, c += 2) {
     const int rel0 = it * 2 * GPC;   // even: the parity of a group's number is known per call site
-    pf_chunk<BITS, GPC, BF16>(sp, g, f0, late, c == c_begin, c, last, rel0, slot, smem, wave, lane, wa, sa, wb, sb,
+    pf_chunk<BITS, GPC, BF16, NT>(sp, g, f0, late, c == c_begin, c, last, rel0, slot, smem, wave, lane, wa, sa, wb, sb,
                               ps, magic, zc, acc, tot);
     slot = slot + 1 == kPfSlots ? 0 : slot + 1;
     if (c + 1 < c_end)
-      pf_chunk<BITS, GPC, BF16>(sp, g, f0, late, false, c + 1, last, rel0 + GPC, slot, smem, wave, lane, wb, sb, wa,
+      pf_chunk<BITS, GPC, BF16, NT>(sp, g, f0, late, false, c + 1, last, rel0 + GPC, slot, smem, wave, lane, wb, sb, wa,
                                 sa, ps, magic, zc, acc, tot);
     slot = slot + 1 == kPfSlots ? 0 : slot + 1;
   }
-  if (late) pf_epilogue<BITS>(acc, ps, tot);   // the late waves' deferred last epilogue
+  if (late) pf_epilogue<BITS, NT>(acc, ps, tot);   // the late waves' deferred last epilogue
   zc.finish((c_end - c_begin) * GPC, lane, tot);
   wait_vmcnt<0>();   // the clamped re-reads of the last chunks land before LDS is reused
+}
+
+template <int GPC, bool BF16, int NT>
+__device__ __forceinline__ void pf_loop_bits(int bits, const PfStream& sp, const PrefillGemm& g, int f0, bool late,
+                                             int c_begin, int c_end, unsigned char* smem, int wave, int lane,
+                                             f32x16 (&tot)[PfCfg::kTiles]) {
+  if (bits == 1)
+    pf_loop<1, GPC, BF16, NT>(sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
+  else if (bits == 2)
+    pf_loop<2, GPC, BF16, NT>(sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
+  else
+    pf_loop<3, GPC, BF16, NT>(sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
 }
 
 // Grid: mt_max * n_tiles * nsplit workgroups (m-tile major); workgroups past
@@ -386,12 +401,14 @@ prefill_kernel(LayerArgs L, const int32_t* __restrict__ offsets, PrefillTables t
 #pragma unroll
     for (int i = 0; i < 16; ++i) tot[t][i] = 0.0f;
 
-  if (bits == 1)
-    pf_loop<1, GPC, GATEUP>(sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
-  else if (bits == 2)
-    pf_loop<2, GPC, GATEUP>(sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
+  // the MFMAs cover the fragment rows that hold the expert's tokens: one,
+  // two, or all four (three run as four; their fourth row is padding)
+  if (nmt == 1)
+    pf_loop_bits<GPC, GATEUP, 1>(bits, sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
+  else if (nmt == 2)
+    pf_loop_bits<GPC, GATEUP, 2>(bits, sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
   else
-    pf_loop<3, GPC, GATEUP>(sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
+    pf_loop_bits<GPC, GATEUP, S::kTiles>(bits, sp, g, f0, late, c_begin, c_end, smem, wave, lane, tot);
 
   // D layout: lane holds column n = lane%32 (weight row) and, for i < 16,
   // row m = 8*(i/4) + 4*(lane/32) + i%4 (token) of each 32x32 tile.
