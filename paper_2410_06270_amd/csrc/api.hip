@@ -525,7 +525,8 @@ mc_status mc_moe_stack_forward(const uint16_t* x_bf16, int n_layers, const mc_la
     const int nb = n_layers - l0 < mc::kRouteBatch ? n_layers - l0 : mc::kRouteBatch;
     if (batch_routes) {
       for (int b = 0; b < nb; ++b)
-        rs[b] = (l0 + b == n_layers - 1) ? *r : mc::routing_set(sets + b * mc::routing_set_bytes(T, E, k), T, E, k);
+        rs[b] = (l0 + b == n_layers - 1) ? *r
+                                         : mc::routing_set(sets + b * mc::routing_set_bytes(T, E, k), T, E, k);
       const size_t te = (size_t)l0 * T;
       s = hip_status(mc::launch_route_batch(logits + te * E, important ? important + te : nullptr, delta32,
                                             tau, rs, nb, st),
