@@ -134,6 +134,32 @@ def test_forward_workspace(lib):
     assert lib.mc_forward_workspace(4, 8, 9, 4096, 14336, ctypes.byref(b)) == 1
 
 
+def _round256(b):
+    return (b + 255) // 256 * 256
+
+
+def test_stack_workspace(lib):
+    """mc_stack_workspace = the normalised input + (batches routed by one
+    workgroup: T <= 64 and T <= 16*64/S) the routing buffers of 8 layers +
+    mc_forward_workspace; each routing set is ten buffers rounded to 256 B."""
+    def ws(fn, T, E, k, d, ffn):
+        b = ctypes.c_size_t()
+        assert getattr(lib, fn)(T, E, k, d, ffn, ctypes.byref(b)) == 0
+        return b.value
+
+    def routing_set(T, E, k):
+        P = T * k
+        return 6 * _round256(4 * P) + _round256(P) + _round256(4 * E) + _round256(4 * (E + 1)) + 256
+
+    for T, E, k, d, ffn, batched in ((1, 8, 2, 4096, 14336, True), (64, 8, 2, 4096, 14336, True),
+                                     (16, 64, 8, 2048, 1024, True), (17, 64, 8, 2048, 1024, False),
+                                     (65, 8, 2, 4096, 14336, False), (1024, 8, 2, 4096, 14336, False),
+                                     (4, 100, 8, 512, 1024, True), (6, 100, 8, 512, 1024, False)):
+        fw = ws("mc_forward_workspace", T, E, k, d, ffn)
+        want = _round256(T * d * 2) + (8 * routing_set(T, E, k) if batched else 0) + fw
+        assert ws("mc_stack_workspace", T, E, k, d, ffn) == want, (T, E, k)
+
+
 def test_forward_rejects(lib):
     r = _fake_routing(32, 8, 2)
     L, _keep = _fake_layer()
