@@ -58,12 +58,24 @@ __global__ void __launch_bounds__(256) prefill_setup_kernel(const int32_t* __res
 
 // One workgroup per fragment row f: its 32 routed rows of x (zero past the
 // expert's count) copied into the fragment layout (bf16, unchanged), and the
-// sum of each group of G columns of each row in fp32 (in column order).
-__global__ void __launch_bounds__(256) prefill_gather_kernel(const uint16_t* __restrict__ x, int d, int G, int E,
-                                                             const int32_t* __restrict__ offsets,
-                                                             const int32_t* __restrict__ pair_token,
-                                                             PrefillTables tb, uint16_t* __restrict__ xt,
-                                                             float* __restrict__ xsum) {
+// sum of each group of G columns of each row in fp32.  Column blocks of 512:
+// each wave reads whole rows of the block (64 lanes x 16 consecutive bytes)
+// into a row-major LDS tile and forms the group sums of its pieces (the GP =
+// G/8 lanes of a group add with the DPP butterfly of the decode slabs); then
+// the workgroup writes the block's fragments (contiguous in the fragment
+// layout) from the tile with consecutive 16-byte stores.
+constexpr int kGatherThreads = 256;
+constexpr int kGatherCols = 512;                     // columns of a block: 8 per lane
+constexpr int kGatherStride = kGatherCols + 8;       // LDS row stride (elements): rows start on different banks
+
+template <int GP>
+__global__ void __launch_bounds__(kGatherThreads) prefill_gather_kernel(const uint16_t* __restrict__ x, int d,
+                                                                        int E, const int32_t* __restrict__ offsets,
+                                                                        const int32_t* __restrict__ pair_token,
+                                                                        PrefillTables tb, uint16_t* __restrict__ xt,
+                                                                        float* __restrict__ xsum) {
+  static_assert(kPfFragRows * kGatherStride * 2 <= 64 * 1024, "gather tile");
+  __shared__ __attribute__((aligned(16))) uint16_t tile[kPfFragRows * kGatherStride];
   const int f = blockIdx.x;
   if (f >= tb.ftile_base[E]) return;
   const int e = tb.ftile_e[f];
@@ -71,26 +83,42 @@ __global__ void __launch_bounds__(256) prefill_gather_kernel(const uint16_t* __r
   expert_range_offsets(offsets, e, tb.P, ebase, ecount);
   const int pos0 = ebase + (f - tb.ftile_base[e]) * kPfFragRows;
   const int pend = ebase + ecount;
-  const int ng = d / G;
-  unsigned char* out = reinterpret_cast<unsigned char*>(xt);
-  for (int idx = threadIdx.x; idx < kPfFragRows * ng; idx += blockDim.x) {
-    const int m = idx % kPfFragRows, gi = idx / kPfFragRows;
-    const int pos = pos0 + m;
-    const bool valid = pos < pend;
-    const u32x4* src =
-        valid ? reinterpret_cast<const u32x4*>(x + (size_t)clamp_token(pair_token[pos], tb.T) * d + G * gi) : nullptr;
-    float sum = 0.0f;
-    for (int q = 0; q < G / 8; ++q) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (valid) {
-        v = src[q];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int kRowsPerWave = kPfFragRows / (kGatherThreads / 64);
+  // this wave's rows: m = wave + 4 j; token rows (or none: zero rows)
+  const uint16_t* src[kRowsPerWave];
 #pragma unroll
-        for (int w = 0; w < 4; ++w)
-          sum += bf16_bits_to_float(v[w] & 0xffffu) + bf16_bits_to_float(v[w] >> 16);
-      }
-      *reinterpret_cast<u32x4*>(out + frag_offset(f, m, G * gi + 8 * q, d)) = v;
+  for (int j = 0; j < kRowsPerWave; ++j) {
+    const int pos = pos0 + wave + 4 * j;
+    src[j] = pos < pend ? x + (size_t)clamp_token(pair_token[pos], tb.T) * d : nullptr;
+  }
+  const int ng = d / (8 * GP);
+  unsigned char* out = reinterpret_cast<unsigned char*>(xt) + frag_offset(f, 0, 0, d);
+  for (int c0 = 0; c0 < d; c0 += kGatherCols) {
+    const int w = (d - c0) < kGatherCols ? (d - c0) : kGatherCols;   // a multiple of 128
+    const bool on = 8 * lane < w;
+    u32x4 v[kRowsPerWave];
+#pragma unroll
+    for (int j = 0; j < kRowsPerWave; ++j) {
+      v[j] = u32x4{0u, 0u, 0u, 0u};
+      if (on && src[j]) v[j] = *reinterpret_cast<const u32x4*>(src[j] + c0 + 8 * lane);
     }
-    xsum[((size_t)f * ng + gi) * 32 + m] = sum;
+    if (c0 > 0) __syncthreads();   // the previous block's tile has been written out
+#pragma unroll
+    for (int j = 0; j < kRowsPerWave; ++j) {
+      const int m = wave + 4 * j;
+      if (on) *reinterpret_cast<u32x4*>(tile + m * kGatherStride + 8 * lane) = v[j];
+      const float sum = lane_group_sum<GP>(sum8<false>(v[j]));
+      if (on && lane % GP == 0) xsum[((size_t)f * ng + (c0 + 8 * lane) / (8 * GP)) * 32 + m] = sum;
+    }
+    __syncthreads();
+    // fragment fi of the block, piece mm: row mm % 32, columns 16 fi + 8 (mm / 32)
+    const int pieces = (w / 16) * 64;
+    for (int p = threadIdx.x; p < pieces; p += kGatherThreads) {
+      const int fi = p >> 6, mm = p & 63;
+      *reinterpret_cast<u32x4*>(out + ((size_t)(c0 / 16 + fi) * 64 + mm) * 16) =
+          *reinterpret_cast<const u32x4*>(tile + (mm & 31) * kGatherStride + 16 * fi + 8 * (mm >> 5));
+    }
   }
 }
 
@@ -150,8 +178,15 @@ hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routin
 
   timing_begin(stream, kSitePrefillPrep);
   hipLaunchKernelGGL(prefill_setup_kernel, dim3(1), dim3(256), 0, stream, r.counts, r.E, tb);
-  hipLaunchKernelGGL(prefill_gather_kernel, dim3(pl.f_max), dim3(256), 0, stream, x, L.d, L.G, r.E,
-                     r.offsets, r.pair_token, tb, xt, xsum);
+  if (L.G == 128)
+    hipLaunchKernelGGL(prefill_gather_kernel<16>, dim3(pl.f_max), dim3(kGatherThreads), 0, stream, x, L.d, r.E,
+                       r.offsets, r.pair_token, tb, xt, xsum);
+  else if (L.G == 64)
+    hipLaunchKernelGGL(prefill_gather_kernel<8>, dim3(pl.f_max), dim3(kGatherThreads), 0, stream, x, L.d, r.E,
+                       r.offsets, r.pair_token, tb, xt, xsum);
+  else
+    hipLaunchKernelGGL(prefill_gather_kernel<4>, dim3(pl.f_max), dim3(kGatherThreads), 0, stream, x, L.d, r.E,
+                       r.offsets, r.pair_token, tb, xt, xsum);
   timing_end(stream, kSitePrefillPrep);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
