@@ -12,53 +12,17 @@ extern template hipError_t launch_prefill_gemm<2>(const LayerArgs&, const int32_
 extern template hipError_t launch_prefill_gemm<4>(const LayerArgs&, const int32_t*, const PrefillTables&,
                                                   const PrefillGemm&, bool, hipStream_t);
 
-// One workgroup: per expert e (thread e), fragment rows ceil(M_e/32) and
-// m-tiles of PfCfg::kTokens tokens, exclusive scans, and the tables.
-// Counts outside [0, P] are taken as 0, and tables that would not fit their
-// capacity are left empty (no m-tiles), so inconsistent routing cannot make
-// any later access leave its buffer.
-__global__ void __launch_bounds__(256) prefill_setup_kernel(const int32_t* __restrict__ counts, int E,
-                                                            PrefillTables tb) {
-  __shared__ int snf[256], snm[256];
-  const int t = threadIdx.x;
-  const int c = t < E ? checked_count(counts[t], tb.P) : 0;
-  const int nf = (c + kPfFragRows - 1) / kPfFragRows;
-  const int nm = (c + PfCfg::kTokens - 1) / PfCfg::kTokens;
-  snf[t] = nf;
-  snm[t] = nm;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    const int a = t >= off ? snf[t - off] : 0;
-    const int b = t >= off ? snm[t - off] : 0;
-    __syncthreads();
-    snf[t] += a;
-    snm[t] += b;
-    __syncthreads();
-  }
-  const int fb = snf[t] - nf, mb = snm[t] - nm;
-  const bool fits = snf[255] <= tb.f_max && snm[255] <= tb.mt_max;
-  if (!fits) {
-    for (int i = t; i <= E; i += blockDim.x) tb.ftile_base[i] = 0;
-    if (t == 255) *tb.mt_count = 0;
-    return;
-  }
-  if (t < E) {
-    tb.ftile_base[t] = fb;
-    for (int i = 0; i < nf; ++i) tb.ftile_e[fb + i] = t;
-    for (int i = 0; i < nm; ++i) {
-      tb.mt_e[mb + i] = t;
-      tb.mt_j[mb + i] = i;
-    }
-  }
-  if (t == 255) {
-    tb.ftile_base[E] = snf[255];
-    *tb.mt_count = snm[255];
-  }
-}
-
-// One workgroup per fragment row f: its 32 routed rows of x (zero past the
-// expert's count) copied into the fragment layout (bf16, unchanged), and the
-// sum of each group of G columns of each row in fp32.  Column blocks of 512:
+// The prefill's preparation, one workgroup per fragment row f (f_max of
+// them).  Every workgroup first scans the expert counts itself (thread e:
+// fragment rows ceil(M_e/32) and m-tiles of PfCfg::kTokens tokens; wave
+// prefix sums), which gives the expert that f belongs to; workgroup 0 also
+// writes the tables the GEMMs read.  Counts outside [0, P] are taken as 0,
+// and tables that would not fit their capacity are left empty (no m-tiles,
+// no fragment rows), so inconsistent routing cannot make any later access
+// leave its buffer.
+// Then f's 32 routed rows of x (zero past the expert's count) are copied
+// into the fragment layout (bf16, unchanged), with the sum of each group of G
+// columns of each row in fp32.  Column blocks of 512:
 // each wave reads whole rows of the block (64 lanes x 16 consecutive bytes)
 // into a row-major LDS tile and forms the group sums of its pieces (the GP =
 // G/8 lanes of a group add with the DPP butterfly of the decode slabs); then
@@ -69,21 +33,76 @@ constexpr int kGatherCols = 512;                     // columns of a block: 8 pe
 constexpr int kGatherStride = kGatherCols + 8;       // LDS row stride (elements): rows start on different banks
 
 template <int GP>
-__global__ void __launch_bounds__(kGatherThreads) prefill_gather_kernel(const uint16_t* __restrict__ x, int d,
-                                                                        int E, const int32_t* __restrict__ offsets,
-                                                                        const int32_t* __restrict__ pair_token,
-                                                                        PrefillTables tb, uint16_t* __restrict__ xt,
-                                                                        float* __restrict__ xsum) {
+__global__ void __launch_bounds__(kGatherThreads) prefill_prep_kernel(const uint16_t* __restrict__ x, int d, int E,
+                                                                      const int32_t* __restrict__ counts,
+                                                                      const int32_t* __restrict__ offsets,
+                                                                      const int32_t* __restrict__ pair_token,
+                                                                      PrefillTables tb, uint16_t* __restrict__ xt,
+                                                                      float* __restrict__ xsum) {
   static_assert(kPfFragRows * kGatherStride * 2 <= 64 * 1024, "gather tile");
+  static_assert(kGatherThreads >= MC_MAX_EXPERTS, "a thread per expert");
+  constexpr int kWaves = kGatherThreads / 64;
   __shared__ __attribute__((aligned(16))) uint16_t tile[kPfFragRows * kGatherStride];
+  __shared__ int wf[kWaves], wm[kWaves], s_e, s_fb;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int f = blockIdx.x;
-  if (f >= tb.ftile_base[E]) return;
-  const int e = tb.ftile_e[f];
+
+  // tables: exclusive prefix sums of the experts' fragment rows and m-tiles
+  const int c = tid < E ? checked_count(counts[tid], tb.P) : 0;
+  const int nf = (c + kPfFragRows - 1) / kPfFragRows;
+  const int nm = (c + PfCfg::kTokens - 1) / PfCfg::kTokens;
+  int sf = nf, sm = nm;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int a = __shfl_up(sf, off), b = __shfl_up(sm, off);
+    if (lane >= off) {
+      sf += a;
+      sm += b;
+    }
+  }
+  if (lane == 63) {
+    wf[wave] = sf;
+    wm[wave] = sm;
+  }
+  __syncthreads();
+  int tf = 0, tm = 0, fb = sf - nf, mb = sm - nm;
+  for (int w = 0; w < kWaves; ++w) {
+    if (w < wave) {
+      fb += wf[w];
+      mb += wm[w];
+    }
+    tf += wf[w];
+    tm += wm[w];
+  }
+  const bool fits = tf <= tb.f_max && tm <= tb.mt_max;
+  if (f == 0) {
+    if (!fits) {
+      for (int i = tid; i <= E; i += kGatherThreads) tb.ftile_base[i] = 0;
+      if (tid == 0) *tb.mt_count = 0;
+    } else {
+      if (tid < E) {
+        tb.ftile_base[tid] = fb;
+        for (int i = 0; i < nm; ++i) {
+          tb.mt_e[mb + i] = tid;
+          tb.mt_j[mb + i] = i;
+        }
+      }
+      if (tid == 0) {
+        tb.ftile_base[E] = tf;
+        *tb.mt_count = tm;
+      }
+    }
+  }
+  if (!fits || f >= tf) return;   // workgroup-uniform
+  if (tid < E && fb <= f && f < fb + nf) {   // exactly one expert holds f
+    s_e = tid;
+    s_fb = fb;
+  }
+  __syncthreads();
+  const int e = s_e;
   int ebase, ecount;
   expert_range_offsets(offsets, e, tb.P, ebase, ecount);
-  const int pos0 = ebase + (f - tb.ftile_base[e]) * kPfFragRows;
+  const int pos0 = ebase + (f - s_fb) * kPfFragRows;
   const int pend = ebase + ecount;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   constexpr int kRowsPerWave = kPfFragRows / (kGatherThreads / 64);
   // this wave's rows: m = wave + 4 j; token rows (or none: zero rows)
   const uint16_t* src[kRowsPerWave];
@@ -143,7 +162,7 @@ PrefillLayout prefill_layout(int T, int E, int k, int d, int ffn) {
   // the GEMMs stage whole m-tiles: kTiles - 1 padding fragment rows past the last one
   const size_t rows = (size_t)(pl.f_max + PfCfg::kTiles) * kPfFragRows;
   pl.tables = 0;
-  const size_t tab = (size_t)(E + 1 + pl.f_max + 2 * pl.mt_max + 1) * sizeof(int32_t);
+  const size_t tab = (size_t)(E + 1 + 2 * pl.mt_max + 1) * sizeof(int32_t);
   pl.x = round256(tab);
   pl.xsum = pl.x + round256(rows * d * sizeof(uint16_t));
   pl.h = pl.xsum + round256(rows * (d / 32) * sizeof(float));   // G >= 32
@@ -160,8 +179,7 @@ hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routin
   PrefillTables tb;
   int32_t* t = reinterpret_cast<int32_t*>(base + pl.tables);
   tb.ftile_base = t;
-  tb.ftile_e = t + (r.E + 1);
-  tb.mt_e = tb.ftile_e + pl.f_max;
+  tb.mt_e = t + (r.E + 1);
   tb.mt_j = tb.mt_e + pl.mt_max;
   tb.mt_count = tb.mt_j + pl.mt_max;
   tb.f_max = pl.f_max;
@@ -177,16 +195,15 @@ hipError_t launch_prefill(const uint16_t* x, const LayerArgs& L, const mc_routin
   *nsplit = pl.nsplit;
 
   timing_begin(stream, kSitePrefillPrep);
-  hipLaunchKernelGGL(prefill_setup_kernel, dim3(1), dim3(256), 0, stream, r.counts, r.E, tb);
   if (L.G == 128)
-    hipLaunchKernelGGL(prefill_gather_kernel<16>, dim3(pl.f_max), dim3(kGatherThreads), 0, stream, x, L.d, r.E,
-                       r.offsets, r.pair_token, tb, xt, xsum);
+    hipLaunchKernelGGL(prefill_prep_kernel<16>, dim3(pl.f_max), dim3(kGatherThreads), 0, stream, x, L.d, r.E,
+                       r.counts, r.offsets, r.pair_token, tb, xt, xsum);
   else if (L.G == 64)
-    hipLaunchKernelGGL(prefill_gather_kernel<8>, dim3(pl.f_max), dim3(kGatherThreads), 0, stream, x, L.d, r.E,
-                       r.offsets, r.pair_token, tb, xt, xsum);
+    hipLaunchKernelGGL(prefill_prep_kernel<8>, dim3(pl.f_max), dim3(kGatherThreads), 0, stream, x, L.d, r.E,
+                       r.counts, r.offsets, r.pair_token, tb, xt, xsum);
   else
-    hipLaunchKernelGGL(prefill_gather_kernel<4>, dim3(pl.f_max), dim3(kGatherThreads), 0, stream, x, L.d, r.E,
-                       r.offsets, r.pair_token, tb, xt, xsum);
+    hipLaunchKernelGGL(prefill_prep_kernel<4>, dim3(pl.f_max), dim3(kGatherThreads), 0, stream, x, L.d, r.E,
+                       r.counts, r.offsets, r.pair_token, tb, xt, xsum);
   timing_end(stream, kSitePrefillPrep);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;

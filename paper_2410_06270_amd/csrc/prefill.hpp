@@ -69,7 +69,6 @@ struct PfCfg {
 // Expert-to-tile tables written by the set-up kernel into the workspace.
 struct PrefillTables {
   int32_t* ftile_base;   // [E+1] first fragment row of each expert
-  int32_t* ftile_e;      // [f_max] expert of each fragment row
   int32_t* mt_e;         // [mt_max] expert of each m-tile
   int32_t* mt_j;         // [mt_max] m-tile index within its expert
   int32_t* mt_count;     // [1] m-tiles in use
