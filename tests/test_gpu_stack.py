@@ -161,6 +161,27 @@ def test_stack_many_layers_equals_chain(mc, small_stack, T, n):
         assert torch.equal(getattr(r, name)[:P], getattr(ref, name)[:P]), name
 
 
+@pytest.mark.parametrize("T", [8, 130])
+def test_stack_without_flags_equals_zero_flags(mc, small_stack, T):
+    """important = NULL means no protected token: 10 layers (two routing
+    launches for small batches) give the same bits as all-zero flags."""
+    E, d, ffn, k = SMALL["E"], SMALL["d"], SMALL["ffn"], SMALL["k"]
+    n = 10
+    x = to_dev(synthetic.activations(1, T, d=d).view(np.int16))
+    lgs = to_dev(np.stack([synthetic.stack_logits(5, l, T, E=E) for l in range(n)]))
+    Ls = [small_stack[l % 4][2] for l in range(n)]
+    outs = []
+    for flags in (None, to_dev(np.zeros((n, T), np.uint8))):
+        r = mc.Routing(T, E, k)
+        y = torch.empty((T, d), dtype=torch.int16, device="cuda")
+        tmp = torch.empty((T, d), dtype=torch.int16, device="cuda")
+        ws = torch.empty(mc.stack_workspace(T, E, k, d, ffn), dtype=torch.uint8, device="cuda")
+        mc.stack_forward(x, Ls, lgs, flags, TAU, r, y, tmp, ws)
+        torch.cuda.synchronize()
+        outs.append(y.cpu().numpy())
+    np.testing.assert_array_equal(outs[0], outs[1])
+
+
 def test_stack_rejects_aliased_buffers(mc, small_stack):
     E, d, ffn, k = SMALL["E"], SMALL["d"], SMALL["ffn"], SMALL["k"]
     T = 4
