@@ -1,6 +1,7 @@
-// prefill.hip -- set-up of the prefill grouped GEMMs (expert tile tables and
-// the fp16 fragment-tiled copy of the routed token rows) and their launcher.
-// The GEMM kernels are in prefill.hpp, one file per group size.
+// prefill.hip -- preparation of the prefill grouped GEMMs (expert tile tables
+// and the bf16 fragment-tiled copy of the routed token rows, in one launch)
+// and their launcher.  The GEMM kernels are in prefill.hpp, one file per
+// group size.
 #include "prefill.hpp"
 
 namespace mc {
