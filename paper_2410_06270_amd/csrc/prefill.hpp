@@ -66,7 +66,8 @@ struct PfCfg {
                 "the exchanged totals and the h tile fit the ring");
 };
 
-// Expert-to-tile tables written by the set-up kernel into the workspace.
+// Expert-to-tile tables, written into the workspace by workgroup 0 of the
+// preparation launch (prefill_prep_kernel).
 struct PrefillTables {
   int32_t* ftile_base;   // [E+1] first fragment row of each expert
   int32_t* mt_e;         // [mt_max] expert of each m-tile
